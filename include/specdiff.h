@@ -1,0 +1,216 @@
+/*
+ * specdiff.h — C ABI of the MI355X (gfx950) speculative-diffusion library.
+ *
+ * The library implements the parallel verification pass of speculative
+ * diffusion sampling with block verification ("Accelerating Speculative
+ * Diffusions via Block Verification"), driven by the paper's Free Drafter,
+ * with a closed-form Gaussian-mixture target.
+ *
+ * Conventions for every entry point:
+ *  - Pointers are DEVICE pointers unless the comment says "host".
+ *  - Arrays are row-major float32 unless stated.  A [B][rows][d] view is given
+ *    by a base pointer and an sd_stride in ELEMENTS (chain stride, row stride);
+ *    the d elements of a row are contiguous.
+ *  - The caller owns all memory.  The library allocates device memory only in
+ *    sd_target_create (freed by sd_target_destroy); everything else lives in
+ *    caller buffers, including a caller workspace sized by the *_workspace query.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
+ *    null stream).  Only sd_run_sampler reads results back (a 4-byte counter per
+ *    round and its statistics).
+ *  - Arguments are validated before any HIP call: a bad argument returns
+ *    SD_EINVAL, a HIP failure SD_EHIP; sd_last_error() then describes it (a
+ *    thread-local string).  Outputs are undefined after an error.
+ *  - Randomness: every draw comes from Philox4x32-10 keyed by `seed`, counter
+ *    (c0, chain, round, tag<<24 | slot) with tags 1 INIT, 2 DRAFT (slot = draft
+ *    step), 3 COIN, 4 USAMPLE, 5 RESID, 6 TARGET; uniform = ((w>>8)+0.5)*2^-24,
+ *    normals by Box-Muller on word pairs; element e of a vector uses c0 = e>>2.
+ *  - Notation: N steps, draft block K (<= SD_MAX_BLOCK), K_b = min(K, N - k)
+ *    valid draft rows of a chain at step k.
+ *  - Entry points are reentrant; an sd_target is immutable and may be shared
+ *    by concurrent streams.
+ */
+#ifndef SPECDIFF_H
+#define SPECDIFF_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define SD_ABI_VERSION 1
+#define SD_MAX_BLOCK 64
+
+typedef enum {
+  SD_OK = 0,
+  SD_EINVAL = -1,       /* invalid argument (checked before any HIP call)    */
+  SD_EHIP = -2,         /* a HIP runtime call failed                          */
+  SD_EUNSUPPORTED = -3, /* valid but not supported by this build              */
+  SD_ENOMEM = -4,       /* device allocation failed (sd_target_create only)   */
+  SD_ENUMERIC = -5      /* a non-finite value was met (sd_run_sampler)        */
+} sd_status;
+
+typedef enum { SD_BLOCK = 0, SD_TOKEN = 1 } sd_verify_mode;           /* Alg. 6 / Alg. 2 */
+typedef enum { SD_FP32 = 0, SD_BF16 = 1 } sd_precision;               /* denoiser GEMMs  */
+typedef enum { SD_USAMPLE_EXACT = 0, SD_USAMPLE_PAPER = 1 } sd_usample_mode; /* Alg. 7 */
+
+/* VP-SDE Euler-Maruyama chain (Sec. 2): beta(s) = beta_min + s (beta_max - beta_min),
+ * t_n = n/N; m^q_n(y) = c1_n y + c2_n score(y), c1_n = 1 + beta_n/(2N),
+ * c2_n = (1 + churn^2) beta_n/(2N), sigma_n = churn sqrt(beta_n/N), beta_n = beta(1 - n/N).
+ * Requires n_steps >= 1, 0 < beta_min <= beta_max, churn > 0 (the paper requires eps > 0). */
+typedef struct {
+  int32_t n_steps;
+  double beta_min, beta_max, churn;
+} sd_schedule;
+
+typedef struct {
+  int64_t chain, row; /* element strides of a [B][rows][d] view */
+} sd_stride;
+
+typedef void* sd_stream;                /* hipStream_t */
+typedef struct sd_target_s* sd_target;  /* opaque Gaussian-mixture target */
+
+int32_t sd_abi_version(void);
+const char* sd_last_error(void);
+
+/* Host table of the schedule for n = 0..N (host out[4][N+1]): rows are the
+ * signal level a_n = sqrt(abar(1 - t_n)), sigma_n, c1_n, c2_n (Sec. 2,
+ * eq. target-distribution). */
+sd_status sd_schedule_table(const sd_schedule* sched, double* host_out);
+
+/* ---------------------------------------------------------------- target --
+ * Closed-form Gaussian-mixture target q_data = sum_m w_m N(mu_m, var_m I):
+ * q_s = sum_m w_m N(a mu_m, (a^2 var_m + 1 - a^2) I) and its score, and the EM
+ * mean m^q_n(x) = c1_n x + c2_n score (eq. target-distribution).
+ * mu [M][d], var [M], log_w [M] are HOST arrays copied at creation.
+ * d >= 1, 1 <= n_comp <= 4096.  precision selects the GEMM operand type. */
+sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp,
+                           const float* mu, const float* var, const float* log_w,
+                           sd_precision precision, sd_target* out);
+sd_status sd_target_destroy(sd_target target);
+/* Workspace bytes sd_target_mean needs for `rows` rows. */
+size_t sd_target_mean_workspace(sd_target target, int32_t rows);
+/* For each row r: mq[r] = m^q_{step[r]}(x[r]) and, if score != NULL, score[r] =
+ * s_{1 - t_step}(x[r]).  x, mq, score are [rows][d] with the given row strides
+ * (>= d); step [rows] int32 in [0, N-1].  Rows are independent ("in parallel",
+ * Alg. 1).  ws: device workspace of >= sd_target_mean_workspace bytes. */
+sd_status sd_target_mean(sd_target target, int32_t rows, const float* x, int64_t x_row_stride,
+                         const int32_t* step, float* mq, int64_t mq_row_stride,
+                         float* score, int64_t score_row_stride, void* ws, size_t ws_bytes,
+                         sd_stream stream);
+
+/* ----------------------------------------------------------------- draft --
+ * Y_0 ~ N(0, I) for B chains (Alg. 8, first line): y [B][d], INIT stream,
+ * round 0. */
+sd_status sd_init_chains(int32_t B, int32_t d, uint64_t seed, float* y, sd_stream stream);
+
+/* Free Drafter block (Sec. 3.3, eq. frozen-draft-drift with the cached score):
+ * for chain b at step k[b] (< N) with K_b = min(K, N - k), yhat_0 = y[b] and for
+ * i = 1..K_b, n = k + i - 1:
+ *   m^p_{i-1} = c1_n yhat_{i-1} + c2_n cache_score[b],  yhat_i = m^p_{i-1} + sigma_n xi_i
+ * (xi_i: DRAFT stream, slot i, round round[b]).  Writes x rows 0..K (row 0 = y[b],
+ * rows K_b+1..K repeat yhat_{K_b}) and mp rows 0..K-1 (rows >= K_b repeat the last
+ * mean).  Chains with k[b] >= N are left untouched.
+ * y, cache_score: [B][d] contiguous; x: [B][K+1][d] view; mp: [B][K][d] view. */
+sd_status sd_draft_block(const sd_schedule* sched, int32_t B, int32_t K, int32_t d,
+                         const float* y, const float* cache_score, const int32_t* k,
+                         const uint32_t* round, uint64_t seed, float* x, sd_stride xs, float* mp,
+                         sd_stride mps, sd_stream stream);
+
+/* ---------------------------------------------------------------- verify --
+ * Verification of B drafted blocks (Alg. 6 block / Alg. 2 token, with the
+ * log-space ratios of App. A.2).  For chain b and j = 1..K_b (kb[b] in [0, K];
+ * 0 = inactive chain):
+ *   Delta_j = (mp_{j-1} - mq_{j-1}) / sigma_{j-1},  Z_j = (y_draft_{j-1} - mp_{j-1}) / sigma_{j-1},
+ *   log_ratio[b][j-1] = -Z_j.Delta_j - ||Delta_j||^2/2,  delta_norm[b][j-1] = ||Delta_j||
+ * (reductions over d accumulated in float64), then the acceptance scan:
+ *   block: log alpha_j = min(0, log alpha_{j-1} + ell_j), h_j = v_j/(v_j + 1 - alpha_j)
+ *          (h_{K_b} = alpha_{K_b}), coins eta_j < h_j, tau = 1 + max{j : c_j = 1},
+ *          log_alpha_res = log alpha_{tau-1};
+ *   token: coins eta_j < min(1, e^{ell_j}), tau = first rejected j (K_b + 1 if none),
+ *          log_alpha_res = 0.
+ * When tau <= K_b it also draws U ~ psi_{alpha_res} for ||Delta_tau|| by Alg. 7
+ * (u_res[b]; NaN otherwise).  eta_j = uniform j-1 of (b, round[b], COIN); the
+ * U-sample uniform is uniform 0 of (b, round[b], USAMPLE).
+ * Inputs: y_draft [B][K][d] view (yhat_{k+1..}), mp [B][K][d] view (m^p_{k..}),
+ * mq [B][>=K][d] view (m^q_{k..}), sigma [B][K+1] float64 (sigma_{k..k+K}),
+ * kb [B] (values above K are clamped to K), round [B].  Outputs: tau [B] int32
+ * (0 for inactive chains),
+ * log_alpha_res [B], u_res [B], delta_norm [B][K], log_ratio [B][K] (float64),
+ * coins [B] bitmask of c_1..c_K (nullable).  No workspace. */
+sd_status sd_verify_block(int32_t B, int32_t K, int32_t d, sd_verify_mode mode,
+                          const float* y_draft, sd_stride ys, const float* mp, sd_stride mps,
+                          const float* mq, sd_stride mqs, const double* sigma, const int32_t* kb,
+                          const uint32_t* round, uint64_t seed, sd_usample_mode usample_mode,
+                          int32_t* tau, double* log_alpha_res, double* u_res, double* delta_norm,
+                          double* log_ratio, uint64_t* coins, sd_stream stream);
+
+/* -------------------------------------------------------------- residual --
+ * The new state Y_{k+tau} of each chain (Alg. 8, residual calculation):
+ *  - tau <= K_b: Decomposition residual (Prop. 1, Alg. 5) with alpha = alpha_res:
+ *      e = Delta_tau/||Delta_tau||, G ~ N(0, I) (RESID stream),
+ *      y = mq_{tau-1} + sigma_{tau-1} (U e + G - e (e.G)),  U = u_res[b];
+ *  - tau = K_b + 1 <= steps_left[b]: y = mq_{K_b} + sigma_{K_b} xi (TARGET stream);
+ *  - tau = K_b + 1 >  steps_left[b]: y = y_draft_{K_b - 1} (the last draft is Y_N).
+ * steps_left[b] = N - k[b] >= K_b; chains with tau[b] <= 0 are skipped.
+ * delta_norm [B][K] as produced by sd_verify_block; mq is a [B][K+1][d] view
+ * (row K_b feeds the full-accept draw).  kb is clamped to K and chains with
+ * tau outside [1, K_b + 1] are skipped.  y_out [B][d] contiguous. */
+sd_status sd_sample_residual(int32_t B, int32_t K, int32_t d, const float* y_draft, sd_stride ys,
+                             const float* mp, sd_stride mps, const float* mq, sd_stride mqs,
+                             const double* sigma, const int32_t* kb, const int32_t* steps_left,
+                             const int32_t* tau, const double* u_res, const double* delta_norm,
+                             const uint32_t* round, uint64_t seed, float* y_out,
+                             sd_stream stream);
+
+/* --------------------------------------------------------------- sampler --
+ * The full speculative sampler (Alg. 8) with the Free Drafter: Y_0 ~ N(0, I),
+ * one explicit target call at Y_0 to seed the cached score, then rounds of
+ * draft -> target means on all min(K_b+1, N-k) rows -> verify -> residual ->
+ * commit until every chain has reached step N.  Chains run in lockstep rounds,
+ * each with its own step k and round counter.  Returns Y_N in y_out [B][d].
+ * tau_trace (nullable): [trace_rounds][B] int32, tau of each chain per round
+ * (0 once a chain has finished).  stats (host, nullable): rounds, chain-rounds,
+ * steps and the tau histogram.  ws: >= sd_sampler_workspace bytes.
+ * Returns SD_ENUMERIC if a non-finite log-ratio was met. */
+typedef struct {
+  int64_t rounds;       /* lockstep rounds launched until all chains finished */
+  int64_t chain_rounds; /* sum over chains of rounds in which the chain was active */
+  int64_t steps;        /* sum over chains of steps advanced (= B * N)          */
+  int64_t tau_hist[SD_MAX_BLOCK + 2]; /* tau_hist[t] = number of chain-rounds with tau = t */
+} sd_stats;
+
+size_t sd_sampler_workspace(sd_target target, int32_t B, int32_t K);
+sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode mode,
+                         sd_usample_mode usample_mode, uint64_t seed, float* y_out,
+                         int32_t* tau_trace, int32_t trace_rounds, sd_stats* stats, void* ws,
+                         size_t ws_bytes, sd_stream stream);
+
+/* ------------------------------------------------------------- profiling --
+ * Per-kernel timing with HIP events recorded around every launch on the
+ * launch's own stream.  sd_profile_enable(1) clears and starts collection,
+ * (0) stops it.  sd_profile_read waits for the recorded events and returns up
+ * to `capacity` entries (host out), *count = number of kernels seen. */
+typedef struct {
+  char name[48];
+  int64_t launches;
+  double total_ms;
+} sd_kernel_stat;
+
+sd_status sd_profile_enable(int32_t on);
+sd_status sd_profile_read(sd_kernel_stat* out, int32_t capacity, int32_t* count);
+
+/* ----------------------------------------------------------- test hooks --
+ * Raw Philox4x32-10 outputs for n counters (device [n][4] uint32 in/out) with
+ * key = seed, and the float32 normals of one (chain, round, tag, slot) stream
+ * (device out [d]).  Used to check the generator against its definition. */
+sd_status sd_philox_words(uint64_t seed, int32_t n, const uint32_t* counters, uint32_t* out,
+                          sd_stream stream);
+sd_status sd_philox_normals(uint64_t seed, uint32_t chain, uint32_t round, uint32_t tag,
+                            uint32_t slot, int32_t d, float* out, sd_stream stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* SPECDIFF_H */

@@ -1,0 +1,118 @@
+// Internal declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "specdiff.h"
+
+namespace sd {
+
+// Thread-local error message behind sd_last_error().
+void set_error(const char* fmt, ...);
+
+// ------------------------------------------------------------- profiling --
+bool prof_on();
+void prof_push(const char* name, hipEvent_t start, hipEvent_t stop);
+void prof_events(hipEvent_t* start, hipEvent_t* stop);
+
+// Enqueue one kernel launch through `launch`; when profiling is on, bracket it
+// with events on the same stream.  Returns the launch error, if any.
+template <class F>
+hipError_t timed(const char* name, hipStream_t s, F&& launch) {
+  if (!prof_on()) {
+    launch();
+    return hipGetLastError();
+  }
+  hipEvent_t a, b;
+  prof_events(&a, &b);
+  (void)hipEventRecord(a, s);
+  launch();
+  hipError_t e = hipGetLastError();
+  (void)hipEventRecord(b, s);
+  prof_push(name, a, b);
+  return e;
+}
+
+// ------------------------------------------------------------- schedule --
+struct Sched {
+  int N;
+  double bmin, bmax, eps;
+};
+
+__host__ __device__ inline double sched_beta(const Sched& s, int n) {
+  const double fwd = 1.0 - (double)n / (double)s.N;
+  return s.bmin + fwd * (s.bmax - s.bmin);
+}
+__host__ __device__ inline double sched_sigma(const Sched& s, int n) {
+  return s.eps * sqrt(sched_beta(s, n) / (double)s.N);
+}
+__host__ __device__ inline double sched_c1(const Sched& s, int n) {
+  return 1.0 + 0.5 * sched_beta(s, n) / (double)s.N;
+}
+__host__ __device__ inline double sched_c2(const Sched& s, int n) {
+  return 0.5 * (1.0 + s.eps * s.eps) * sched_beta(s, n) / (double)s.N;
+}
+__host__ __device__ inline double sched_signal(const Sched& s, int n) {
+  const double fwd = 1.0 - (double)n / (double)s.N;
+  return sqrt(exp(-(s.bmin * fwd + 0.5 * (s.bmax - s.bmin) * fwd * fwd)));
+}
+
+inline Sched to_sched(const sd_schedule* p) {
+  return Sched{p->n_steps, p->beta_min, p->beta_max, p->churn};
+}
+
+// ------------------------------------------------------- target internals --
+struct Target {
+  Sched sc;
+  int d, M;
+  sd_precision prec;
+  float* mu;      // [M][d]
+  float* muT;     // [d][M]
+  double* var;    // [M]
+  double* logw;   // [M]
+  double* musq;   // [M] ||mu_m||^2 (float64 from the float32 means)
+  int device;
+};
+
+size_t target_ws_bytes(const Target& t, int rows);
+// Rows' EM means (and scores if score != nullptr).  gate: nullable device flag;
+// when it reads 0 every kernel exits at once (finished sampler rounds).
+hipError_t target_mean_launch(const Target& t, int rows, const float* x, int64_t ldx,
+                              const int32_t* step, float* mq, int64_t ldq, float* score,
+                              int64_t lds, void* ws, hipStream_t s, const int* gate);
+
+// ---------------------------------------------------------------- kernels --
+hipError_t init_chains_launch(int B, int d, uint64_t seed, float* y, hipStream_t s);
+hipError_t draft_launch(const Sched& sc, int B, int K, int d, const float* y, const float* cs,
+                        const int32_t* k, const uint32_t* rnd, uint64_t seed, float* x,
+                        sd_stride xs, float* mp, sd_stride mps, hipStream_t s, const int* gate);
+hipError_t verify_launch(int B, int K, int d, int mode, const float* yd, sd_stride ys,
+                         const float* mp, sd_stride mps, const float* mq, sd_stride mqs,
+                         const double* sigma, const int32_t* kb, const uint32_t* rnd,
+                         uint64_t seed, int umode, int32_t* tau, double* lar, double* ures,
+                         double* dn, double* lr, uint64_t* coins, int* nanflag, hipStream_t s,
+                         const int* gate);
+hipError_t residual_launch(int B, int K, int d, const float* yd, sd_stride ys, const float* mp,
+                           sd_stride mps, const float* mq, sd_stride mqs, const double* sigma,
+                           const int32_t* kb, const int32_t* left, const int32_t* tau,
+                           const double* ures, const double* dn, const uint32_t* rnd,
+                           uint64_t seed, float* y, hipStream_t s, const int* gate);
+// Sampler-only kernels.
+hipError_t fill_i32_launch(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+hipError_t fill_i64_launch(int64_t* p, int64_t n, int64_t v, hipStream_t s);
+hipError_t prepare_launch(const Sched& sc, int B, int K, const int32_t* k, int32_t* kb,
+                          int32_t* left, int32_t* step, double* sigma, int* cnt_zero,
+                          hipStream_t s, const int* gate);
+hipError_t commit_launch(int B, int K, int d, int N, const int32_t* tau, const int32_t* kb,
+                         int32_t* k, uint32_t* rnd, const float* score, sd_stride ss,
+                         float* cache, int* cnt, int64_t* hist, int64_t* steps, int32_t* trace,
+                         int r, int trace_rounds, hipStream_t s, const int* gate);
+hipError_t philox_words_launch(uint64_t seed, int n, const uint32_t* ctr, uint32_t* out,
+                               hipStream_t s);
+hipError_t philox_normals_launch(uint64_t seed, uint32_t chain, uint32_t rnd, uint32_t tag,
+                                 uint32_t slot, int d, float* out, hipStream_t s);
+
+inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+}  // namespace sd

@@ -1,0 +1,252 @@
+// Verification of drafted blocks: log density ratios (App. A.2) reduced over
+// d, then the block (Alg. 6) or token (Alg. 2) acceptance scan and the U draw
+// of Alg. 7.
+//
+// logratio_kernel: one workgroup per (chain, draft row).  The three float32
+// rows (draft, draft mean, target mean) are streamed once with 16-byte
+// non-temporal loads; differences and products are formed in float64 and
+// accumulated in float64, then reduced across the wavefront with shuffles and
+// across the four wavefronts through LDS.  Pure HBM streaming: 12 B per element.
+//
+// scan_kernel: one wavefront per chain, lane j-1 owns draft step j (K <= 64).
+// Every lane replays the prefix recursion log alpha_j = min(0, log alpha_{j-1}
+// + ell_j) in the same order as the definition, evaluates its h_j, draws its
+// coin, and a ballot gives tau.  U is found by inverting Psi_alpha: the
+// doubling of Alg. 7 is done for all 64 candidate lower ends at once (lane i
+// tests u* - 2^i), and the bisection becomes a 64-way multisection that
+// shrinks the bracket 65-fold per step until it collapses in float64.
+#include "common.hpp"
+#include "dmath.hpp"
+#include "philox.hpp"
+
+namespace sd {
+namespace {
+
+constexpr int kThreads = 256;
+typedef float f4v __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
+  return v;
+}
+
+__global__ __launch_bounds__(kThreads) void logratio_kernel(
+    int K, int d, const float* __restrict__ yd, int64_t yc, int64_t yr,
+    const float* __restrict__ mp, int64_t pc, int64_t pr, const float* __restrict__ mq,
+    int64_t qc, int64_t qr, const double* __restrict__ sigma, const int32_t* __restrict__ kb,
+    double* __restrict__ dn, double* __restrict__ lr, bool vec, const int* gate) {
+  if (gate && *gate == 0) return;
+  const int row = blockIdx.x;
+  const int b = row / K, j = row - b * K;
+  if (j >= kb[b]) {
+    if (threadIdx.x == 0) {
+      dn[row] = 0.0;
+      lr[row] = 0.0;
+    }
+    return;
+  }
+  const float* py = yd + (int64_t)b * yc + (int64_t)j * yr;
+  const float* pp = mp + (int64_t)b * pc + (int64_t)j * pr;
+  const float* pq = mq + (int64_t)b * qc + (int64_t)j * qr;
+  double s2 = 0.0, sz = 0.0;
+  if (vec) {
+    const f4v* vy = reinterpret_cast<const f4v*>(py);
+    const f4v* vp = reinterpret_cast<const f4v*>(pp);
+    const f4v* vq = reinterpret_cast<const f4v*>(pq);
+    const int n4 = d >> 2;
+#pragma unroll 4
+    for (int i = threadIdx.x; i < n4; i += kThreads) {
+      const f4v a = __builtin_nontemporal_load(vy + i);
+      const f4v p = __builtin_nontemporal_load(vp + i);
+      const f4v q = __builtin_nontemporal_load(vq + i);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        const double dd = (double)p[c] - (double)q[c];
+        const double zz = (double)a[c] - (double)p[c];
+        s2 = fma(dd, dd, s2);
+        sz = fma(zz, dd, sz);
+      }
+    }
+  } else {
+    for (int i = threadIdx.x; i < d; i += kThreads) {
+      const double dd = (double)pp[i] - (double)pq[i];
+      const double zz = (double)py[i] - (double)pp[i];
+      s2 = fma(dd, dd, s2);
+      sz = fma(zz, dd, sz);
+    }
+  }
+  s2 = wave_sum(s2);
+  sz = wave_sum(sz);
+  __shared__ double red[2][kThreads / 64];
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  if (lane == 0) {
+    red[0][w] = s2;
+    red[1][w] = sz;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double t2 = 0.0, tz = 0.0;
+    for (int i = 0; i < kThreads / 64; ++i) {
+      t2 += red[0][i];
+      tz += red[1][i];
+    }
+    const double s = sigma[(int64_t)b * (K + 1) + j];
+    const double inv = 1.0 / (s * s);
+    dn[row] = sqrt(t2 * inv);
+    lr[row] = -tz * inv - 0.5 * t2 * inv;
+  }
+}
+
+// log Psi_alpha(x) given the log normaliser Lstar = log(alpha Phi(u*) - Phi(u* - v)).
+__device__ __forceinline__ double log_cdf(double x, double la, double v, double us,
+                                          double Lstar) {
+  if (x >= us) return 0.0;
+  return log_excess(x, la, v) - Lstar;
+}
+
+// Exact inverse of Psi_alpha at u, with all 64 lanes of the wavefront.
+__device__ double usample_exact(double u, double la, double v, int lane) {
+  const double us = la / v + 0.5 * v;
+  const double Lstar = log_excess(us, la, v);
+  const double logu = log(u);
+  // doubling of the bracket width: lane i tests the lower end u* - 2^i
+  const double cand = us - ldexp(1.0, lane);
+  const uint64_t above = __ballot(log_cdf(cand, la, v, us, Lstar) > logu);
+  const int p = (~above == 0ull) ? 63 : (__ffsll((unsigned long long)~above) - 1);
+  double lo = us - ldexp(1.0, p);
+  double hi = p == 0 ? us : us - ldexp(1.0, p - 1);
+  if (~above == 0ull) hi = us - ldexp(1.0, 62);
+  for (int it = 0; it < 64; ++it) {
+    const double mid = 0.5 * (lo + hi);
+    if (!(mid > lo && mid < hi)) break;
+    const double x = lo + (hi - lo) * ((double)(lane + 1) / 65.0);
+    const uint64_t below = __ballot(log_cdf(x, la, v, us, Lstar) < logu);
+    const int cnt = __popcll(below);
+    const double nlo = __shfl(x, cnt > 0 ? cnt - 1 : 0);
+    const double nhi = __shfl(x, cnt < 64 ? cnt : 63);
+    lo = cnt > 0 ? nlo : lo;
+    hi = cnt < 64 ? nhi : hi;
+  }
+  return 0.5 * (lo + hi);
+}
+
+// The capped doubling/bisection of the paper's experiments (3 + 4 steps).
+__device__ double usample_paper(double u, double la, double v) {
+  const double us = la / v + 0.5 * v;
+  const double Lstar = log_excess(us, la, v);
+  const double logu = log(u);
+  double hi = us, lo = us - 1.0;
+  for (int n = 0; n < 3 && log_cdf(lo, la, v, us, Lstar) > logu; ++n) lo = hi - 2.0 * (hi - lo);
+  double mid = 0.5 * (lo + hi);
+  for (int n = 0; n < 4; ++n) {
+    const double lc = log_cdf(mid, la, v, us, Lstar);
+    if (fabs(exp(lc) - u) <= 1e-6) break;
+    if (lc < logu)
+      lo = mid;
+    else
+      hi = mid;
+    mid = 0.5 * (lo + hi);
+  }
+  return mid;
+}
+
+__global__ __launch_bounds__(kThreads) void scan_kernel(
+    int B, int K, int mode, int umode, const double* __restrict__ dn,
+    const double* __restrict__ lr, const int32_t* __restrict__ kbv,
+    const uint32_t* __restrict__ rnd, uint64_t seed, int32_t* __restrict__ tau,
+    double* __restrict__ lar, double* __restrict__ ures, uint64_t* __restrict__ coins,
+    int* nanflag, const int* gate) {
+  if (gate && *gate == 0) return;
+  const int lane = threadIdx.x & 63;
+  const int b = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (b >= B) return;  // whole wavefront
+  const int kb = min(kbv[b], K);
+  if (kb <= 0) {
+    if (lane == 0) {
+      tau[b] = 0;
+      lar[b] = 0.0;
+      ures[b] = NAN;
+      if (coins) coins[b] = 0ull;
+    }
+    return;
+  }
+  const bool valid = lane < kb;
+  const double ell = valid ? lr[(int64_t)b * K + lane] : 0.0;
+  const double vn = valid ? dn[(int64_t)b * K + lane] : 0.0;
+  if (nanflag && __ballot(valid && !(isfinite(ell) && isfinite(vn))) != 0ull && lane == 0)
+    atomicOr(nanflag, 1);
+  // prefix recursion, replayed per lane in the definition's order
+  double acc = 0.0, la = 0.0;
+  for (int i = 0; i < kb; ++i) {
+    const double e = __shfl(ell, i);
+    acc = fmin(0.0, acc + e);
+    if (i == lane) la = acc;
+  }
+  const double vnext = __shfl_down(vn, 1);
+  double lh;
+  if (mode == SD_BLOCK)
+    lh = (lane + 1 < kb) ? block_log_h(la, vnext) : la;
+  else
+    lh = fmin(0.0, ell);
+  const uint32_t r = rnd[b];
+  const uint4 w = philox((uint32_t)(lane >> 2), (uint32_t)b, r, TAG_COIN << 24, seed);
+  const double eta = uniform64(pick(w, lane & 3));
+  const uint64_t cm = __ballot(valid && log(eta) < lh);
+  const uint64_t vmask = kb >= 64 ? ~0ull : ((1ull << kb) - 1ull);
+  int t;
+  if (mode == SD_BLOCK) {
+    t = cm ? (64 - __clzll((long long)cm)) + 1 : 1;
+  } else {
+    const uint64_t rej = ~cm & vmask;
+    t = rej ? __ffsll((unsigned long long)rej) : kb + 1;
+  }
+  const double la_prev = __shfl(la, t >= 2 ? t - 2 : 0);
+  const double la_res = (mode == SD_BLOCK && t >= 2) ? la_prev : 0.0;
+  double U = NAN;
+  if (t <= kb) {
+    const double v = __shfl(vn, t - 1);  // > 0: a rejection never lands on a zero offset
+    const uint4 wu = philox(0u, (uint32_t)b, r, TAG_USAMPLE << 24, seed);
+    const double u = uniform64(wu.x);
+    if (umode == SD_USAMPLE_PAPER) {
+      double up = 0.0;
+      if (lane == 0) up = usample_paper(u, la_res, v);
+      U = __shfl(up, 0);
+    } else {
+      U = usample_exact(u, la_res, v, lane);
+    }
+  }
+  if (lane == 0) {
+    tau[b] = t;
+    lar[b] = la_res;
+    ures[b] = U;
+    if (coins) coins[b] = cm;
+  }
+}
+
+}  // namespace
+
+hipError_t verify_launch(int B, int K, int d, int mode, const float* yd, sd_stride ys,
+                         const float* mp, sd_stride mps, const float* mq, sd_stride mqs,
+                         const double* sigma, const int32_t* kb, const uint32_t* rnd,
+                         uint64_t seed, int umode, int32_t* tau, double* lar, double* ures,
+                         double* dn, double* lr, uint64_t* coins, int* nanflag, hipStream_t s,
+                         const int* gate) {
+  const bool vec = (d % 4 == 0) && ys.chain % 4 == 0 && ys.row % 4 == 0 && mps.chain % 4 == 0 &&
+                   mps.row % 4 == 0 && mqs.chain % 4 == 0 && mqs.row % 4 == 0 &&
+                   aligned16(yd) && aligned16(mp) && aligned16(mq);
+  const int64_t rows = (int64_t)B * K;
+  hipError_t e = timed("logratio_reduce", s, [&] {
+    logratio_kernel<<<(unsigned)rows, kThreads, 0, s>>>(K, d, yd, ys.chain, ys.row, mp,
+                                                        mps.chain, mps.row, mq, mqs.chain,
+                                                        mqs.row, sigma, kb, dn, lr, vec, gate);
+  });
+  if (e != hipSuccess) return e;
+  const int per = kThreads / 64;
+  return timed("block_scan", s, [&] {
+    scan_kernel<<<(B + per - 1) / per, kThreads, 0, s>>>(B, K, mode, umode, dn, lr, kb, rnd, seed,
+                                                        tau, lar, ures, coins, nanflag, gate);
+  });
+}
+
+}  // namespace sd
