@@ -1,0 +1,250 @@
+"""Benchmark of the speculative-diffusion verification pass on one MI355X.
+
+Step = one full run of the sampler (all hot-path steps: Free-Drafter drafts,
+the Gaussian-mixture target on every draft state, log-ratio reductions, the
+block-verification scan with U-sampling, the residual draw and the commit)
+over one batch of B chains from Y_0 to Y_N, on the pixel-sized workload
+(d = 3*32*32, M = 64 components, B = 1024 chains, K = 8 drafts, N = 200 steps,
+float32).  value = verified chain-steps per second = B * N / seconds per run.
+
+Per-kernel durations are measured live with HIP events recorded around every
+launch on the launch's stream; the dominant kernel's roofline uses its
+algorithmic work (see the ALGO table below) over its measured time.  The
+verification-only workload (B = 4096, K = 32, d = 12288) and token
+verification are reported as extra fields; the CPU oracle is timed on a
+bounded sample of chains of the same workload.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+FP32_PEAK_TFLOPS = 157.3
+METRIC = "verified chain-steps/sec + mean accepted steps per block; % MFMA / HBM peak"
+
+
+def _counts_from_trace(trace, N, K):
+    """Per round: active chains, verified draft rows and drafted rows, from the tau trace."""
+    R, B = trace.shape
+    k = np.zeros(B, dtype=np.int64)
+    act, rows_verified, rows_target = [], [], []
+    for r in range(R):
+        t = trace[r]
+        a = t > 0
+        if not a.any():
+            break
+        kb = np.minimum(K, N - k)
+        act.append(int(a.sum()))
+        rows_verified.append(int(kb[a].sum()))
+        rows_target.append(int(np.minimum(kb + 1, N - k)[a].sum()))
+        k = np.where(a, np.minimum(k + t, N), k)
+    return np.array(act), np.array(rows_verified), np.array(rows_target)
+
+
+def algorithmic_work(name, B, K, d, M, act, rows_verified, runs):
+    """(bound, total algorithmic bytes or flops) of a kernel over `runs` sampler runs.
+
+    Units: the GEMMs count 2 flops per multiply-add over every row they are
+    launched on (B (K+1) rows per round plus the B rows of the one explicit
+    target call per run); the streaming kernels count the float32 bytes their
+    rows must move once (active chains only).  Rounds launched after every
+    chain has finished exit at once and count no work.
+    """
+    rows = B * (K + 1) * len(act) + B
+    if name == "gmm_logits":
+        return "mfma", 2.0 * rows * d * M * runs
+    if name == "gmm_mean":
+        return "mfma", 2.0 * rows * M * d * runs
+    if name == "logratio_reduce":
+        return "hbm", 3.0 * 4 * d * rows_verified.sum() * runs
+    if name == "draft_block":
+        return "hbm", 4.0 * d * (2 + (K + 1) + K) * act.sum() * runs
+    if name == "residual_draw":
+        return "hbm", 4.0 * d * 3 * act.sum() * runs
+    if name == "commit":
+        return "hbm", 4.0 * d * 2 * act.sum() * runs
+    return None, 0.0
+
+
+def run_sampler_bench(lib, name, mode, steps, warmup, profile):
+    import torch
+    from paper_2606_13426_amd.inputs import WORKLOADS, workload_gmm
+    cfg = WORKLOADS[name]
+    B, K, N, d, M = cfg["B"], cfg["K"], cfg["N"], cfg["d"], cfg["M"]
+    p = workload_gmm(name)
+    tgt = lib.Target(lib.schedule(N), p["mu"], p["var"], p["log_w"])
+    ws = torch.empty(lib.sd_sampler_workspace(tgt, B, K), dtype=torch.uint8, device="cuda")
+    y = torch.empty(B, d, dtype=torch.float32, device="cuda")
+    seed = 0
+    for _ in range(warmup):
+        lib.sd_run_sampler(tgt, B, K, seed, mode=mode, y_out=y, ws=ws)
+    torch.cuda.synchronize()
+    if profile:
+        lib.sd_profile_enable(True)
+    stats = []
+    t0 = time.perf_counter()
+    for s in range(steps):
+        _, st, trace = lib.sd_run_sampler(tgt, B, K, seed, mode=mode, y_out=y, ws=ws,
+                                          trace_rounds=N if s == 0 else 0)
+        stats.append(st)
+        if s == 0:
+            trace0 = trace.cpu().numpy()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = lib.sd_profile_read() if profile else {}
+    if profile:
+        lib.sd_profile_enable(False)
+    sec = (t1 - t0) / steps
+    st = stats[0]
+    be = st["steps"] / st["chain_rounds"]
+    act, rows_v, rows_t = _counts_from_trace(trace0, N, K)
+    return dict(B=B, K=K, N=N, d=d, M=M, sec=sec, be=be, rounds=st["rounds"], prof=prof,
+                act=act, rows_verified=rows_v, rows_target=rows_t, tau_hist=st["tau_hist"][: K + 2],
+                steps=steps)
+
+
+def roofline_of(res, steps):
+    prof = res["prof"]
+    if not prof:
+        return None, {}
+    name = max(prof, key=lambda n: prof[n][1])
+    table = {}
+    for kname, (launches, ms) in prof.items():
+        bound, work = algorithmic_work(kname, res["B"], res["K"], res["d"], res["M"], res["act"],
+                                       res["rows_verified"], steps)
+        entry = dict(launches=launches, avg_us=1e3 * ms / max(launches, 1), total_ms=ms)
+        if bound == "hbm":
+            entry.update(bound="hbm", achieved=work / (ms * 1e-3) / 1e9, unit="GB/s", peak=HBM_PEAK_GBS)
+        elif bound == "mfma":
+            entry.update(bound="mfma", achieved=work / (ms * 1e-3) / 1e12, unit="TFLOP/s",
+                         peak=FP32_PEAK_TFLOPS)
+        if bound:
+            entry["frac"] = entry["achieved"] / entry["peak"]
+            entry["algorithmic_per_launch"] = work / max(launches, 1)
+        table[kname] = entry
+    e = table[name]
+    roof = dict(kernel=name, bound=e.get("bound"), achieved=e.get("achieved"), peak=e.get("peak"),
+                unit=e.get("unit"), frac=e.get("frac"), traffic=None,
+                avg_launch_us=e["avg_us"], launches=e["launches"])
+    return roof, table
+
+
+def verify_bench(lib, steps, warmup):
+    """Verification-only workload: one sd_verify_block + sd_sample_residual per step."""
+    import torch
+    from paper_2606_13426_amd.inputs import WORKLOADS, verify_inputs
+    cfg = WORKLOADS["verify12288"]
+    B, K, d, N = cfg["B"], cfg["K"], cfg["d"], cfg["N"]
+    sig = lib.sd_schedule_table(lib.schedule(N))[1]
+    inp = verify_inputs(B, K, d, N, sig, seed=1, device="cuda", perturb=cfg["perturb"])
+    y = torch.empty(B, d, device="cuda")
+    out = None
+    seed = 11
+
+    def step():
+        nonlocal out
+        out = lib.sd_verify_block(inp["y_draft"], inp["mp"], inp["mq"], inp["sigma"], inp["kb"],
+                                  inp["round"], seed, out=out)
+        lib.sd_sample_residual(inp["y_draft"], inp["mp"], inp["mq"], inp["sigma"], inp["kb"],
+                               inp["steps_left"], out["tau"], out["u_res"], out["delta_norm"],
+                               inp["round"], seed, y)
+
+    for _ in range(warmup):
+        step()
+    torch.cuda.synchronize()
+    lib.sd_profile_enable(True)
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = lib.sd_profile_read()
+    lib.sd_profile_enable(False)
+    sec = (t1 - t0) / steps
+    tau = out["tau"].cpu().numpy()
+    lr_launches, lr_ms = prof["logratio_reduce"]
+    algo = 3.0 * 4 * d * B * K
+    res_bytes = 4.0 * d * 3 * B
+    del inp
+    return dict(workload="verify12288", B=B, K=K, d=d,
+                value=B * K / sec, unit="verified chain-steps/s", ms_per_step=1e3 * sec,
+                mean_tau=float(tau.mean()),
+                logratio=dict(bound="hbm", achieved=algo / (lr_ms / lr_launches * 1e-3) / 1e9,
+                              peak=HBM_PEAK_GBS, unit="GB/s",
+                              frac=algo / (lr_ms / lr_launches * 1e-3) / 1e9 / HBM_PEAK_GBS,
+                              avg_launch_us=1e3 * lr_ms / lr_launches),
+                pass_GBps=(algo + res_bytes) / sec / 1e9,
+                kernels={k: dict(launches=v[0], avg_us=1e3 * v[1] / max(v[0], 1)) for k, v in prof.items()})
+
+
+def cpu_baseline(name, budget_s):
+    """The oracle (single-threaded NumPy float64) on a bounded sample of chains."""
+    from oracle import sampler as osamp
+    from oracle.gmm import GMM
+    from oracle.schedule import Schedule
+    from paper_2606_13426_amd.inputs import WORKLOADS, workload_gmm
+    cfg = WORKLOADS[name]
+    p = workload_gmm(name)
+    g = GMM(p["mu"], p["var"], p["log_w"])
+    sch = Schedule(cfg["N"])
+    t0 = time.perf_counter()
+    chains = 0
+    while chains < cfg["B"]:
+        osamp.run_sampler(g, sch, cfg["B"], cfg["K"], 0, chains=[chains])
+        chains += 1
+        if time.perf_counter() - t0 > budget_s:
+            break
+    el = time.perf_counter() - t0
+    return dict(value=chains * cfg["N"] / el, unit="chain-steps/s", cores=1, kind="oracle",
+                sample=f"{chains} of {cfg['B']} chains of {name}, full {cfg['N']}-step runs, "
+                       f"{el:.1f} s, single-threaded NumPy float64")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="pixel3072")
+    ap.add_argument("--no-extra", action="store_true", help="skip the token and verification-only runs")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): chains are independent and "
+              "would shard across GPUs without communication, but multi-GPU runs are not part of this build",
+              file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_13426_amd import _lib as lib
+    lib.load()
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    res = run_sampler_bench(lib, args.workload, lib.SD_BLOCK, args.steps, args.warmup, profile=True)
+    roof, table = roofline_of(res, args.steps)
+    line = dict(metric=METRIC, value=res["B"] * res["N"] / res["sec"], unit="chain-steps/s", n_gpus=1,
+                steps=args.steps, warmup=args.warmup, ms_per_step=1e3 * res["sec"], higher_is_better=True,
+                scaling="weak", vs_baseline=None, dtype="f32", data="synthetic",
+                config=dict(workload=args.workload, d=res["d"], M=res["M"], B=res["B"], K=res["K"],
+                            N=res["N"], verification="block", drafter="free", usample="exact",
+                            parallelism="single-gpu"),
+                mean_accepted_steps_per_block=res["be"], rounds_per_run=res["rounds"],
+                roofline=roof, kernels=table)
+    if not args.no_extra:
+        tok = run_sampler_bench(lib, args.workload, lib.SD_TOKEN, max(2, args.steps // 2), 1, profile=False)
+        line["token"] = dict(value=tok["B"] * tok["N"] / tok["sec"], ms_per_step=1e3 * tok["sec"],
+                             mean_accepted_steps_per_block=tok["be"], rounds_per_run=tok["rounds"])
+        line["verify_only"] = verify_bench(lib, args.steps, args.warmup)
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_budget)
+    print(json.dumps(line))
+
+
+if __name__ == "__main__":
+    main()
