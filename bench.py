@@ -60,16 +60,16 @@ def algorithmic_work(name, B, K, d, M, act, rows_verified, runs):
     rows = B * (K + 1) * len(act) + B
     if name == "gmm_logits":
         return "mfma", 2.0 * rows * d * M * runs
-    if name == "gmm_mean":
+    if name in ("gmm_mean", "gmm_mean_lr"):
         return "mfma", 2.0 * rows * M * d * runs
     if name == "logratio_reduce":
         return "hbm", 3.0 * 4 * d * rows_verified.sum() * runs
-    if name == "draft_block":
-        return "hbm", 4.0 * d * (2 + (K + 1) + K) * act.sum() * runs
-    if name == "residual_draw":
+    if name == "draft_block":   # reads y and the cached (x, m^q) row; writes K+1 drafts, K means
+        return "hbm", 4.0 * d * (3 + (K + 1) + K) * act.sum() * runs
+    if name == "residual_commit":   # reads two rows, writes the new state
         return "hbm", 4.0 * d * 3 * act.sum() * runs
-    if name == "commit":
-        return "hbm", 4.0 * d * 2 * act.sum() * runs
+    if name == "advance":   # residual rows, cache rows; new state, K+1 drafts, K means
+        return "hbm", 4.0 * d * (4 + 1 + (K + 1) + K) * act.sum() * runs
     return None, 0.0
 
 
@@ -83,10 +83,23 @@ def run_sampler_bench(lib, name, mode, steps, warmup, profile):
     ws = torch.empty(lib.sd_sampler_workspace(tgt, B, K), dtype=torch.uint8, device="cuda")
     y = torch.empty(B, d, dtype=torch.float32, device="cuda")
     seed = 0
-    for _ in range(warmup):
+    breakdown, only = {}, None
+    nw = max(warmup, 2 if profile else 0)
+    for w in range(nw):
+        last = w == nw - 1
+        if profile and last:
+            # the last (profiled) warm-up run gives the per-kernel breakdown and
+            # names the dominant kernel; the timed runs then bracket only it
+            lib.sd_profile_only(None)
+            lib.sd_profile_enable(True)
         lib.sd_run_sampler(tgt, B, K, seed, mode=mode, y_out=y, ws=ws)
+        if profile and last:
+            breakdown = lib.sd_profile_read()
+            lib.sd_profile_enable(False)
+            only = max(breakdown, key=lambda n: breakdown[n][1])
     torch.cuda.synchronize()
     if profile:
+        lib.sd_profile_only(only)
         lib.sd_profile_enable(True)
     stats = []
     t0 = time.perf_counter()
@@ -101,24 +114,31 @@ def run_sampler_bench(lib, name, mode, steps, warmup, profile):
     prof = lib.sd_profile_read() if profile else {}
     if profile:
         lib.sd_profile_enable(False)
+        lib.sd_profile_only(None)
     sec = (t1 - t0) / steps
     st = stats[0]
     be = st["steps"] / st["chain_rounds"]
     act, rows_v, rows_t = _counts_from_trace(trace0, N, K)
     return dict(B=B, K=K, N=N, d=d, M=M, sec=sec, be=be, rounds=st["rounds"], prof=prof,
+                breakdown=breakdown,
                 act=act, rows_verified=rows_v, rows_target=rows_t, tau_hist=st["tau_hist"][: K + 2],
                 steps=steps)
 
 
 def roofline_of(res, steps):
+    """Roofline of the dominant kernel (timed live over the timed runs) and the
+    per-kernel table of the profiled warm-up run (one sampler run)."""
     prof = res["prof"]
     if not prof:
         return None, {}
     name = max(prof, key=lambda n: prof[n][1])
     table = {}
-    for kname, (launches, ms) in prof.items():
+    sources = dict(res["breakdown"])
+    sources[name] = prof[name]
+    for kname, (launches, ms) in sources.items():
+        runs = steps if kname == name else 1
         bound, work = algorithmic_work(kname, res["B"], res["K"], res["d"], res["M"], res["act"],
-                                       res["rows_verified"], steps)
+                                       res["rows_verified"], runs)
         entry = dict(launches=launches, avg_us=1e3 * ms / max(launches, 1), total_ms=ms)
         if bound == "hbm":
             entry.update(bound="hbm", achieved=work / (ms * 1e-3) / 1e9, unit="GB/s", peak=HBM_PEAK_GBS)
@@ -216,7 +236,21 @@ def main():
     ap.add_argument("--no-extra", action="store_true", help="skip the token and verification-only runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run a plain device copy of 1 GiB five times (the reference "
+                         "kernel of known size for scaling the HBM byte counters) and exit")
     args = ap.parse_args()
+    if args.calibrate_copy:
+        import torch
+        n = (1 << 30) // 4
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(6):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps(dict(calibrate_copy_bytes_read=4 * n, calibrate_copy_bytes_written=4 * n,
+                              copies=6)))
+        return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): chains are independent and "
               "would shard across GPUs without communication, but multi-GPU runs are not part of this build",

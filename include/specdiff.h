@@ -84,7 +84,7 @@ sd_status sd_schedule_table(const sd_schedule* sched, double* host_out);
  * q_s = sum_m w_m N(a mu_m, (a^2 var_m + 1 - a^2) I) and its score, and the EM
  * mean m^q_n(x) = c1_n x + c2_n score (eq. target-distribution).
  * mu [M][d], var [M], log_w [M] are HOST arrays copied at creation.
- * d >= 1, 1 <= n_comp <= 4096.  precision selects the GEMM operand type. */
+ * d >= 1, 1 <= n_comp <= 1024.  precision selects the GEMM operand type. */
 sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp,
                            const float* mu, const float* var, const float* log_w,
                            sd_precision precision, sd_target* out);
@@ -199,6 +199,9 @@ typedef struct {
 } sd_kernel_stat;
 
 sd_status sd_profile_enable(int32_t on);
+/* Restrict collection to launches of the kernel named `name` (host string,
+ * copied); NULL times every kernel again. */
+sd_status sd_profile_only(const char* name);
 sd_status sd_profile_read(sd_kernel_stat* out, int32_t capacity, int32_t* count);
 
 /* ----------------------------------------------------------- test hooks --

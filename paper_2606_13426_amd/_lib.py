@@ -69,6 +69,7 @@ SIGNATURES = [
     ("sd_run_sampler", c_int32, [P, c_int32, c_int32, c_int32, c_int32, c_uint64, P, P, c_int32,
                                  ctypes.POINTER(sd_stats), P, c_size_t, P]),
     ("sd_profile_enable", c_int32, [c_int32]),
+    ("sd_profile_only", c_int32, [c_char_p]),
     ("sd_profile_read", c_int32, [ctypes.POINTER(sd_kernel_stat), c_int32, ctypes.POINTER(c_int32)]),
     ("sd_philox_words", c_int32, [c_uint64, c_int32, P, P, P]),
     ("sd_philox_normals", c_int32, [c_uint64, c_uint32, c_uint32, c_uint32, c_uint32, c_int32, P, P]),
@@ -245,6 +246,10 @@ def sd_run_sampler(target, B, K, seed, mode=SD_BLOCK, usample_mode=SD_USAMPLE_EX
 
 def sd_profile_enable(on=True):
     _check(load().sd_profile_enable(1 if on else 0), "sd_profile_enable")
+
+
+def sd_profile_only(name=None):
+    _check(load().sd_profile_only(None if name is None else name.encode()), "sd_profile_only")
 
 
 def sd_profile_read():

@@ -1,0 +1,136 @@
+// The sampler's end of a round and start of the next, fused elementwise.
+//
+// After the fused verification has decided tau (and, for a rejection, the
+// scalar rcoef = (U - e.G)/||Delta||), every remaining step of the round is
+// elementwise in the coordinates:
+//   residual  y_i = m^q_i + sigma G_i + rcoef (m^p_i - m^q_i)     (Alg. 5 with e.G known)
+//             or the full-accept target draw, or the last draft at step N (Alg. 8);
+//   commit    k <- min(k + tau, N), round <- round + 1 (one thread per chain);
+//   draft     the next round's Free-Drafter block from y_i, whose cached score
+//             is that of row min(tau, K_b) of this round (Sec. 3.3), recovered
+//             from the same round's (x, m^q) rows.
+// Each thread owns four coordinates of one chain: it reads every row it needs
+// (m^p/m^q of the residual row, the cache row, the last draft) before it
+// overwrites that chain's x and m^p rows at the same coordinates, so one pass
+// replaces the separate residual, commit and draft kernels and the state
+// never leaves registers between them.
+#include "common.hpp"
+#include "philox.hpp"
+#include "rows.hpp"
+
+namespace sd {
+namespace {
+
+constexpr int kThreads = 256;
+
+__global__ __launch_bounds__(kThreads) void advance_kernel(
+    Sched sc, const float4* __restrict__ coef, int B, int K, int d, uint64_t seed,
+    const int32_t* __restrict__ kcur, const uint32_t* __restrict__ rcur,
+    const int32_t* __restrict__ crow_cur, const int32_t* __restrict__ cstep_cur,
+    int32_t* __restrict__ knext, uint32_t* __restrict__ rnext, int32_t* __restrict__ crow_next,
+    int32_t* __restrict__ cstep_next, const int32_t* __restrict__ tauv,
+    const int32_t* __restrict__ rmode, const float* __restrict__ rcoef,
+    const float* __restrict__ rsig, float* __restrict__ X, float* __restrict__ MP,
+    const float* __restrict__ MQ, float* __restrict__ y, int32_t* __restrict__ step,
+    double* __restrict__ sigma, int32_t* __restrict__ hist, int64_t* __restrict__ steps,
+    int* act_next, int32_t* __restrict__ trace, int r_round, int trace_rounds, bool vec_ok,
+    const int* gate) {
+  if (gate && *gate == 0) return;
+  const int N = sc.N, K1 = K + 1;
+  const int b = blockIdx.y;
+  const int t = tauv[b];
+  const int k = kcur[b];
+  const uint32_t r = rcur[b];
+  const bool active = t > 0;
+  const int kb = active ? min(K, N - k) : 0;
+  const int knew = active ? min(k + t, N) : k;
+  const int cr = min(t, kb);
+  const int cs = min(k + cr, N - 1);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    if (active) {
+      knext[b] = knew;
+      rnext[b] = r + 1u;
+      crow_next[b] = cr;
+      cstep_next[b] = cs;
+      hist[(int64_t)b * (SD_MAX_BLOCK + 2) + t] += 1;
+      steps[b] += knew - k;
+      if (knew < N) *act_next = 1;
+    } else {
+      knext[b] = k;
+      rnext[b] = r;
+      crow_next[b] = crow_cur[b];
+      cstep_next[b] = cstep_cur[b];
+    }
+    if (trace && r_round < trace_rounds) trace[(int64_t)r_round * B + b] = active ? t : 0;
+  }
+  if (!active) return;
+  // the next round's step index and sigma of every target row
+  if (blockIdx.x == 0 && threadIdx.x <= K && knew < N) {
+    const int j = threadIdx.x;
+    step[(int64_t)b * K1 + j] = min(knew + j, N - 1);
+    sigma[(int64_t)b * K1 + j] = sched_sigma(sc, min(knew + j, N));
+  }
+  const int g = blockIdx.x * kThreads + threadIdx.x;
+  const int e0 = 4 * g;
+  if (e0 >= d) return;
+  const int cnt = min(4, d - e0);
+  const bool vec = vec_ok && cnt == 4;
+  float* xb = X + (int64_t)b * K1 * d + e0;
+  float* mb = MP + (int64_t)b * K * d + e0;
+  const float* qb = MQ + (int64_t)b * K1 * d + e0;
+  float yv[4];
+  const int rm = rmode[b];
+  if (rm == 1) {
+    float pv[4], qv[4];
+    load4(mb + (int64_t)(t - 1) * d, cnt, vec, pv);
+    load4(qb + (int64_t)(t - 1) * d, cnt, vec, qv);
+    const float sg = rsig[b], cf = rcoef[b];
+    const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, TAG_RESID << 24, seed));
+#pragma unroll
+    for (int c = 0; c < 4; ++c) yv[c] = qv[c] + sg * get4(z, c) + cf * (pv[c] - qv[c]);
+  } else if (rm == 2) {
+    float qv[4];
+    load4(qb + (int64_t)kb * d, cnt, vec, qv);
+    const float sg = rsig[b];
+    const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, TAG_TARGET << 24, seed));
+#pragma unroll
+    for (int c = 0; c < 4; ++c) yv[c] = qv[c] + sg * get4(z, c);
+  } else {
+    load4(xb + (int64_t)kb * d, cnt, vec, yv);
+  }
+  store4(y + (int64_t)b * d + e0, cnt, vec, yv);
+  if (knew >= N) return;
+  float xcv[4], qcv[4], sv[4];
+  load4(xb + (int64_t)cr * d, cnt, vec, xcv);
+  load4(qb + (int64_t)cr * d, cnt, vec, qcv);
+  const float4 cc = step_coef(sc, coef, cs);
+#pragma unroll
+  for (int c = 0; c < 4; ++c) sv[c] = qcv[c] - cc.x * xcv[c];  // c2_c S_c
+  store4(xb, cnt, vec, yv);
+  draft_rows(sc, coef, K, knew, min(K, N - knew), (uint32_t)b, r + 1u, seed, g, yv, sv, cc.w, xb,
+             d, mb, d, cnt, vec);
+}
+
+}  // namespace
+
+hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int d,
+                          uint64_t seed, const int32_t* kcur, const uint32_t* rcur,
+                          const int32_t* crow_cur, const int32_t* cstep_cur, int32_t* knext,
+                          uint32_t* rnext, int32_t* crow_next, int32_t* cstep_next,
+                          const int32_t* tau, const int32_t* rmode, const float* rcoef,
+                          const float* rsig, float* x, float* mp, const float* mq, float* y,
+                          int32_t* step, double* sigma, int32_t* hist, int64_t* steps,
+                          int* act_next, int32_t* trace, int r, int trace_rounds, hipStream_t s,
+                          const int* gate) {
+  const int ng = (d + 3) / 4;
+  dim3 grid((ng + kThreads - 1) / kThreads, B);
+  const bool vec = (d % 4 == 0) && aligned16(x) && aligned16(mp) && aligned16(mq) && aligned16(y);
+  return timed("advance", s, [&] {
+    advance_kernel<<<grid, kThreads, 0, s>>>(sc, coef, B, K, d, seed, kcur, rcur, crow_cur,
+                                             cstep_cur, knext, rnext, crow_next, cstep_next, tau,
+                                             rmode, rcoef, rsig, x, mp, mq, y, step, sigma, hist,
+                                             steps, act_next, trace, r, trace_rounds, vec, gate);
+  });
+}
+
+}  // namespace sd

@@ -54,7 +54,12 @@ void drain_locked() {
 }
 }  // namespace
 
-bool prof_on() { return g_prof; }
+std::string g_prof_only;
+
+bool prof_on(const char* name) {
+  if (!g_prof) return false;
+  return g_prof_only.empty() || g_prof_only == name;
+}
 
 void prof_events(hipEvent_t* a, hipEvent_t* b) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
@@ -132,7 +137,7 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
   *out = nullptr;
   SD_CHECK_ARG(sched_ok(sched), "sd_target_create: invalid schedule (need N >= 1, 0 < beta_min <= beta_max, churn > 0)");
   SD_CHECK_ARG(d >= 1, "sd_target_create: d = %d < 1", d);
-  SD_CHECK_ARG(n_comp >= 1 && n_comp <= 4096, "sd_target_create: n_comp = %d not in [1, 4096]", n_comp);
+  SD_CHECK_ARG(n_comp >= 1 && n_comp <= 1024, "sd_target_create: n_comp = %d not in [1, 1024]", n_comp);
   SD_CHECK_ARG(mu && var && log_w, "sd_target_create: mu/var/log_w must be host arrays");
   SD_CHECK_ARG(precision == SD_FP32 || precision == SD_BF16, "sd_target_create: unknown precision");
   if (precision == SD_BF16) {
@@ -169,9 +174,10 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
   (void)hipGetDevice(&t->device);
   bool ok = hipMalloc(&t->mu, sizeof(float) * M * D) == hipSuccess &&
             hipMalloc(&t->muT, sizeof(float) * M * D) == hipSuccess &&
-            hipMalloc(&t->var, sizeof(double) * M) == hipSuccess &&
+            hipMalloc(&t->ls, sizeof(double2) * M * (size_t)sched->n_steps) == hipSuccess &&
             hipMalloc(&t->logw, sizeof(double) * M) == hipSuccess &&
-            hipMalloc(&t->musq, sizeof(double) * M) == hipSuccess;
+            hipMalloc(&t->musq, sizeof(double) * M) == hipSuccess &&
+            hipMalloc(&t->coef, sizeof(float4) * (size_t)(sched->n_steps + 1)) == hipSuccess;
   if (!ok) {
     set_error("sd_target_create: device allocation failed");
     sd_target_destroy(reinterpret_cast<sd_target>(t));
@@ -179,9 +185,27 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
   }
   ok = hipMemcpy(t->mu, mu, sizeof(float) * M * D, hipMemcpyHostToDevice) == hipSuccess &&
        hipMemcpy(t->muT, muT.data(), sizeof(float) * M * D, hipMemcpyHostToDevice) == hipSuccess &&
-       hipMemcpy(t->var, vv.data(), sizeof(double) * M, hipMemcpyHostToDevice) == hipSuccess &&
+
        hipMemcpy(t->logw, lw.data(), sizeof(double) * M, hipMemcpyHostToDevice) == hipSuccess &&
        hipMemcpy(t->musq, msq.data(), sizeof(double) * M, hipMemcpyHostToDevice) == hipSuccess;
+  std::vector<double2> ls(M * (size_t)sched->n_steps);
+  for (int n = 0; n < sched->n_steps; ++n) {
+    const double a = sched_signal(t->sc, n), a2 = a * a;
+    for (size_t m = 0; m < M; ++m) {
+      const double s2 = a2 * vv[m] + 1.0 - a2;
+      ls[(size_t)n * M + m] = make_double2(log(s2), 1.0 / s2);
+    }
+  }
+  ok = ok && hipMemcpy(t->ls, ls.data(), sizeof(double2) * ls.size(), hipMemcpyHostToDevice) ==
+                 hipSuccess;
+  std::vector<float4> coef((size_t)sched->n_steps + 1);
+  for (int n = 0; n <= sched->n_steps; ++n) {
+    const double c2 = sched_c2(t->sc, n);
+    coef[n] = make_float4((float)sched_c1(t->sc, n), (float)c2, (float)sched_sigma(t->sc, n),
+                          (float)(1.0 / c2));
+  }
+  ok = ok && hipMemcpy(t->coef, coef.data(), sizeof(float4) * coef.size(), hipMemcpyHostToDevice) ==
+                 hipSuccess;
   if (!ok) {
     set_error("sd_target_create: copy to device failed");
     sd_target_destroy(reinterpret_cast<sd_target>(t));
@@ -196,9 +220,10 @@ sd_status sd_target_destroy(sd_target target) {
   Target* t = reinterpret_cast<Target*>(target);
   if (t->mu) (void)hipFree(t->mu);
   if (t->muT) (void)hipFree(t->muT);
-  if (t->var) (void)hipFree(t->var);
+  if (t->ls) (void)hipFree(t->ls);
   if (t->logw) (void)hipFree(t->logw);
   if (t->musq) (void)hipFree(t->musq);
+  if (t->coef) (void)hipFree(t->coef);
   delete t;
   return SD_OK;
 }
@@ -228,7 +253,7 @@ sd_status sd_target_mean(sd_target target, int32_t rows, const float* x, int64_t
 sd_status sd_init_chains(int32_t B, int32_t d, uint64_t seed, float* y, sd_stream stream) {
   SD_CHECK_ARG(B >= 1 && d >= 1, "sd_init_chains: need B >= 1 and d >= 1");
   SD_CHECK_ARG(y, "sd_init_chains: y is NULL");
-  SD_HIP(init_chains_launch(B, d, seed, y, (hipStream_t)stream));
+  SD_HIP(init_chains_launch(B, d, seed, y, nullptr, 0, (hipStream_t)stream));
   return SD_OK;
 }
 
@@ -285,7 +310,7 @@ sd_status sd_sample_residual(int32_t B, int32_t K, int32_t d, const float* y_dra
   SD_CHECK_ARG(mqs.row >= d && mqs.chain >= (int64_t)(K + 1) * mqs.row,
                "sd_sample_residual: mq stride too small for [B][K+1][d]");
   SD_HIP(residual_launch(B, K, d, y_draft, ys, mp, mps, mq, mqs, sigma, kb, steps_left, tau,
-                         u_res, delta_norm, round, seed, y_out, (hipStream_t)stream, nullptr));
+                         u_res, delta_norm, round, seed, y_out, (hipStream_t)stream));
   return SD_OK;
 }
 
@@ -295,9 +320,10 @@ sd_status sd_sample_residual(int32_t B, int32_t K, int32_t d, const float* y_dra
 namespace {
 
 struct SamplerLayout {
-  size_t y, cache, x, mp, mq, score, sigma, lar, ures, dn, lr, k, step, kb, left, tau, rnd, cnt,
-      hist, steps, nan, tws, total;
+  size_t y, x, mp, mq, sigma, step, k2, rnd2, crow2, cstep2, tau, rmode, rcoef, rsig, hist, steps,
+      act, nan, kb, left, dummy_i32, dummy_i64, lrp, tws, total;
   size_t tws_bytes;
+  int nct;
 };
 
 inline size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -311,27 +337,30 @@ SamplerLayout sampler_layout(const Target& t, int B, int K) {
     off = a256(off + bytes);
     return o;
   };
+  L.nct = lr_tiles(t);
   L.y = take(4 * Bs * d);
-  L.cache = take(4 * Bs * d);
   L.x = take(4 * Bs * K1 * d);
   L.mp = take(4 * Bs * K * d);
   L.mq = take(4 * Bs * K1 * d);
-  L.score = take(4 * Bs * K1 * d);
   L.sigma = take(8 * Bs * K1);
-  L.lar = take(8 * Bs);
-  L.ures = take(8 * Bs);
-  L.dn = take(8 * Bs * K);
-  L.lr = take(8 * Bs * K);
-  L.k = take(4 * Bs);
   L.step = take(4 * Bs * K1);
+  L.k2 = take(4 * 2 * Bs);
+  L.rnd2 = take(4 * 2 * Bs);
+  L.crow2 = take(4 * 2 * Bs);
+  L.cstep2 = take(4 * 2 * Bs);
+  L.tau = take(4 * Bs);
+  L.rmode = take(4 * Bs);
+  L.rcoef = take(4 * Bs);
+  L.rsig = take(4 * Bs);
+  L.hist = take(4 * Bs * (SD_MAX_BLOCK + 2));
+  L.steps = take(8 * Bs);
+  L.act = take(4 * 2);
+  L.nan = take(4);
   L.kb = take(4 * Bs);
   L.left = take(4 * Bs);
-  L.tau = take(4 * Bs);
-  L.rnd = take(4 * Bs);
-  L.cnt = take(4 * 2);
-  L.hist = take(8 * (SD_MAX_BLOCK + 2));
-  L.steps = take(8);
-  L.nan = take(4);
+  L.dummy_i32 = take(4 * (Bs + 2));
+  L.dummy_i64 = take(8 * (SD_MAX_BLOCK + 3));
+  L.lrp = take(8 * 3 * Bs * K1 * (size_t)L.nct);
   const size_t rows = Bs * K1;
   L.tws_bytes = target_ws_bytes(t, (int)rows);
   L.tws = take(L.tws_bytes);
@@ -368,72 +397,82 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
   hipStream_t s = (hipStream_t)stream;
   char* base = static_cast<char*>(ws);
   auto F = [&](size_t o) { return reinterpret_cast<float*>(base + o); };
-  auto D = [&](size_t o) { return reinterpret_cast<double*>(base + o); };
   auto I = [&](size_t o) { return reinterpret_cast<int32_t*>(base + o); };
   const int d = t.d, N = t.sc.N, K1 = K + 1;
-  float *y = F(L.y), *cache = F(L.cache), *x = F(L.x), *mp = F(L.mp), *mq = F(L.mq),
-        *score = F(L.score);
-  double *sigma = D(L.sigma), *lar = D(L.lar), *ures = D(L.ures), *dn = D(L.dn), *lr = D(L.lr);
-  int32_t *kk = I(L.k), *step = I(L.step), *kb = I(L.kb), *left = I(L.left), *tau = I(L.tau);
-  uint32_t* rnd = reinterpret_cast<uint32_t*>(base + L.rnd);
-  int* cnt = I(L.cnt);
-  int64_t* hist = reinterpret_cast<int64_t*>(base + L.hist);
+  float *y = F(L.y), *x = F(L.x), *mp = F(L.mp), *mq = F(L.mq), *rcoef = F(L.rcoef),
+        *rsig = F(L.rsig);
+  double* sigma = reinterpret_cast<double*>(base + L.sigma);
+  double* lrp = reinterpret_cast<double*>(base + L.lrp);
+  int32_t *step = I(L.step), *k2 = I(L.k2), *crow2 = I(L.crow2), *cstep2 = I(L.cstep2),
+          *tau = I(L.tau), *rmode = I(L.rmode), *hist = I(L.hist), *act = I(L.act),
+          *nanflag = I(L.nan), *kb = I(L.kb), *left = I(L.left), *dummy = I(L.dummy_i32);
+  uint32_t* rnd2 = reinterpret_cast<uint32_t*>(base + L.rnd2);
   int64_t* steps = reinterpret_cast<int64_t*>(base + L.steps);
-  int* nanflag = I(L.nan);
+  int64_t* dummy64 = reinterpret_cast<int64_t*>(base + L.dummy_i64);
   void* tws = base + L.tws;
-
   const sd_stride xs{(int64_t)K1 * d, d}, mps{(int64_t)K * d, d}, mqs{(int64_t)K1 * d, d};
-  const sd_stride ys{(int64_t)K1 * d, d};  // drafts are rows 1..K of x
-  const float* ydraft = x + d;
 
-  // Y_0 and the one explicit target call that seeds the Free-Drafter cache
-  SD_HIP(init_chains_launch(B, d, seed, y, s));
-  SD_HIP(fill_i32_launch(kk, B, 0, s));
-  SD_HIP(fill_i32_launch(reinterpret_cast<int32_t*>(rnd), B, 0, s));
-  SD_HIP(fill_i32_launch(step, B, 0, s));
-  SD_HIP(fill_i32_launch(cnt, 2, B, s));
+  // Y_0 (also row 0 of x); the one explicit target call at Y_0, whose mean
+  // (row 0 of mq) seeds the Free Drafter's cached score; the round-0 rows'
+  // steps and sigmas; the first draft block.
+  SD_HIP(fill_i32_launch(k2, 2 * (int64_t)B, 0, s));
+  SD_HIP(fill_i32_launch(reinterpret_cast<int32_t*>(rnd2), 2 * (int64_t)B, 0, s));
+  SD_HIP(fill_i32_launch(crow2, 2 * (int64_t)B, 0, s));
+  SD_HIP(fill_i32_launch(cstep2, 2 * (int64_t)B, 0, s));
+  SD_HIP(fill_i32_launch(hist, (int64_t)B * (SD_MAX_BLOCK + 2), 0, s));
+  SD_HIP(fill_i64_launch(steps, B, 0, s));
+  SD_HIP(fill_i32_launch(act, 1, 1, s));
+  SD_HIP(fill_i32_launch(act + 1, 1, 0, s));
   SD_HIP(fill_i32_launch(nanflag, 1, 0, s));
-  SD_HIP(fill_i64_launch(hist, SD_MAX_BLOCK + 2, 0, s));
-  SD_HIP(fill_i64_launch(steps, 1, 0, s));
-  SD_HIP(target_mean_launch(t, B, y, d, step, mq, d, cache, d, tws, s, nullptr));
+  SD_HIP(fill_i32_launch(step, B, 0, s));
+  SD_HIP(fill_i32_launch(tau, B, 0, s));
+  SD_HIP(fill_i32_launch(dummy, B + 2, 0, s));
+  SD_HIP(init_chains_launch(B, d, seed, y, x, (int64_t)K1 * d, s));
+  SD_HIP(target_mean_launch(t, B, x, (int64_t)K1 * d, step, mq, (int64_t)K1 * d, nullptr, 0, tws,
+                            s, nullptr));
+  SD_HIP(prepare_launch(t.sc, B, K, k2, kb, left, step, sigma, tau, dummy, dummy + B,
+                        dummy + B + 1, dummy64, dummy64 + SD_MAX_BLOCK + 2, s));
+  SD_HIP(draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2, cstep2, mq, mqs, k2, rnd2, seed, x,
+                             xs, mp, mps, s, nullptr));
 
-  int32_t* host_cnt = nullptr;
+  int32_t* host_act = nullptr;
   constexpr int kLag = 3;
   hipEvent_t ev[kLag + 1];
-  SD_HIP(hipHostMalloc(reinterpret_cast<void**>(&host_cnt), sizeof(int32_t) * (kLag + 1), hipHostMallocDefault));
+  SD_HIP(hipHostMalloc(reinterpret_cast<void**>(&host_act), sizeof(int32_t) * (kLag + 1), hipHostMallocDefault));
   for (int i = 0; i <= kLag; ++i) {
-    host_cnt[i] = -1;
+    host_act[i] = -1;
     (void)hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
   }
   sd_status st = SD_OK;
-  int64_t rounds = 0;
-  const int max_rounds = N + kLag + 2;
+  int64_t rounds = -1;
+  // a round advances every active chain by at least one step, so at most N
+  // rounds have work; the queue runs kLag rounds ahead of the flag it reads
+  const int max_rounds = N + 1 + kLag;
   int r = 0;
-  bool done = false;
-  for (; r < max_rounds && !done; ++r) {
-    int* cur = cnt + (r & 1);
-    const int* gate = cnt + ((r + 1) & 1);
-    hipError_t e = prepare_launch(t.sc, B, K, kk, kb, left, step, sigma, cur, s, gate);
-    if (e == hipSuccess) e = draft_launch(t.sc, B, K, d, y, cache, kk, rnd, seed, x, xs, mp, mps, s, gate);
-    if (e == hipSuccess) e = target_mean_launch(t, B * K1, x, d, step, mq, d, score, d, tws, s, gate);
+  for (; r < max_rounds && rounds < 0; ++r) {
+    const int cur = r & 1, nxt = cur ^ 1;
+    const int* gate = act + cur;
+    hipError_t e = target_mean_lr_launch(t, B * K1, K1, x, step, mq, mp, lrp, rnd2 + cur * B, seed,
+                                         tws, s, gate);
     if (e == hipSuccess)
-      e = verify_launch(B, K, d, (int)mode, ydraft, ys, mp, mps, mq, mqs, sigma, kb, rnd, seed,
-                        (int)usample_mode, tau, lar, ures, dn, lr, nullptr, nanflag, s, gate);
+      e = scan_fused_launch(B, K, d, N, (int)mode, (int)usample_mode, lrp, L.nct, sigma,
+                            k2 + cur * B, rnd2 + cur * B, seed, mp, mq, tau, rmode, rcoef, rsig,
+                            nanflag, act + nxt, s, gate);
     if (e == hipSuccess)
-      e = residual_launch(B, K, d, ydraft, ys, mp, mps, mq, mqs, sigma, kb, left, tau, ures, dn,
-                          rnd, seed, y, s, gate);
-    if (e == hipSuccess)
-      e = commit_launch(B, K, d, N, tau, kb, kk, rnd, score, mqs, cache, cur, hist, steps,
-                        tau_trace, r, tau_trace ? trace_rounds : 0, s, gate);
+      e = advance_launch(t.sc, t.coef, B, K, d, seed, k2 + cur * B, rnd2 + cur * B,
+                         crow2 + cur * B, cstep2 + cur * B, k2 + nxt * B, rnd2 + nxt * B,
+                         crow2 + nxt * B, cstep2 + nxt * B, tau, rmode, rcoef, rsig, x, mp, mq, y,
+                         step, sigma, hist, steps, act + nxt, tau_trace, r,
+                         tau_trace ? trace_rounds : 0, s, gate);
     const int slot = r % (kLag + 1);
-    if (e == hipSuccess) e = hipMemcpyAsync(&host_cnt[slot], cur, sizeof(int32_t), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(&host_act[slot], act + nxt, sizeof(int32_t), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipEventRecord(ev[slot], s);
     if (e != hipSuccess) {
       set_error("sd_run_sampler: launch failed in round %d: %s", r, hipGetErrorString(e));
       st = SD_EHIP;
       break;
     }
-    // look at the counter of round r - kLag (the queue keeps kLag rounds ahead)
     const int back = r - kLag;
     if (back >= 0) {
       const int bs = back % (kLag + 1);
@@ -442,35 +481,32 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
         st = SD_EHIP;
         break;
       }
-      if (host_cnt[bs] == 0) {
-        done = true;
-        rounds = back + 1;
-      }
+      if (host_act[bs] == 0) rounds = back + 1;
     }
   }
-  if (st == SD_OK && !done) {
-    // drain: find the first round whose counter read zero
+  if (st == SD_OK && rounds < 0) {
     for (int back = r - kLag < 0 ? 0 : r - kLag; back < r; ++back) {
       const int bs = back % (kLag + 1);
       (void)hipEventSynchronize(ev[bs]);
-      if (host_cnt[bs] == 0) {
-        done = true;
+      if (host_act[bs] == 0) {
         rounds = back + 1;
         break;
       }
     }
-    if (!done) {
+    if (rounds < 0) {
       set_error("sd_run_sampler: chains still active after %d rounds", r);
       st = SD_EHIP;
     }
   }
   if (st == SD_OK) {
-    hipError_t e = hipMemcpyAsync(y_out, y, sizeof(float) * (size_t)B * d, hipMemcpyDeviceToDevice, s);
-    int64_t h_hist[SD_MAX_BLOCK + 2];
-    int64_t h_steps = 0;
+    std::vector<int32_t> h_hist((size_t)B * (SD_MAX_BLOCK + 2));
+    std::vector<int64_t> h_steps(B);
     int32_t h_nan = 0;
-    if (e == hipSuccess) e = hipMemcpyAsync(h_hist, hist, sizeof(h_hist), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipMemcpyAsync(&h_steps, steps, sizeof(int64_t), hipMemcpyDeviceToHost, s);
+    hipError_t e = hipMemcpyAsync(y_out, y, sizeof(float) * (size_t)B * d, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(h_hist.data(), hist, sizeof(int32_t) * h_hist.size(), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(h_steps.data(), steps, sizeof(int64_t) * B, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipMemcpyAsync(&h_nan, nanflag, sizeof(int32_t), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
@@ -480,11 +516,11 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
       if (stats) {
         memset(stats, 0, sizeof(*stats));
         stats->rounds = rounds;
-        stats->steps = h_steps;
-        for (int i = 0; i < SD_MAX_BLOCK + 2; ++i) {
-          stats->tau_hist[i] = h_hist[i];
-          stats->chain_rounds += h_hist[i];
+        for (int b = 0; b < B; ++b) {
+          stats->steps += h_steps[b];
+          for (int i = 0; i < SD_MAX_BLOCK + 2; ++i) stats->tau_hist[i] += h_hist[(size_t)b * (SD_MAX_BLOCK + 2) + i];
         }
+        for (int i = 0; i < SD_MAX_BLOCK + 2; ++i) stats->chain_rounds += stats->tau_hist[i];
       }
       if (h_nan) {
         set_error("sd_run_sampler: non-finite log-ratio met");
@@ -494,7 +530,7 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
   }
   (void)hipStreamSynchronize(s);
   for (int i = 0; i <= kLag; ++i) (void)hipEventDestroy(ev[i]);
-  (void)hipHostFree(host_cnt);
+  (void)hipHostFree(host_act);
   return st;
 }
 
@@ -506,6 +542,12 @@ sd_status sd_profile_enable(int32_t on) {
     g_stats.clear();
   }
   g_prof = on != 0;
+  return SD_OK;
+}
+
+sd_status sd_profile_only(const char* name) {
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_only = name ? name : "";
   return SD_OK;
 }
 

@@ -12,7 +12,7 @@ namespace sd {
 void set_error(const char* fmt, ...);
 
 // ------------------------------------------------------------- profiling --
-bool prof_on();
+bool prof_on(const char* name);
 void prof_push(const char* name, hipEvent_t start, hipEvent_t stop);
 void prof_events(hipEvent_t* start, hipEvent_t* stop);
 
@@ -20,7 +20,7 @@ void prof_events(hipEvent_t* start, hipEvent_t* stop);
 // with events on the same stream.  Returns the launch error, if any.
 template <class F>
 hipError_t timed(const char* name, hipStream_t s, F&& launch) {
-  if (!prof_on()) {
+  if (!prof_on(name)) {
     launch();
     return hipGetLastError();
   }
@@ -69,9 +69,10 @@ struct Target {
   sd_precision prec;
   float* mu;      // [M][d]
   float* muT;     // [d][M]
-  double* var;    // [M]
   double* logw;   // [M]
   double* musq;   // [M] ||mu_m||^2 (float64 from the float32 means)
+  float4* coef;   // [N+1] per step: (c1_n, c2_n, sigma_n, 1/c2_n) rounded to float32
+  double2* ls;    // [N][M] per step and component: (log s2, 1/s2), s2 = a_n^2 var_m + 1 - a_n^2
   int device;
 };
 
@@ -82,11 +83,48 @@ hipError_t target_mean_launch(const Target& t, int rows, const float* x, int64_t
                               const int32_t* step, float* mq, int64_t ldq, float* score,
                               int64_t lds, void* ws, hipStream_t s, const int* gate);
 
+// The sampler's target call on its [B][K+1][d] block (x rows contiguous,
+// row stride d) that also leaves the verification's partial sums in
+// lrp[row][lr_tiles(t)][3] (see gmm_mean_lr_kernel); rnd = chains' rounds.
+hipError_t target_mean_lr_launch(const Target& t, int rows, int K1, const float* x,
+                                 const int32_t* step, float* mq, const float* mp, double* lrp,
+                                 const uint32_t* rnd, uint64_t seed, void* ws, hipStream_t s,
+                                 const int* gate);
+int lr_tiles(const Target& t);
+// Sampler verification on the fused partials (see scan_fused_kernel).
+hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, const double* lrp,
+                             int nct, const double* sigma, const int32_t* kcur,
+                             const uint32_t* rcur, uint64_t seed, const float* mp,
+                             const float* mq, int32_t* tau, int32_t* rmode, float* rcoef,
+                             float* rsig, int* nanflag, int* act_next, hipStream_t s,
+                             const int* gate);
+// Residual, commit and the next round's Free-Drafter block, elementwise over
+// (chain, four coordinates); per-chain state is read from the *cur arrays and
+// written to the *next arrays (round parity), so no workgroup races another.
+hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int d,
+                          uint64_t seed, const int32_t* kcur, const uint32_t* rcur,
+                          const int32_t* crow_cur, const int32_t* cstep_cur, int32_t* knext,
+                          uint32_t* rnext, int32_t* crow_next, int32_t* cstep_next,
+                          const int32_t* tau, const int32_t* rmode, const float* rcoef,
+                          const float* rsig, float* x, float* mp, const float* mq, float* y,
+                          int32_t* step, double* sigma, int32_t* hist, int64_t* steps,
+                          int* act_next, int32_t* trace, int r, int trace_rounds, hipStream_t s,
+                          const int* gate);
+
 // ---------------------------------------------------------------- kernels --
-hipError_t init_chains_launch(int B, int d, uint64_t seed, float* y, hipStream_t s);
+hipError_t init_chains_launch(int B, int d, uint64_t seed, float* y, float* x0, int64_t x0c,
+                              hipStream_t s);
 hipError_t draft_launch(const Sched& sc, int B, int K, int d, const float* y, const float* cs,
                         const int32_t* k, const uint32_t* rnd, uint64_t seed, float* x,
                         sd_stride xs, float* mp, sd_stride mps, hipStream_t s, const int* gate);
+// Draft whose cached score is recovered from row crow[b] of the previous
+// round's x / target means at step cstep[b] (the sampler's Free Drafter).
+hipError_t draft_cached_launch(const Sched& sc, const float4* coef, int B, int K, int d,
+                               const float* y,
+                               const int32_t* crow, const int32_t* cstep, const float* mqprev,
+                               sd_stride mqs, const int32_t* k, const uint32_t* rnd,
+                               uint64_t seed, float* x, sd_stride xs, float* mp, sd_stride mps,
+                               hipStream_t s, const int* gate);
 hipError_t verify_launch(int B, int K, int d, int mode, const float* yd, sd_stride ys,
                          const float* mp, sd_stride mps, const float* mq, sd_stride mqs,
                          const double* sigma, const int32_t* kb, const uint32_t* rnd,
@@ -97,17 +135,21 @@ hipError_t residual_launch(int B, int K, int d, const float* yd, sd_stride ys, c
                            sd_stride mps, const float* mq, sd_stride mqs, const double* sigma,
                            const int32_t* kb, const int32_t* left, const int32_t* tau,
                            const double* ures, const double* dn, const uint32_t* rnd,
-                           uint64_t seed, float* y, hipStream_t s, const int* gate);
+                           uint64_t seed, float* y, hipStream_t s);
 // Sampler-only kernels.
+hipError_t residual_commit_launch(int B, int K, int d, int N, const float* yd, sd_stride ys,
+                                  const float* mp, sd_stride mps, const float* mq, sd_stride mqs,
+                                  const double* sigma, const int32_t* kb, const int32_t* left,
+                                  const int32_t* tau, const double* ures, const double* dn,
+                                  uint32_t* rnd, uint64_t seed, float* y, int32_t* k,
+                                  int32_t* crow, int32_t* cstep, int32_t* adv, int32_t* trace,
+                                  int r, int trace_rounds, hipStream_t s, const int* gate);
 hipError_t fill_i32_launch(int32_t* p, int64_t n, int32_t v, hipStream_t s);
 hipError_t fill_i64_launch(int64_t* p, int64_t n, int64_t v, hipStream_t s);
 hipError_t prepare_launch(const Sched& sc, int B, int K, const int32_t* k, int32_t* kb,
-                          int32_t* left, int32_t* step, double* sigma, int* cnt_zero,
-                          hipStream_t s, const int* gate);
-hipError_t commit_launch(int B, int K, int d, int N, const int32_t* tau, const int32_t* kb,
-                         int32_t* k, uint32_t* rnd, const float* score, sd_stride ss,
-                         float* cache, int* cnt, int64_t* hist, int64_t* steps, int32_t* trace,
-                         int r, int trace_rounds, hipStream_t s, const int* gate);
+                          int32_t* left, int32_t* step, double* sigma, int32_t* tau,
+                          int32_t* adv, int* cnt_cur, int* cnt_next, int64_t* hist,
+                          int64_t* steps, hipStream_t s);
 hipError_t philox_words_launch(uint64_t seed, int n, const uint32_t* ctr, uint32_t* out,
                                hipStream_t s);
 hipError_t philox_normals_launch(uint64_t seed, uint32_t chain, uint32_t rnd, uint32_t tag,

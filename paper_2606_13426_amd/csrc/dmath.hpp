@@ -46,8 +46,16 @@ __device__ inline double log_ratio_below(double x, double la, double v) {
   return log_ndtr(x - v) - log_ndtr(x) - la;
 }
 
-// log(alpha Phi(x) - Phi(x - v)) for x <= u*.
+// log(alpha Phi(x) - Phi(x - v)) for x <= u*.  Below -1 both CDFs come from
+// one erfcx pair: log Phi(x) = log(erfcx(t1)/2) - t1^2 and the ratio above.
 __device__ inline double log_excess(double x, double la, double v) {
+  if (x < -1.0) {
+    const double t1 = -x * kSqrt1_2, t2 = -(x - v) * kSqrt1_2;
+    const double e1 = erfcx(t1), e2 = erfcx(t2);
+    const double us = la / v + 0.5 * v;
+    const double r = log(e2 / e1) + v * (x - us);
+    return la + log(0.5 * e1) - t1 * t1 + log1mexp(fmin(0.0, r));
+  }
   return la + log_ndtr(x) + log1mexp(fmin(0.0, log_ratio_below(x, la, v)));
 }
 

@@ -6,33 +6,15 @@
 // and every draft row and draft mean is written once (HBM-bound, no reuse).
 #include "common.hpp"
 #include "philox.hpp"
+#include "rows.hpp"
 
 namespace sd {
 namespace {
 
 constexpr int kThreads = 256;
 
-__device__ __forceinline__ void load4(const float* p, int cnt, bool vec, float (&v)[4]) {
-  if (vec) {
-    const float4 t = *reinterpret_cast<const float4*>(p);
-    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
-  } else {
-#pragma unroll
-    for (int c = 0; c < 4; ++c) v[c] = c < cnt ? p[c] : 0.0f;
-  }
-}
-
-__device__ __forceinline__ void store4(float* p, int cnt, bool vec, const float (&v)[4]) {
-  if (vec) {
-    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
-  } else {
-#pragma unroll
-    for (int c = 0; c < 4; ++c)
-      if (c < cnt) p[c] = v[c];
-  }
-}
-
-__global__ __launch_bounds__(kThreads) void init_chains_kernel(int d, uint64_t seed, float* y) {
+__global__ __launch_bounds__(kThreads) void init_chains_kernel(int d, uint64_t seed, float* y,
+                                                               float* x0, int64_t x0c) {
   const int b = blockIdx.y;
   const int g = blockIdx.x * kThreads + threadIdx.x;
   const int e0 = 4 * g;
@@ -41,13 +23,27 @@ __global__ __launch_bounds__(kThreads) void init_chains_kernel(int d, uint64_t s
   float* p = y + (int64_t)b * d + e0;
   const int cnt = min(4, d - e0);
   for (int c = 0; c < cnt; ++c) p[c] = get4(z, c);
+  if (x0) {
+    float* q = x0 + (int64_t)b * x0c + e0;
+    for (int c = 0; c < cnt; ++c) q[c] = get4(z, c);
+  }
 }
 
+// Draft block of one chain, four coordinates per thread.  The cached target
+// score enters only as c2_n S_c.  With CACHE_FROM_MEANS the score is not
+// stored: it is the score behind the target mean m^q_c = c1_c x_c + c2_c S_c
+// of row crow of the previous round (step cstep), so
+//   c2_n S_c = (c2_n / c2_c) (m^q_c - c1_c x_c),
+// read from the same x / mq buffers before this chain's rows are overwritten
+// (each thread reads and then writes only its own coordinates).
+template <bool CACHE_FROM_MEANS>
 __global__ __launch_bounds__(kThreads) void draft_kernel(
-    Sched sc, int K, int d, const float* __restrict__ y, const float* __restrict__ cs,
-    const int32_t* __restrict__ kk, const uint32_t* __restrict__ rnd, uint64_t seed,
-    float* __restrict__ x, int64_t xc, int64_t xr, float* __restrict__ mp, int64_t mc,
-    int64_t mr, bool vec_ok, const int* gate) {
+    Sched sc, const float4* __restrict__ coef, int K, int d, const float* __restrict__ y,
+    const float* __restrict__ cs,
+    const int32_t* __restrict__ crow, const int32_t* __restrict__ cstep,
+    const float* __restrict__ mqprev, int64_t qc, int64_t qr, const int32_t* __restrict__ kk,
+    const uint32_t* __restrict__ rnd, uint64_t seed, float* __restrict__ x, int64_t xc,
+    int64_t xr, float* __restrict__ mp, int64_t mc, int64_t mr, bool vec_ok, const int* gate) {
   if (gate && *gate == 0) return;
   const int b = blockIdx.y;
   const int g = blockIdx.x * kThreads + threadIdx.x;
@@ -59,48 +55,68 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(
   const uint32_t r = rnd[b];
   const int cnt = min(4, d - e0);
   const bool vec = vec_ok && cnt == 4;
-  float yv[4], sv[4], m[4];
-  load4(y + (int64_t)b * d + e0, cnt, vec, yv);
-  load4(cs + (int64_t)b * d + e0, cnt, vec, sv);
+  float yv[4], sv[4];
   float* xb = x + (int64_t)b * xc + e0;
   float* mb = mp + (int64_t)b * mc + e0;
-  store4(xb, cnt, vec, yv);
-  for (int i = 1; i <= kb; ++i) {
-    const int n = k + i - 1;
-    const float c1 = (float)sched_c1(sc, n);
-    const float c2 = (float)sched_c2(sc, n);
-    const float sg = (float)sched_sigma(sc, n);
-    const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, (TAG_DRAFT << 24) | (uint32_t)i, seed));
+  load4(y + (int64_t)b * d + e0, cnt, vec, yv);
+  float scale = 1.0f;
+  if (CACHE_FROM_MEANS) {
+    const int cr = crow[b];
+    const float4 cc = step_coef(sc, coef, cstep[b]);
+    float xcv[4], qcv[4];
+    load4(xb + (int64_t)cr * xr, cnt, vec, xcv);
+    load4(mqprev + (int64_t)b * qc + (int64_t)cr * qr + e0, cnt, vec, qcv);
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      m[c] = c1 * yv[c] + c2 * sv[c];
-      yv[c] = m[c] + sg * get4(z, c);
-    }
-    store4(mb + (int64_t)(i - 1) * mr, cnt, vec, m);
-    store4(xb + (int64_t)i * xr, cnt, vec, yv);
+    for (int c = 0; c < 4; ++c) sv[c] = qcv[c] - cc.x * xcv[c];  // c2_c S_c
+    scale = cc.w;
+  } else {
+    load4(cs + (int64_t)b * d + e0, cnt, vec, sv);
   }
-  // rows past the valid block repeat the last draft / mean, so every row the
-  // target call reads is finite
-  for (int i = kb + 1; i <= K; ++i) {
-    store4(mb + (int64_t)(i - 1) * mr, cnt, vec, m);
-    store4(xb + (int64_t)i * xr, cnt, vec, yv);
-  }
+  store4(xb, cnt, vec, yv);
+  draft_rows(sc, coef, K, k, kb, (uint32_t)b, r, seed, g, yv, sv, scale, xb, xr, mb, mr, cnt, vec);
 }
 
-// One thread per chain: the block size K_b, the steps left, the step index of
-// every target row and sigma_{k+j} for j = 0..K; thread 0 also clears this
-// round's active-chain counter.
-__global__ __launch_bounds__(kThreads) void prepare_kernel(Sched sc, int B, int K,
-                                                           const int32_t* __restrict__ kk,
-                                                           int32_t* kb, int32_t* left,
-                                                           int32_t* step, double* sigma,
-                                                           int* cnt_zero, const int* gate) {
+// One thread per chain, at the start of a round:
+//  * books the previous round's outcome (tau histogram, steps advanced) and
+//    clears it, so that a round is counted exactly once;
+//  * counts the chains still active (a ballot per wavefront) into cnt_cur,
+//    which gates every later kernel of the round, and clears the next slot;
+//  * writes the block size K_b, the steps left, the step index of every
+//    target row and sigma_{k+j} for j = 0..K.
+__global__ __launch_bounds__(kThreads) void prepare_kernel(
+    Sched sc, int B, int K, const int32_t* __restrict__ kk, int32_t* kb, int32_t* left,
+    int32_t* step, double* sigma, int32_t* tau, int32_t* adv, int* cnt_cur, int* cnt_next,
+    int64_t* hist, int64_t* steps) {
+  __shared__ int h[SD_MAX_BLOCK + 2];
+  for (int i = threadIdx.x; i < SD_MAX_BLOCK + 2; i += kThreads) h[i] = 0;
+  __syncthreads();
   const int b = blockIdx.x * kThreads + threadIdx.x;
-  if (b == 0) *cnt_zero = 0;
-  if (gate && *gate == 0) return;
-  if (b >= B) return;
-  const int k = kk[b];
-  kb[b] = k < sc.N ? min(K, sc.N - k) : 0;
+  if (b == 0) *cnt_next = 0;
+  const bool in = b < B;
+  const int t = in ? tau[b] : 0;
+  const int a = in ? adv[b] : 0;
+  const int k = in ? kk[b] : sc.N;
+  if (in) {
+    if (t > 0 && t < SD_MAX_BLOCK + 2) atomicAdd(&h[t], 1);
+    tau[b] = 0;
+    adv[b] = 0;
+  }
+  unsigned long long sa = (unsigned long long)a;
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) sa += __shfl_xor(sa, o);
+  const uint64_t act = __ballot(in && k < sc.N);
+  if ((threadIdx.x & 63) == 0) {
+    if (act) atomicAdd(cnt_cur, __popcll(act));
+    if (sa) atomicAdd((unsigned long long*)steps, sa);
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < SD_MAX_BLOCK + 2; i += kThreads)
+    if (h[i]) atomicAdd((unsigned long long*)&hist[i], (unsigned long long)h[i]);
+  if (!in || k >= sc.N) {
+    if (in) kb[b] = 0;
+    return;
+  }
+  kb[b] = min(K, sc.N - k);
   left[b] = sc.N - k;
   for (int j = 0; j <= K; ++j) {
     step[(int64_t)b * (K + 1) + j] = min(k + j, sc.N - 1);
@@ -139,10 +155,18 @@ __global__ void philox_normals_kernel(uint64_t seed, uint32_t chain, uint32_t rn
 
 }  // namespace
 
-hipError_t init_chains_launch(int B, int d, uint64_t seed, float* y, hipStream_t s) {
+hipError_t init_chains_launch(int B, int d, uint64_t seed, float* y, float* x0, int64_t x0c,
+                              hipStream_t s) {
   const int ng = (d + 3) / 4;
   dim3 grid((ng + kThreads - 1) / kThreads, B);
-  return timed("init_chains", s, [&] { init_chains_kernel<<<grid, kThreads, 0, s>>>(d, seed, y); });
+  return timed("init_chains", s,
+               [&] { init_chains_kernel<<<grid, kThreads, 0, s>>>(d, seed, y, x0, x0c); });
+}
+
+static bool draft_vec(int d, sd_stride xs, sd_stride mps, const float* y, const float* x,
+                      const float* mp) {
+  return (d % 4 == 0) && (xs.chain % 4 == 0) && (xs.row % 4 == 0) && (mps.chain % 4 == 0) &&
+         (mps.row % 4 == 0) && aligned16(y) && aligned16(x) && aligned16(mp);
 }
 
 hipError_t draft_launch(const Sched& sc, int B, int K, int d, const float* y, const float* cs,
@@ -150,21 +174,39 @@ hipError_t draft_launch(const Sched& sc, int B, int K, int d, const float* y, co
                         sd_stride xs, float* mp, sd_stride mps, hipStream_t s, const int* gate) {
   const int ng = (d + 3) / 4;
   dim3 grid((ng + kThreads - 1) / kThreads, B);
-  const bool vec = (d % 4 == 0) && (xs.chain % 4 == 0) && (xs.row % 4 == 0) &&
-                   (mps.chain % 4 == 0) && (mps.row % 4 == 0) && aligned16(y) &&
-                   aligned16(cs) && aligned16(x) && aligned16(mp);
+  const bool vec = draft_vec(d, xs, mps, y, x, mp) && aligned16(cs);
   return timed("draft_block", s, [&] {
-    draft_kernel<<<grid, kThreads, 0, s>>>(sc, K, d, y, cs, k, rnd, seed, x, xs.chain, xs.row,
-                                           mp, mps.chain, mps.row, vec, gate);
+    draft_kernel<false><<<grid, kThreads, 0, s>>>(sc, nullptr, K, d, y, cs, nullptr, nullptr, nullptr, 0, 0,
+                                                  k, rnd, seed, x, xs.chain, xs.row, mp, mps.chain,
+                                                  mps.row, vec, gate);
+  });
+}
+
+hipError_t draft_cached_launch(const Sched& sc, const float4* coef, int B, int K, int d,
+                               const float* y,
+                               const int32_t* crow, const int32_t* cstep, const float* mqprev,
+                               sd_stride mqs, const int32_t* k, const uint32_t* rnd,
+                               uint64_t seed, float* x, sd_stride xs, float* mp, sd_stride mps,
+                               hipStream_t s, const int* gate) {
+  const int ng = (d + 3) / 4;
+  dim3 grid((ng + kThreads - 1) / kThreads, B);
+  const bool vec = draft_vec(d, xs, mps, y, x, mp) && aligned16(mqprev) && mqs.chain % 4 == 0 &&
+                   mqs.row % 4 == 0;
+  return timed("draft_block", s, [&] {
+    draft_kernel<true><<<grid, kThreads, 0, s>>>(sc, coef, K, d, y, nullptr, crow, cstep, mqprev,
+                                                 mqs.chain, mqs.row, k, rnd, seed, x, xs.chain,
+                                                 xs.row, mp, mps.chain, mps.row, vec, gate);
   });
 }
 
 hipError_t prepare_launch(const Sched& sc, int B, int K, const int32_t* k, int32_t* kb,
-                          int32_t* left, int32_t* step, double* sigma, int* cnt_zero,
-                          hipStream_t s, const int* gate) {
+                          int32_t* left, int32_t* step, double* sigma, int32_t* tau,
+                          int32_t* adv, int* cnt_cur, int* cnt_next, int64_t* hist,
+                          int64_t* steps, hipStream_t s) {
   const int nb = (B + kThreads - 1) / kThreads;
   return timed("prepare_round", s, [&] {
-    prepare_kernel<<<nb, kThreads, 0, s>>>(sc, B, K, k, kb, left, step, sigma, cnt_zero, gate);
+    prepare_kernel<<<nb, kThreads, 0, s>>>(sc, B, K, k, kb, left, step, sigma, tau, adv, cnt_cur,
+                                           cnt_next, hist, steps);
   });
 }
 

@@ -25,8 +25,10 @@ __device__ __forceinline__ uint4 philox(uint32_t c0, uint32_t c1, uint32_t c2, u
   uint32_t k0 = (uint32_t)seed, k1 = (uint32_t)(seed >> 32);
 #pragma unroll
   for (int r = 0; r < 10; ++r) {
-    const uint32_t lo0 = 0xD2511F53u * c0, hi0 = __umulhi(0xD2511F53u, c0);
-    const uint32_t lo1 = 0xCD9E8D57u * c2, hi1 = __umulhi(0xCD9E8D57u, c2);
+    // one 32x32 -> 64-bit product per multiplier (a single v_mad_u64_u32)
+    const uint64_t p0 = (uint64_t)0xD2511F53u * c0, p1 = (uint64_t)0xCD9E8D57u * c2;
+    const uint32_t lo0 = (uint32_t)p0, hi0 = (uint32_t)(p0 >> 32);
+    const uint32_t lo1 = (uint32_t)p1, hi1 = (uint32_t)(p1 >> 32);
     const uint32_t n0 = hi1 ^ c1 ^ k0, n2 = hi0 ^ c3 ^ k1;
     c0 = n0;
     c1 = lo1;
@@ -47,16 +49,30 @@ __device__ __forceinline__ double uniform64(uint32_t w) {
   return ((double)(w >> 8) + 0.5) * 0x1p-24;
 }
 
-// Box-Muller on (w0, w1) and (w2, w3).  The radius is computed from the exact
-// float64 uniform (its float32 rounding would map 1 - 2^-25 to 1 and lose the
-// small-radius tail); the angle 2 pi u uses sincospi in float32.
+// -2 ln u for the 24-bit uniform u = (m + 0.5) 2^-24 of word w, in float32
+// without losing the small-radius tail.  For u < 1/2, u is exact in float32.
+// For u >= 1/2, t = 1 - u = (2^24 - 1 - m + 0.5) 2^-24 is exact, w = fl(1 - t)
+// and ln u = ln w + (u - w)/w with u - w = -((w - 1) + t) exact, so one logf
+// serves both halves (no divergent branch).
+__device__ __forceinline__ float neg2log_u24(uint32_t w) {
+  const uint32_t m = w >> 8;
+  const bool hi = m >= (1u << 23);
+  const float t = ((float)((1u << 24) - 1u - m) + 0.5f) * 0x1p-24f;
+  const float wv = hi ? 1.0f - t : ((float)m + 0.5f) * 0x1p-24f;
+  const float corr = hi ? -((wv - 1.0f) + t) / wv : 0.0f;
+  return -2.0f * (logf(wv) + corr);
+}
+
+// Box-Muller on (w0, w1) and (w2, w3): radius sqrt(-2 ln u_a), angle 2 pi u_b.
+// The hardware sine and cosine take their argument in revolutions, so they
+// evaluate sin(2 pi u_b), cos(2 pi u_b) directly on u_b in (0, 1).
 __device__ __forceinline__ float4 normals4(uint4 w) {
-  const float ra = sqrtf((float)(-2.0 * log(uniform64(w.x))));
-  const float rc = sqrtf((float)(-2.0 * log(uniform64(w.z))));
-  float sa, ca, sc, cc;
-  sincospif(((float)(w.y >> 8) + 0.5f) * 0x1p-23f, &sa, &ca);
-  sincospif(((float)(w.w >> 8) + 0.5f) * 0x1p-23f, &sc, &cc);
-  return make_float4(ra * ca, ra * sa, rc * cc, rc * sc);
+  const float ra = sqrtf(neg2log_u24(w.x));
+  const float rc = sqrtf(neg2log_u24(w.z));
+  const float ub = ((float)(w.y >> 8) + 0.5f) * 0x1p-24f;
+  const float ud = ((float)(w.w >> 8) + 0.5f) * 0x1p-24f;
+  return make_float4(ra * __builtin_amdgcn_cosf(ub), ra * __builtin_amdgcn_sinf(ub),
+                     rc * __builtin_amdgcn_cosf(ud), rc * __builtin_amdgcn_sinf(ud));
 }
 
 __device__ __forceinline__ float get4(const float4& v, int i) {

@@ -6,16 +6,18 @@
 //     y = m^q + sigma (U e + G - e (e.G)),  e = (m^p - m^q) / (sigma ||Delta||),
 // rewritten per coordinate as  y_i = mq_i + sigma G_i + c (mp_i - mq_i)  with
 // c = (U - e.G)/||Delta||, so one float64 reduction (e.G) followed by one
-// elementwise pass suffices; G is regenerated from Philox in both passes
-// instead of being stored.
+// elementwise pass suffices; G and the two rows stay in registers between the
+// passes (up to 512 threads x 4 groups of 4 coordinates).
 #include "common.hpp"
 #include "philox.hpp"
 
 namespace sd {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kMaxThreads = 512;
+constexpr int kKeep = 4;  // float4 groups per thread kept in registers (d <= 8192)
 
+// Sum over the workgroup (blockDim.x a multiple of 64, at most 512).
 __device__ __forceinline__ double block_sum(double v, double* red) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o);
@@ -23,55 +25,108 @@ __device__ __forceinline__ double block_sum(double v, double* red) {
   if (lane == 0) red[w] = v;
   __syncthreads();
   double t = 0.0;
-  for (int i = 0; i < kThreads / 64; ++i) t += red[i];
+  for (int i = 0; i < (int)(blockDim.x >> 6); ++i) t += red[i];
   return t;
 }
 
-__global__ __launch_bounds__(kThreads) void residual_kernel(
-    int K, int d, const float* __restrict__ yd, int64_t yc, int64_t yr,
+__device__ __forceinline__ void ld4(const float* p, int cnt, float (&v)[4]) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v[c] = c < cnt ? p[c] : 0.0f;
+}
+
+// The rejection case: one pass reads m^q, m^p and draws G for this thread's
+// groups (kept in registers), reduces e.G, and the second pass writes
+// y = m^q + sigma G + c (m^p - m^q) from the registers.  Groups beyond
+// kKeep * blockDim.x (d > 8192) are re-read and redrawn in the second pass.
+__device__ void decomposition_row(int b, int d, uint32_t r, uint64_t seed, const float* p,
+                                  const float* q, double s, double v, double U, float* out,
+                                  double* red) {
+  const int ng = (d + 3) / 4;
+  const int nt = blockDim.x;
+  const uint32_t c3 = TAG_RESID << 24;
+  float gq[kKeep][4], gd[kKeep][4], gz[kKeep][4];
+  double acc = 0.0;
+#pragma unroll
+  for (int i = 0; i < kKeep; ++i) {
+    const int g = threadIdx.x + i * nt;
+    if (g < ng) {
+      const int e0 = 4 * g, cnt = min(4, d - e0);
+      const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, c3, seed));
+      float pv[4];
+      ld4(p + e0, cnt, pv);
+      ld4(q + e0, cnt, gq[i]);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        gz[i][c] = get4(z, c);
+        gd[i][c] = pv[c] - gq[i][c];
+        if (c < cnt) acc += ((double)pv[c] - (double)gq[i][c]) * (double)gz[i][c];
+      }
+    }
+  }
+  for (int g = threadIdx.x + kKeep * nt; g < ng; g += nt) {
+    const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, c3, seed));
+    const int e0 = 4 * g, cnt = min(4, d - e0);
+    for (int c = 0; c < cnt; ++c) acc += ((double)p[e0 + c] - (double)q[e0 + c]) * (double)get4(z, c);
+  }
+  const double eG = block_sum(acc, red) / (s * v);
+  const float coef = (float)((U - eG) / v);
+  const float sf = (float)s;
+#pragma unroll
+  for (int i = 0; i < kKeep; ++i) {
+    const int g = threadIdx.x + i * nt;
+    if (g < ng) {
+      const int e0 = 4 * g, cnt = min(4, d - e0);
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (c < cnt) out[e0 + c] = gq[i][c] + sf * gz[i][c] + coef * gd[i][c];
+    }
+  }
+  for (int g = threadIdx.x + kKeep * nt; g < ng; g += nt) {
+    const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, c3, seed));
+    const int e0 = 4 * g, cnt = min(4, d - e0);
+    for (int c = 0; c < cnt; ++c) {
+      const float qi = q[e0 + c];
+      out[e0 + c] = qi + sf * get4(z, c) + coef * (p[e0 + c] - qi);
+    }
+  }
+}
+
+// With COMMIT (the sampler) the same workgroup then advances the chain:
+// k <- min(k + tau, N), round <- round + 1, and records where the Free Drafter
+// finds its cached score next round (row min(tau, K_b) of this round's target
+// means, at step k + min(tau, K_b)) and how many steps the chain advanced.
+template <bool COMMIT>
+__global__ __launch_bounds__(kMaxThreads) void residual_kernel(
+    int B, int K, int d, int N, const float* __restrict__ yd, int64_t yc, int64_t yr,
     const float* __restrict__ mp, int64_t pc, int64_t pr, const float* __restrict__ mq,
     int64_t qc, int64_t qr, const double* __restrict__ sigma, const int32_t* __restrict__ kbv,
     const int32_t* __restrict__ left, const int32_t* __restrict__ tauv,
-    const double* __restrict__ ures, const double* __restrict__ dn,
-    const uint32_t* __restrict__ rnd, uint64_t seed, float* __restrict__ y, const int* gate) {
+    const double* __restrict__ ures, const double* __restrict__ dn, uint32_t* rnd, uint64_t seed,
+    float* __restrict__ y, int32_t* kk, int32_t* crow, int32_t* cstep, int32_t* adv,
+    int32_t* trace, int r_round, int trace_rounds, const int* gate) {
+  __shared__ double red[kMaxThreads / 64];
   if (gate && *gate == 0) return;
   const int b = blockIdx.x;
   const int t = tauv[b];
   const int kb = min(kbv[b], K);
-  if (t <= 0 || kb <= 0 || t > kb + 1) return;
+  if (t <= 0 || kb <= 0 || t > kb + 1) {
+    if (COMMIT && threadIdx.x == 0 && trace && r_round < trace_rounds)
+      trace[(int64_t)r_round * B + b] = 0;
+    return;
+  }
   const uint32_t r = rnd[b];
   float* out = y + (int64_t)b * d;
   const int ng = (d + 3) / 4;
   if (t <= kb) {
-    const float* p = mp + (int64_t)b * pc + (int64_t)(t - 1) * pr;
-    const float* q = mq + (int64_t)b * qc + (int64_t)(t - 1) * qr;
-    const double s = sigma[(int64_t)b * (K + 1) + (t - 1)];
-    const double v = dn[(int64_t)b * K + (t - 1)];
-    const uint32_t c3 = TAG_RESID << 24;
-    double acc = 0.0;
-    for (int g = threadIdx.x; g < ng; g += kThreads) {
-      const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, c3, seed));
-      const int e0 = 4 * g, cnt = min(4, d - e0);
-      for (int c = 0; c < cnt; ++c)
-        acc += ((double)p[e0 + c] - (double)q[e0 + c]) * (double)get4(z, c);
-    }
-    __shared__ double red[kThreads / 64];
-    const double eG = block_sum(acc, red) / (s * v);
-    const float coef = (float)((ures[b] - eG) / v);
-    const float sf = (float)s;
-    for (int g = threadIdx.x; g < ng; g += kThreads) {
-      const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, c3, seed));
-      const int e0 = 4 * g, cnt = min(4, d - e0);
-      for (int c = 0; c < cnt; ++c) {
-        const float qi = q[e0 + c];
-        out[e0 + c] = qi + sf * get4(z, c) + coef * (p[e0 + c] - qi);
-      }
-    }
+    decomposition_row(b, d, r, seed, mp + (int64_t)b * pc + (int64_t)(t - 1) * pr,
+                      mq + (int64_t)b * qc + (int64_t)(t - 1) * qr,
+                      sigma[(int64_t)b * (K + 1) + (t - 1)], dn[(int64_t)b * K + (t - 1)], ures[b],
+                      out, red);
   } else if (kb + 1 <= left[b]) {
     // full accept: draw Y_{k+K_b+1} from the target kernel at the last draft
     const float* q = mq + (int64_t)b * qc + (int64_t)kb * qr;
     const float sf = (float)sigma[(int64_t)b * (K + 1) + kb];
-    for (int g = threadIdx.x; g < ng; g += kThreads) {
+    for (int g = threadIdx.x; g < ng; g += blockDim.x) {
       const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, TAG_TARGET << 24, seed));
       const int e0 = 4 * g, cnt = min(4, d - e0);
       for (int c = 0; c < cnt; ++c) out[e0 + c] = q[e0 + c] + sf * get4(z, c);
@@ -79,42 +134,29 @@ __global__ __launch_bounds__(kThreads) void residual_kernel(
   } else {
     // the block reached step N: the last draft is Y_N
     const float* src = yd + (int64_t)b * yc + (int64_t)(kb - 1) * yr;
-    for (int i = threadIdx.x; i < d; i += kThreads) out[i] = src[i];
+    for (int i = threadIdx.x; i < d; i += blockDim.x) out[i] = src[i];
+  }
+  if (COMMIT) {
+    __syncthreads();  // every thread has read rnd[b] before it changes
+    if (threadIdx.x == 0) {
+      const int k = kk[b];
+      const int knew = min(k + t, N);
+      const int cr = min(t, kb);
+      kk[b] = knew;
+      rnd[b] = r + 1u;
+      crow[b] = cr;
+      cstep[b] = min(k + cr, N - 1);
+      adv[b] = knew - k;
+      if (trace && r_round < trace_rounds) trace[(int64_t)r_round * B + b] = t;
+    }
   }
 }
 
-// Advance k, the round counter and the Free-Drafter cache (the target score
-// of row min(tau, K_b) of this round), count the chains still active and
-// record tau.
-__global__ __launch_bounds__(kThreads) void commit_kernel(
-    int B, int K, int d, int N, const int32_t* __restrict__ tauv, const int32_t* __restrict__ kbv,
-    int32_t* kk, uint32_t* rnd, const float* __restrict__ score, int64_t sc, int64_t sr,
-    float* __restrict__ cache, int* cnt, int64_t* hist, int64_t* steps, int32_t* trace, int r,
-    int trace_rounds, const int* gate) {
-  if (gate && *gate == 0) return;
-  const int b = blockIdx.x;
-  const int t = tauv[b];
-  const int kb = min(kbv[b], K);
-  if (t <= 0 || t > kb + 1) {
-    if (threadIdx.x == 0 && trace && r < trace_rounds) trace[(int64_t)r * B + b] = 0;
-    return;
-  }
-  const int k = kk[b];
-  const int knew = min(k + t, N);
-  if (knew < N) {
-    const float* src = score + (int64_t)b * sc + (int64_t)min(t, kb) * sr;
-    float* dst = cache + (int64_t)b * d;
-    for (int i = threadIdx.x; i < d; i += kThreads) dst[i] = src[i];
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    kk[b] = knew;
-    rnd[b] = rnd[b] + 1u;
-    if (knew < N) atomicAdd(cnt, 1);
-    atomicAdd((unsigned long long*)&hist[t], 1ull);
-    atomicAdd((unsigned long long*)steps, (unsigned long long)(knew - k));
-    if (trace && r < trace_rounds) trace[(int64_t)r * B + b] = t;
-  }
+// Threads per workgroup: one float4 group per thread up to 512 threads.
+inline int residual_threads(int d) {
+  const int ng = (d + 3) / 4;
+  const int t = ((ng + 63) / 64) * 64;
+  return t < kMaxThreads ? t : kMaxThreads;
 }
 
 }  // namespace
@@ -123,21 +165,26 @@ hipError_t residual_launch(int B, int K, int d, const float* yd, sd_stride ys, c
                            sd_stride mps, const float* mq, sd_stride mqs, const double* sigma,
                            const int32_t* kb, const int32_t* left, const int32_t* tau,
                            const double* ures, const double* dn, const uint32_t* rnd,
-                           uint64_t seed, float* y, hipStream_t s, const int* gate) {
+                           uint64_t seed, float* y, hipStream_t s) {
   return timed("residual_draw", s, [&] {
-    residual_kernel<<<B, kThreads, 0, s>>>(K, d, yd, ys.chain, ys.row, mp, mps.chain, mps.row, mq,
-                                           mqs.chain, mqs.row, sigma, kb, left, tau, ures, dn,
-                                           rnd, seed, y, gate);
+    residual_kernel<false><<<B, residual_threads(d), 0, s>>>(
+        B, K, d, 0, yd, ys.chain, ys.row, mp, mps.chain, mps.row, mq, mqs.chain, mqs.row, sigma,
+        kb, left, tau, ures, dn, const_cast<uint32_t*>(rnd), seed, y, nullptr, nullptr, nullptr,
+        nullptr, nullptr, 0, 0, nullptr);
   });
 }
 
-hipError_t commit_launch(int B, int K, int d, int N, const int32_t* tau, const int32_t* kb,
-                         int32_t* k, uint32_t* rnd, const float* score, sd_stride ss,
-                         float* cache, int* cnt, int64_t* hist, int64_t* steps, int32_t* trace,
-                         int r, int trace_rounds, hipStream_t s, const int* gate) {
-  return timed("commit", s, [&] {
-    commit_kernel<<<B, kThreads, 0, s>>>(B, K, d, N, tau, kb, k, rnd, score, ss.chain, ss.row,
-                                         cache, cnt, hist, steps, trace, r, trace_rounds, gate);
+hipError_t residual_commit_launch(int B, int K, int d, int N, const float* yd, sd_stride ys,
+                                  const float* mp, sd_stride mps, const float* mq, sd_stride mqs,
+                                  const double* sigma, const int32_t* kb, const int32_t* left,
+                                  const int32_t* tau, const double* ures, const double* dn,
+                                  uint32_t* rnd, uint64_t seed, float* y, int32_t* k,
+                                  int32_t* crow, int32_t* cstep, int32_t* adv, int32_t* trace,
+                                  int r, int trace_rounds, hipStream_t s, const int* gate) {
+  return timed("residual_commit", s, [&] {
+    residual_kernel<true><<<B, residual_threads(d), 0, s>>>(
+        B, K, d, N, yd, ys.chain, ys.row, mp, mps.chain, mps.row, mq, mqs.chain, mqs.row, sigma,
+        kb, left, tau, ures, dn, rnd, seed, y, k, crow, cstep, adv, trace, r, trace_rounds, gate);
   });
 }
 

@@ -14,7 +14,8 @@
 // coin, and a ballot gives tau.  U is found by inverting Psi_alpha: the
 // doubling of Alg. 7 is done for all 64 candidate lower ends at once (lane i
 // tests u* - 2^i), and the bisection becomes a 64-way multisection that
-// shrinks the bracket 65-fold per step until it collapses in float64.
+// shrinks the bracket 65-fold per step until it is 1e-13 (relative) wide or
+// has collapsed in float64.
 #include "common.hpp"
 #include "dmath.hpp"
 #include "philox.hpp"
@@ -119,7 +120,7 @@ __device__ double usample_exact(double u, double la, double v, int lane) {
   if (~above == 0ull) hi = us - ldexp(1.0, 62);
   for (int it = 0; it < 64; ++it) {
     const double mid = 0.5 * (lo + hi);
-    if (!(mid > lo && mid < hi)) break;
+    if (!(mid > lo && mid < hi) || hi - lo <= 1e-13 * fmax(1.0, fabs(lo))) break;
     const double x = lo + (hi - lo) * ((double)(lane + 1) / 65.0);
     const uint64_t below = __ballot(log_cdf(x, la, v, us, Lstar) < logu);
     const int cnt = __popcll(below);
@@ -151,6 +152,60 @@ __device__ double usample_paper(double u, double la, double v) {
   return mid;
 }
 
+// The acceptance decision of one chain (one wavefront; lane j-1 holds ell_j
+// and ||Delta_j|| of draft step j, kb valid steps): prefix recursion, h_j,
+// coins, tau, alpha_res and, when tau <= kb, the U draw of Alg. 7.
+struct Decision {
+  int tau;
+  double la_res, U;
+  uint64_t coins;
+};
+
+__device__ Decision decide(int mode, int umode, int kb, double ell, double vn, uint32_t b,
+                           uint32_t r, uint64_t seed, int lane) {
+  const bool valid = lane < kb;
+  // prefix recursion, replayed per lane in the definition's order
+  double acc = 0.0, la = 0.0;
+  for (int i = 0; i < kb; ++i) {
+    const double e = __shfl(ell, i);
+    acc = fmin(0.0, acc + e);
+    if (i == lane) la = acc;
+  }
+  const double vnext = __shfl_down(vn, 1);
+  double lh;
+  if (mode == SD_BLOCK)
+    lh = (lane + 1 < kb) ? block_log_h(la, vnext) : la;
+  else
+    lh = fmin(0.0, ell);
+  const uint4 w = philox((uint32_t)(lane >> 2), b, r, TAG_COIN << 24, seed);
+  const double eta = uniform64(pick(w, lane & 3));
+  const uint64_t cm = __ballot(valid && log(eta) < lh);
+  const uint64_t vmask = kb >= 64 ? ~0ull : ((1ull << kb) - 1ull);
+  int t;
+  if (mode == SD_BLOCK) {
+    t = cm ? (64 - __clzll((long long)cm)) + 1 : 1;
+  } else {
+    const uint64_t rej = ~cm & vmask;
+    t = rej ? __ffsll((unsigned long long)rej) : kb + 1;
+  }
+  const double la_prev = __shfl(la, t >= 2 ? t - 2 : 0);
+  const double la_res = (mode == SD_BLOCK && t >= 2) ? la_prev : 0.0;
+  double U = NAN;
+  if (t <= kb) {
+    const double v = __shfl(vn, t - 1);  // > 0: a rejection never lands on a zero offset
+    const uint4 wu = philox(0u, b, r, TAG_USAMPLE << 24, seed);
+    const double u = uniform64(wu.x);
+    if (umode == SD_USAMPLE_PAPER) {
+      double up = 0.0;
+      if (lane == 0) up = usample_paper(u, la_res, v);
+      U = __shfl(up, 0);
+    } else {
+      U = usample_exact(u, la_res, v, lane);
+    }
+  }
+  return Decision{t, la_res, U, cm};
+}
+
 __global__ __launch_bounds__(kThreads) void scan_kernel(
     int B, int K, int mode, int umode, const double* __restrict__ dn,
     const double* __restrict__ lr, const int32_t* __restrict__ kbv,
@@ -176,51 +231,84 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(
   const double vn = valid ? dn[(int64_t)b * K + lane] : 0.0;
   if (nanflag && __ballot(valid && !(isfinite(ell) && isfinite(vn))) != 0ull && lane == 0)
     atomicOr(nanflag, 1);
-  // prefix recursion, replayed per lane in the definition's order
-  double acc = 0.0, la = 0.0;
-  for (int i = 0; i < kb; ++i) {
-    const double e = __shfl(ell, i);
-    acc = fmin(0.0, acc + e);
-    if (i == lane) la = acc;
+  const Decision D = decide(mode, umode, kb, ell, vn, (uint32_t)b, rnd[b], seed, lane);
+  if (lane == 0) {
+    tau[b] = D.tau;
+    lar[b] = D.la_res;
+    ures[b] = D.U;
+    if (coins) coins[b] = D.coins;
   }
-  const double vnext = __shfl_down(vn, 1);
-  double lh;
-  if (mode == SD_BLOCK)
-    lh = (lane + 1 < kb) ? block_log_h(la, vnext) : la;
-  else
-    lh = fmin(0.0, ell);
-  const uint32_t r = rnd[b];
-  const uint4 w = philox((uint32_t)(lane >> 2), (uint32_t)b, r, TAG_COIN << 24, seed);
-  const double eta = uniform64(pick(w, lane & 3));
-  const uint64_t cm = __ballot(valid && log(eta) < lh);
-  const uint64_t vmask = kb >= 64 ? ~0ull : ((1ull << kb) - 1ull);
-  int t;
-  if (mode == SD_BLOCK) {
-    t = cm ? (64 - __clzll((long long)cm)) + 1 : 1;
-  } else {
-    const uint64_t rej = ~cm & vmask;
-    t = rej ? __ffsll((unsigned long long)rej) : kb + 1;
-  }
-  const double la_prev = __shfl(la, t >= 2 ? t - 2 : 0);
-  const double la_res = (mode == SD_BLOCK && t >= 2) ? la_prev : 0.0;
-  double U = NAN;
-  if (t <= kb) {
-    const double v = __shfl(vn, t - 1);  // > 0: a rejection never lands on a zero offset
-    const uint4 wu = philox(0u, (uint32_t)b, r, TAG_USAMPLE << 24, seed);
-    const double u = uniform64(wu.x);
-    if (umode == SD_USAMPLE_PAPER) {
-      double up = 0.0;
-      if (lane == 0) up = usample_paper(u, la_res, v);
-      U = __shfl(up, 0);
-    } else {
-      U = usample_exact(u, la_res, v, lane);
+}
+
+// The sampler's verification: sums the partials of the fused target call
+// (fixed tile order) into ||Delta_j||, ell_j and, for the residual,
+// e.G = sum_i (m^p - m^q)_i G_i / (sigma ||Delta||) of every row, decides, and
+// hands the next kernel what it needs to form the residual elementwise:
+//   rmode 1: y = m^q + sigma G + rcoef (m^p - m^q),  rcoef = (U - e.G)/||Delta||
+//   rmode 2: y = m^q_{K_b} + sigma xi'  (full accept, target draw)
+//   rmode 3: y = yhat_{K_b}             (full accept that reaches step N)
+// It also clears the next round's active flag before looking at its gate.
+__global__ __launch_bounds__(kThreads) void scan_fused_kernel(
+    int B, int K, int d, int N, int mode, int umode, const double* __restrict__ lrp, int nct,
+    const double* __restrict__ sigma, const int32_t* __restrict__ kcur,
+    const uint32_t* __restrict__ rcur, uint64_t seed, const float* __restrict__ MP,
+    const float* __restrict__ MQ, int32_t* __restrict__ tau, int32_t* __restrict__ rmode,
+    float* __restrict__ rcoef, float* __restrict__ rsig, int* nanflag, int* act_next,
+    const int* gate) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) *act_next = 0;
+  if (gate && *gate == 0) return;
+  const int lane = threadIdx.x & 63;
+  const int b = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
+  if (b >= B) return;
+  const int K1 = K + 1;
+  const int k = kcur[b];
+  const int kb = k < N ? min(K, N - k) : 0;
+  if (kb <= 0) {
+    if (lane == 0) {
+      tau[b] = 0;
+      rmode[b] = 0;
     }
+    return;
+  }
+  const bool valid = lane < kb;
+  double s2 = 0.0, sz = 0.0, sg = 1.0;
+  double sgd = 0.0;
+  if (valid) {
+    const double* pl = lrp + ((int64_t)b * K1 + lane) * nct * 3;
+    for (int ct = 0; ct < nct; ++ct) {
+      s2 += pl[3 * ct];
+      sz += pl[3 * ct + 1];
+      sgd += pl[3 * ct + 2];
+    }
+    sg = sigma[(int64_t)b * K1 + lane];
+  }
+  const double inv = 1.0 / (sg * sg);
+  const double vn = valid ? sqrt(s2 * inv) : 0.0;
+  const double ell = valid ? -sz * inv - 0.5 * s2 * inv : 0.0;
+  if (__ballot(valid && !(isfinite(ell) && isfinite(vn))) != 0ull && lane == 0) atomicOr(nanflag, 1);
+  const uint32_t r = rcur[b];
+  const Decision D = decide(mode, umode, kb, ell, vn, (uint32_t)b, r, seed, lane);
+  const int t = D.tau;
+  int rm;
+  float cf = 0.f, sgo = 0.f;
+  if (t <= kb) {
+    const double v = __shfl(vn, t - 1);
+    const double st = sigma[(int64_t)b * K1 + (t - 1)];
+    const double eG = __shfl(sgd, t - 1) / (st * v);
+    rm = 1;
+    cf = (float)((D.U - eG) / v);
+    sgo = (float)st;
+  } else if (kb + 1 <= N - k) {
+    rm = 2;
+    sgo = (float)sigma[(int64_t)b * K1 + kb];
+  } else {
+    rm = 3;
   }
   if (lane == 0) {
     tau[b] = t;
-    lar[b] = la_res;
-    ures[b] = U;
-    if (coins) coins[b] = cm;
+    rmode[b] = rm;
+    rcoef[b] = cf;
+    rsig[b] = sgo;
   }
 }
 
@@ -246,6 +334,20 @@ hipError_t verify_launch(int B, int K, int d, int mode, const float* yd, sd_stri
   return timed("block_scan", s, [&] {
     scan_kernel<<<(B + per - 1) / per, kThreads, 0, s>>>(B, K, mode, umode, dn, lr, kb, rnd, seed,
                                                         tau, lar, ures, coins, nanflag, gate);
+  });
+}
+
+hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, const double* lrp,
+                             int nct, const double* sigma, const int32_t* kcur,
+                             const uint32_t* rcur, uint64_t seed, const float* mp,
+                             const float* mq, int32_t* tau, int32_t* rmode, float* rcoef,
+                             float* rsig, int* nanflag, int* act_next, hipStream_t s,
+                             const int* gate) {
+  const int per = kThreads / 64;
+  return timed("scan_fused", s, [&] {
+    scan_fused_kernel<<<(B + per - 1) / per, kThreads, 0, s>>>(
+        B, K, d, N, mode, umode, lrp, nct, sigma, kcur, rcur, seed, mp, mq, tau, rmode, rcoef,
+        rsig, nanflag, act_next, gate);
   });
 }
 
