@@ -84,7 +84,12 @@ sd_status sd_schedule_table(const sd_schedule* sched, double* host_out);
  * q_s = sum_m w_m N(a mu_m, (a^2 var_m + 1 - a^2) I) and its score, and the EM
  * mean m^q_n(x) = c1_n x + c2_n score (eq. target-distribution).
  * mu [M][d], var [M], log_w [M] are HOST arrays copied at creation.
- * d >= 1, 1 <= n_comp <= 1024.  precision selects the GEMM operand type. */
+ * d >= 1, 1 <= n_comp <= 1024.  precision selects the GEMM operand type:
+ * SD_FP32 multiplies float32 operands; SD_BF16 stores mu as bf16 (round to
+ * nearest even) and rounds x and the softmax weights to bf16 before the two
+ * products, accumulating in float32 (||x||^2, ||mu||^2 and the softmax stay
+ * float64 from the float32 values; the epilogue is float32).  Only the copies
+ * of the chosen precision are allocated. */
 sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp,
                            const float* mu, const float* var, const float* log_w,
                            sd_precision precision, sd_target* out);

@@ -130,6 +130,13 @@ sd_status sd_schedule_table(const sd_schedule* sched, double* host_out) {
 }
 
 // ---------------------------------------------------------------- target --
+// float32 -> bf16 bits, round to nearest even (finite inputs).
+static uint16_t bf16_rne(float f) {
+  uint32_t u;
+  memcpy(&u, &f, 4);
+  return (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+}
+
 sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, const float* mu,
                            const float* var, const float* log_w, sd_precision precision,
                            sd_target* out) {
@@ -140,10 +147,6 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
   SD_CHECK_ARG(n_comp >= 1 && n_comp <= 1024, "sd_target_create: n_comp = %d not in [1, 1024]", n_comp);
   SD_CHECK_ARG(mu && var && log_w, "sd_target_create: mu/var/log_w must be host arrays");
   SD_CHECK_ARG(precision == SD_FP32 || precision == SD_BF16, "sd_target_create: unknown precision");
-  if (precision == SD_BF16) {
-    set_error("sd_target_create: the bf16 GEMM path is not built in this version");
-    return SD_EUNSUPPORTED;
-  }
   for (int m = 0; m < n_comp; ++m) {
     SD_CHECK_ARG(var[m] > 0.0f && var[m] < 1.0e30f, "sd_target_create: var[%d] must be positive and finite", m);
     SD_CHECK_ARG(isfinite(log_w[m]), "sd_target_create: log_w[%d] is not finite", m);
@@ -172,8 +175,12 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
   t->M = n_comp;
   t->prec = precision;
   (void)hipGetDevice(&t->device);
-  bool ok = hipMalloc(&t->mu, sizeof(float) * M * D) == hipSuccess &&
-            hipMalloc(&t->muT, sizeof(float) * M * D) == hipSuccess &&
+  const bool bf = precision == SD_BF16;
+  // the operand copies of the chosen precision only
+  bool ok = (bf ? hipMalloc(&t->mu16, sizeof(uint16_t) * M * D) == hipSuccess &&
+                      hipMalloc(&t->muT16, sizeof(uint16_t) * M * D) == hipSuccess
+                : hipMalloc(&t->mu, sizeof(float) * M * D) == hipSuccess &&
+                      hipMalloc(&t->muT, sizeof(float) * M * D) == hipSuccess) &&
             hipMalloc(&t->ls, sizeof(double2) * M * (size_t)sched->n_steps) == hipSuccess &&
             hipMalloc(&t->logw, sizeof(double) * M) == hipSuccess &&
             hipMalloc(&t->musq, sizeof(double) * M) == hipSuccess &&
@@ -183,8 +190,24 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
     sd_target_destroy(reinterpret_cast<sd_target>(t));
     return SD_ENOMEM;
   }
-  ok = hipMemcpy(t->mu, mu, sizeof(float) * M * D, hipMemcpyHostToDevice) == hipSuccess &&
-       hipMemcpy(t->muT, muT.data(), sizeof(float) * M * D, hipMemcpyHostToDevice) == hipSuccess &&
+  if (bf) {
+    std::vector<uint16_t> h(M * D), hT(M * D);
+    for (size_t m = 0; m < M; ++m)
+      for (size_t i = 0; i < D; ++i) {
+        const uint16_t v = bf16_rne(mu[m * D + i]);
+        h[m * D + i] = v;
+        hT[i * M + m] = v;
+      }
+    ok = hipMemcpy(t->mu16, h.data(), sizeof(uint16_t) * M * D, hipMemcpyHostToDevice) ==
+             hipSuccess &&
+         hipMemcpy(t->muT16, hT.data(), sizeof(uint16_t) * M * D, hipMemcpyHostToDevice) ==
+             hipSuccess;
+  } else {
+    ok = hipMemcpy(t->mu, mu, sizeof(float) * M * D, hipMemcpyHostToDevice) == hipSuccess &&
+         hipMemcpy(t->muT, muT.data(), sizeof(float) * M * D, hipMemcpyHostToDevice) ==
+             hipSuccess;
+  }
+  ok = ok &&
 
        hipMemcpy(t->logw, lw.data(), sizeof(double) * M, hipMemcpyHostToDevice) == hipSuccess &&
        hipMemcpy(t->musq, msq.data(), sizeof(double) * M, hipMemcpyHostToDevice) == hipSuccess;
@@ -220,6 +243,8 @@ sd_status sd_target_destroy(sd_target target) {
   Target* t = reinterpret_cast<Target*>(target);
   if (t->mu) (void)hipFree(t->mu);
   if (t->muT) (void)hipFree(t->muT);
+  if (t->mu16) (void)hipFree(t->mu16);
+  if (t->muT16) (void)hipFree(t->muT16);
   if (t->ls) (void)hipFree(t->ls);
   if (t->logw) (void)hipFree(t->logw);
   if (t->musq) (void)hipFree(t->musq);

@@ -69,6 +69,8 @@ struct Target {
   sd_precision prec;
   float* mu;      // [M][d]
   float* muT;     // [d][M]
+  uint16_t* mu16;   // [M][d] bf16 (round to nearest even), bf16 precision only
+  uint16_t* muT16;  // [d][M] bf16, bf16 precision only
   double* logw;   // [M]
   double* musq;   // [M] ||mu_m||^2 (float64 from the float32 means)
   float4* coef;   // [N+1] per step: (c1_n, c2_n, sigma_n, 1/c2_n) rounded to float32
@@ -77,6 +79,7 @@ struct Target {
 };
 
 size_t target_ws_bytes(const Target& t, int rows);
+size_t target_ws_bytes_bf16(const Target& t, int rows);
 // Rows' EM means (and scores if score != nullptr).  gate: nullable device flag;
 // when it reads 0 every kernel exits at once (finished sampler rounds).
 hipError_t target_mean_launch(const Target& t, int rows, const float* x, int64_t ldx,
@@ -91,6 +94,21 @@ hipError_t target_mean_lr_launch(const Target& t, int rows, int K1, const float*
                                  const uint32_t* rnd, uint64_t seed, void* ws, hipStream_t s,
                                  const int* gate);
 int lr_tiles(const Target& t);
+// bf16 versions of the three calls above (dispatched to by them).
+hipError_t target_mean_bf16_launch(const Target& t, int rows, const float* x, int64_t ldx,
+                                   const int32_t* step, float* mq, int64_t ldq, float* score,
+                                   int64_t lds, void* ws, hipStream_t s, const int* gate);
+hipError_t target_mean_lr_bf16_launch(const Target& t, int rows, int K1, const float* x,
+                                      const int32_t* step, float* mq, const float* mp,
+                                      double* lrp, const uint32_t* rnd, uint64_t seed, void* ws,
+                                      hipStream_t s, const int* gate);
+int lr_tiles_bf16(const Target& t);
+// Softmax over the split logits partials part[S][rows][M] (+ xsq[S][rows]):
+// P[rows][M] = r a / s2 (float32, or bf16 when p_bf16) and rowc[rows][3] =
+// (c1, c2, rho) of each row's step.
+hipError_t gmm_softmax_launch(const Target& t, int rows, int S, const float* part,
+                              const double* xsq, const int32_t* step, void* P, bool p_bf16,
+                              float* rowc, hipStream_t s, const int* gate);
 // Sampler verification on the fused partials (see scan_fused_kernel).
 hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, const double* lrp,
                              int nct, const double* sigma, const int32_t* kcur,
@@ -156,5 +174,17 @@ hipError_t philox_normals_launch(uint64_t seed, uint32_t chain, uint32_t rnd, ui
                                  uint32_t slot, int d, float* out, hipStream_t s);
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
+
+#ifdef __HIPCC__
+// Workgroups are dispatched round-robin over the eight XCDs, each with its own
+// L2.  Remap the linear workgroup id so that XCD x works on the contiguous
+// x-th eighth of the tile space (tiles that share operand rows stay on one
+// L2); the innermost tile index is the fastest-varying one.
+__device__ __forceinline__ int xcd_tile(int total) {
+  const int L = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
+  if (total % 8 != 0) return L;
+  return (L % 8) * (total / 8) + L / 8;
+}
+#endif
 
 }  // namespace sd

@@ -135,16 +135,6 @@ __device__ __forceinline__ int out_col() {
   return (w & 1) * 32 + (lane & 31);
 }
 
-// Workgroups are dispatched round-robin over the eight XCDs, each with its own
-// L2.  Remap the linear workgroup id so that XCD x works on the contiguous
-// x-th eighth of the tile space (tiles that share operand rows stay on one
-// L2); the innermost tile index is the fastest-varying one.
-__device__ __forceinline__ int xcd_tile(int total) {
-  const int L = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
-  if (total % 8 != 0) return L;
-  return (L % 8) * (total / 8) + L / 8;
-}
-
 __global__ __launch_bounds__(kThreads) void gmm_logits_kernel(
     int R, int M, int d, const float* __restrict__ X, int64_t ldx, bool vecx,
     const float* __restrict__ mu, bool vecmu, int ksplit, float* __restrict__ part,
@@ -196,11 +186,12 @@ __global__ __launch_bounds__(kThreads) void gmm_logits_kernel(
 // reduction, one exp per component and one sum reduction.
 constexpr int kMaxPer = 16;  // components per lane held in registers (M <= 1024)
 
+template <class TP>
 __global__ __launch_bounds__(kThreads) void gmm_softmax_kernel(
     int R, int M, int d, int S, const float* __restrict__ part, const double* __restrict__ xsq,
     const int32_t* __restrict__ step, Sched sc, const double2* __restrict__ ls,
     const double* __restrict__ logw, const double* __restrict__ musq, const float4* __restrict__ coef,
-    float* __restrict__ P, float* __restrict__ rowc, const int* gate) {
+    TP* __restrict__ P, float* __restrict__ rowc, const int* gate) {
   if (gate && *gate == 0) return;
   const int lane = threadIdx.x & 63;
   const int row = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
@@ -244,7 +235,11 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_kernel(
     if (m < M) {
       const double rm = (double)e[i] * inv;
       const double is2 = lsn[m].y;
-      P[(int64_t)row * M + m] = (float)(rm * a * is2);
+      const float pm = (float)(rm * a * is2);
+      if constexpr (sizeof(TP) == 2)
+        P[(int64_t)row * M + m] = __builtin_bit_cast(uint16_t, (__bf16)pm);
+      else
+        P[(int64_t)row * M + m] = pm;
       rho += rm * is2;
     }
   }
@@ -482,11 +477,32 @@ Plan make_plan(const Target& t, int R) {
 
 }  // namespace
 
-size_t target_ws_bytes(const Target& t, int rows) { return make_plan(t, rows).total; }
+size_t target_ws_bytes(const Target& t, int rows) {
+  return t.prec == SD_BF16 ? target_ws_bytes_bf16(t, rows) : make_plan(t, rows).total;
+}
+
+hipError_t gmm_softmax_launch(const Target& t, int R, int S, const float* part, const double* xsq,
+                              const int32_t* step, void* P, bool p_bf16, float* rowc,
+                              hipStream_t s, const int* gate) {
+  const int per = kThreads / 64;
+  const int nb = (R + per - 1) / per;
+  return timed("gmm_softmax", s, [&] {
+    if (p_bf16)
+      gmm_softmax_kernel<<<nb, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc, t.ls,
+                                                 t.logw, t.musq, t.coef,
+                                                 static_cast<uint16_t*>(P), rowc, gate);
+    else
+      gmm_softmax_kernel<<<nb, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc, t.ls,
+                                                 t.logw, t.musq, t.coef, static_cast<float*>(P),
+                                                 rowc, gate);
+  });
+}
 
 hipError_t target_mean_launch(const Target& t, int R, const float* x, int64_t ldx,
                               const int32_t* step, float* mq, int64_t ldq, float* score,
                               int64_t lds, void* ws, hipStream_t s, const int* gate) {
+  if (t.prec == SD_BF16)
+    return target_mean_bf16_launch(t, R, x, ldx, step, mq, ldq, score, lds, ws, s, gate);
   const Plan p = make_plan(t, R);
   char* base = static_cast<char*>(ws);
   float* part = reinterpret_cast<float*>(base + p.off_part);
@@ -502,12 +518,7 @@ hipError_t target_mean_launch(const Target& t, int R, const float* x, int64_t ld
                                               part, xsq, gate);
   });
   if (e != hipSuccess) return e;
-  const int per = kThreads / 64;
-  e = timed("gmm_softmax", s, [&] {
-    gmm_softmax_kernel<<<(R + per - 1) / per, kThreads, 0, s>>>(R, t.M, t.d, p.S, part, xsq,
-                                                               step, t.sc, t.ls, t.logw,
-                                                               t.musq, t.coef, P, rowc, gate);
-  });
+  e = gmm_softmax_launch(t, R, p.S, part, xsq, step, P, false, rowc, s, gate);
   if (e != hipSuccess) return e;
   dim3 g2((R + TILE - 1) / TILE, (t.d + TILE - 1) / TILE);
   return timed("gmm_mean", s, [&] {
@@ -520,6 +531,8 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
                                  const int32_t* step, float* mq, const float* mp, double* lrp,
                                  const uint32_t* rnd, uint64_t seed, void* ws, hipStream_t s,
                                  const int* gate) {
+  if (t.prec == SD_BF16)
+    return target_mean_lr_bf16_launch(t, R, K1, x, step, mq, mp, lrp, rnd, seed, ws, s, gate);
   const Plan p = make_plan(t, R);
   char* base = static_cast<char*>(ws);
   float* part = reinterpret_cast<float*>(base + p.off_part);
@@ -534,12 +547,7 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
                                               p.ksplit, part, xsq, gate);
   });
   if (e != hipSuccess) return e;
-  const int per = kThreads / 64;
-  e = timed("gmm_softmax", s, [&] {
-    gmm_softmax_kernel<<<(R + per - 1) / per, kThreads, 0, s>>>(R, t.M, t.d, p.S, part, xsq,
-                                                               step, t.sc, t.ls, t.logw,
-                                                               t.musq, t.coef, P, rowc, gate);
-  });
+  e = gmm_softmax_launch(t, R, p.S, part, xsq, step, P, false, rowc, s, gate);
   if (e != hipSuccess) return e;
   dim3 g2((t.d + TILE - 1) / TILE, (R + TILE - 1) / TILE);
   return timed("gmm_mean_lr", s, [&] {
@@ -548,6 +556,8 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
   });
 }
 
-int lr_tiles(const Target& t) { return (t.d + TILE - 1) / TILE; }
+int lr_tiles(const Target& t) {
+  return t.prec == SD_BF16 ? lr_tiles_bf16(t) : (t.d + TILE - 1) / TILE;
+}
 
 }  // namespace sd

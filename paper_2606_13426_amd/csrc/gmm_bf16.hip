@@ -1,0 +1,372 @@
+// Gaussian-mixture target with bf16 operands on the matrix cores (float32
+// accumulation), for the large configurations: the same three steps as the
+// float32 path (logits GEMM split over d, float64 softmax, mean GEMM with the
+// EM epilogue) on 128 x 128 tiles of v_mfma_f32_32x32x16_bf16.
+//   gmm_logits_bf16: S = X mu^T, X float32 rounded to bf16 on staging, mu bf16;
+//                    ||x||^2 in float64 from the unrounded float32 values;
+//   softmax:         the float32 path's kernel, writing P in bf16;
+//   gmm_mean_bf16 / gmm_mean_lr_bf16: O = P mu (mu^T stored as bf16) and the
+//                    epilogue in float32, the latter with the verification
+//                    partial sums of the sampler (as the float32 path).
+// The 128 x 128 accumulator tile is handed to the epilogue through LDS in two
+// passes of 64 columns, each over the operand buffers' storage.
+#include "common.hpp"
+#include "gemm_bf16.hpp"
+#include "philox.hpp"
+
+namespace sd {
+namespace {
+
+using namespace bf16;
+
+constexpr int LDO = 68;         // staging row stride in floats (one 64-column pass)
+constexpr int kMaxChains = 65;  // chains that 128 rows of [B][K+1] can touch (K+1 >= 2)
+
+static_assert(sizeof(float) * TM * LDO <= sizeof(OperandLds), "staging must fit the operand LDS");
+
+__global__ __launch_bounds__(kThreads) void gmm_logits_bf16_kernel(
+    int R, int M, int d, const float* __restrict__ X, int64_t ldx, bool vecx,
+    const uint16_t* __restrict__ mu, bool vecmu, int ksplit, float* __restrict__ part,
+    double* __restrict__ xsq, const int* gate) {
+  if (gate && *gate == 0) return;
+  __shared__ OperandLds sm;
+  // grid (splits, row tiles, column tiles), split fastest (as the float32 path)
+  const int nsplit = gridDim.x, nrt = gridDim.y;
+  const int lin = xcd_tile(nsplit * nrt * gridDim.z);
+  const int s = lin % nsplit, rt = (lin / nsplit) % nrt, ct = lin / (nsplit * nrt);
+  const int r0 = rt * TM, c0 = ct * TN;
+  const int kbeg = s * ksplit, kend = min(d, kbeg + ksplit);
+  f32x16 acc[2][2];
+  zero(acc);
+  double sq[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
+  const bool want_sq = ct == 0;
+  if (want_sq)
+    tile<true>(sm, X, ldx, R, vecx, mu, d, M, vecmu, r0, c0, kbeg, kend, acc, sq);
+  else
+    tile<false>(sm, X, ldx, R, vecx, mu, d, M, vecmu, r0, c0, kbeg, kend, acc, sq);
+  float* ps = part + (int64_t)s * R * M;
+#pragma unroll
+  for (int qb = 0; qb < 2; ++qb) {
+    const int col = c0 + out_col(qb);
+    if (col >= M) continue;
+#pragma unroll
+    for (int qa = 0; qa < 2; ++qa)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = r0 + out_row(qa, v);
+        if (row < R) ps[(int64_t)row * M + col] = acc[qa][qb][v];
+      }
+  }
+  if (want_sq) {
+    // the 16 threads that loaded a row are 16 consecutive lanes
+#pragma unroll
+    for (int h = 0; h < 8; ++h) {
+      double t = sq[h];
+      t += __shfl_xor(t, 1);
+      t += __shfl_xor(t, 2);
+      t += __shfl_xor(t, 4);
+      t += __shfl_xor(t, 8);
+      const int row = r0 + (threadIdx.x >> 4) + 16 * h;
+      if ((threadIdx.x & 15) == 0 && row < R) xsq[(int64_t)s * R + row] = t;
+    }
+  }
+}
+
+// Pass p of the epilogue stages accumulator blocks qb = p of every wavefront:
+// tile columns 64 wc + 32 p + (0..31) go to staging columns 32 wc + (0..31).
+// In the epilogue thread t owns tile row t/2 and staging columns
+// 32 (t % 2) .. + 31, i.e. tile columns 64 (t % 2) + 32 p .. + 31.
+__device__ __forceinline__ void stage(float* stg, const f32x16 (&acc)[2][2], int p) {
+  const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int sc = 32 * (w & 1) + (lane & 31);
+#pragma unroll
+  for (int qa = 0; qa < 2; ++qa)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) stg[out_row(qa, v) * LDO + sc] = acc[qa][p][v];
+}
+
+__device__ __forceinline__ void load_rc(float* rc, const float* __restrict__ rowc, int r0, int R) {
+  for (int e = threadIdx.x; e < 3 * TM; e += kThreads)
+    rc[e] = r0 + e / 3 < R ? rowc[3 * (int64_t)r0 + e] : 0.f;
+}
+
+// Eight float4 of a row span starting at p (cnt valid elements from there).
+__device__ __forceinline__ void load32(const float* p, int cnt, bool vec, float4 (&v)[8]) {
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const int c = cnt - 4 * q;
+    if (vec && c >= 4) {
+      v[q] = *reinterpret_cast<const float4*>(p + 4 * q);
+    } else {
+      v[q] = make_float4(c > 0 ? p[4 * q] : 0.f, c > 1 ? p[4 * q + 1] : 0.f,
+                         c > 2 ? p[4 * q + 2] : 0.f, c > 3 ? p[4 * q + 3] : 0.f);
+    }
+  }
+}
+
+__device__ __forceinline__ void store4v(float* p, int c, bool vec, float4 v) {
+  if (vec && c >= 4) {
+    *reinterpret_cast<float4*>(p) = v;
+  } else {
+    if (c > 0) p[0] = v.x;
+    if (c > 1) p[1] = v.y;
+    if (c > 2) p[2] = v.z;
+    if (c > 3) p[3] = v.w;
+  }
+}
+
+__device__ __forceinline__ float comp(const float4& v, int c) {
+  return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w;
+}
+
+// Public target call: m^q = c1 x + c2 (O - rho x) (and the score if asked).
+__global__ __launch_bounds__(kThreads) void gmm_mean_bf16_kernel(
+    int R, int M, int d, const uint16_t* __restrict__ P, bool vecp,
+    const uint16_t* __restrict__ muT, const float* __restrict__ X, int64_t ldx, bool vecx,
+    const float* __restrict__ rowc, float* __restrict__ mq, int64_t ldq, bool vecq,
+    float* __restrict__ score, int64_t lds, bool vecs, const int* gate) {
+  if (gate && *gate == 0) return;
+  __shared__ OperandLds sm;
+  __shared__ float rc[3 * TM];
+  const int nct = gridDim.x;
+  const int lin = xcd_tile(nct * gridDim.y);
+  const int ct = lin % nct, rt = lin / nct;
+  const int r0 = rt * TM, c0 = ct * TN;
+  load_rc(rc, rowc, r0, R);
+  f32x16 acc[2][2];
+  zero(acc);
+  double unused[8];
+  tile<false>(sm, P, M, R, vecp, muT, M, d, vecp, r0, c0, 0, M, acc, unused);
+  float* stg = reinterpret_cast<float*>(&sm);
+  const int lr = threadIdx.x >> 1, gsel = threadIdx.x & 1;
+  const int row = r0 + lr;
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    __syncthreads();  // operand tiles (p = 0) or the previous pass are consumed
+    stage(stg, acc, p);
+    __syncthreads();
+    if (row >= R) continue;
+    const int col = c0 + 64 * gsel + 32 * p;
+    const int cnt = min(32, d - col);
+    if (cnt <= 0) continue;
+    float4 xv[8];
+    load32(X + (int64_t)row * ldx + col, cnt, vecx, xv);
+    const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
+    const float* o = &stg[lr * LDO + 32 * gsel];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const float4 ov = *reinterpret_cast<const float4*>(o + 4 * q);
+      const float4 sv = make_float4(ov.x - rho * xv[q].x, ov.y - rho * xv[q].y,
+                                    ov.z - rho * xv[q].z, ov.w - rho * xv[q].w);
+      const float4 qv = make_float4(c1 * xv[q].x + c2 * sv.x, c1 * xv[q].y + c2 * sv.y,
+                                    c1 * xv[q].z + c2 * sv.z, c1 * xv[q].w + c2 * sv.w);
+      store4v(mq + (int64_t)row * ldq + col + 4 * q, cnt - 4 * q, vecq, qv);
+      if (score) store4v(score + (int64_t)row * lds + col + 4 * q, cnt - 4 * q, vecs, sv);
+    }
+  }
+}
+
+// The sampler's mean GEMM on its [B][K+1][d] block with the verification
+// partials: for draft rows j < K and this tile's columns, float64 sums of
+// (m^p - m^q)^2, (yhat_{j+1} - m^p)(m^p - m^q) and G (m^p - m^q), G the
+// residual's normals of the chain's round, into lrp[row][column tile][3].
+__global__ __launch_bounds__(kThreads) void gmm_mean_lr_bf16_kernel(
+    int R, int M, int d, int K1, const uint16_t* __restrict__ P, bool vecp,
+    const uint16_t* __restrict__ muT, const float* __restrict__ X, const float* __restrict__ rowc,
+    const float* __restrict__ MP, float* __restrict__ mq, double* __restrict__ lrp, bool vecd,
+    const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
+  if (gate && *gate == 0) return;
+  __shared__ OperandLds sm;
+  __shared__ float rc[3 * TM];
+  __shared__ float gz[kMaxChains * LDO];
+  const int nct = gridDim.x;
+  const int lin = xcd_tile(nct * gridDim.y);
+  const int ct = lin % nct, rt = lin / nct;
+  const int r0 = rt * TM, c0 = ct * TN;
+  load_rc(rc, rowc, r0, R);
+  f32x16 acc[2][2];
+  zero(acc);
+  double unused[8];
+  tile<false>(sm, P, M, R, vecp, muT, M, d, vecp, r0, c0, 0, M, acc, unused);
+  float* stg = reinterpret_cast<float*>(&sm);
+  const int lr = threadIdx.x >> 1, gsel = threadIdx.x & 1;
+  const int row = r0 + lr;
+  const int b = row / K1, j = row - b * K1;
+  const bool has_row = row < R;
+  const bool has_draft = has_row && j < K1 - 1;
+  const int b_first = r0 / K1;
+  const int nchain = min((min(r0 + TM, R) - 1) / K1 - b_first + 1, kMaxChains);
+  double s2 = 0.0, sz = 0.0, sgd = 0.0;
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    __syncthreads();
+    stage(stg, acc, p);
+    // G of this pass's columns for every chain of the tile, four coordinates
+    // (one Philox block) per item: staging column 4 gq is tile column
+    // 64 (gq / 8) + 32 p + 4 (gq % 8)
+    for (int e = threadIdx.x; e < nchain * 16; e += kThreads) {
+      const int cl = e >> 4, gq = e & 15;
+      const int bb = b_first + cl;
+      const int tcol = c0 + 64 * (gq >> 3) + 32 * p + 4 * (gq & 7);
+      const float4 z = normals4(philox((uint32_t)(tcol >> 2), (uint32_t)bb, rnd[bb],
+                                       TAG_RESID << 24, seed));
+      *reinterpret_cast<float4*>(&gz[cl * LDO + 4 * gq]) = z;
+    }
+    __syncthreads();
+    if (!has_row) continue;
+    const int col = c0 + 64 * gsel + 32 * p;
+    const int cnt = min(32, d - col);
+    if (cnt <= 0) continue;
+    float4 xv[8], yv[8], pv[8];
+    const float* px = X + (int64_t)row * d + col;
+    load32(px, cnt, vecd, xv);
+    if (has_draft) {
+      load32(px + d, cnt, vecd, yv);
+      load32(MP + ((int64_t)b * (K1 - 1) + j) * d + col, cnt, vecd, pv);
+    }
+    const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
+    const float* o = &stg[lr * LDO + 32 * gsel];
+    const float* g = &gz[(b - b_first) * LDO + 32 * gsel];
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      const float4 ov = *reinterpret_cast<const float4*>(o + 4 * q);
+      const float4 x = xv[q];
+      const float4 qv = make_float4(c1 * x.x + c2 * (ov.x - rho * x.x),
+                                    c1 * x.y + c2 * (ov.y - rho * x.y),
+                                    c1 * x.z + c2 * (ov.z - rho * x.z),
+                                    c1 * x.w + c2 * (ov.w - rho * x.w));
+      const int c = cnt - 4 * q;
+      store4v(mq + (int64_t)row * d + col + 4 * q, c, vecd, qv);
+      if (has_draft) {
+        const float4 gv = *reinterpret_cast<const float4*>(g + 4 * q);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          if (e < c) {
+            const double dd = (double)comp(pv[q], e) - (double)comp(qv, e);
+            const double zz = (double)comp(yv[q], e) - (double)comp(pv[q], e);
+            s2 = fma(dd, dd, s2);
+            sz = fma(zz, dd, sz);
+            sgd = fma((double)comp(gv, e), dd, sgd);
+          }
+        }
+      }
+    }
+  }
+  s2 += __shfl_xor(s2, 1);
+  sz += __shfl_xor(sz, 1);
+  sgd += __shfl_xor(sgd, 1);
+  if (gsel == 0 && has_row) {
+    double* o = lrp + ((int64_t)row * nct + ct) * 3;
+    o[0] = s2;
+    o[1] = sz;
+    o[2] = sgd;
+  }
+}
+
+struct Plan {
+  int S, ksplit;
+  size_t off_part, off_xsq, off_p, off_rowc, total;
+};
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Split of the logits GEMM over d, chosen as in the float32 path for
+// 128 x 128 tiles.
+Plan make_plan(const Target& t, int R) {
+  Plan p{};
+  const int tiles = ((R + TM - 1) / TM) * ((t.M + TN - 1) / TN);
+  const int nchunks = (t.d + KC - 1) / KC;
+  int best_cost = 1 << 30, best_per = nchunks;
+  for (int S = 1; S <= 8 && S <= nchunks; ++S) {
+    const int per = (nchunks + S - 1) / S;
+    const int splits = (nchunks + per - 1) / per;
+    const int cost = ((tiles * splits + 255) / 256) * per;
+    if (cost < best_cost) {
+      best_cost = cost;
+      best_per = per;
+    }
+  }
+  p.ksplit = best_per * KC;
+  p.S = (t.d + p.ksplit - 1) / p.ksplit;
+  size_t off = 0;
+  p.off_part = off;
+  off = align256(off + sizeof(float) * (size_t)p.S * R * t.M);
+  p.off_xsq = off;
+  off = align256(off + sizeof(double) * (size_t)p.S * R);
+  p.off_p = off;
+  off = align256(off + sizeof(uint16_t) * (size_t)R * t.M);
+  p.off_rowc = off;
+  off = align256(off + sizeof(float) * 3 * (size_t)R);
+  p.total = off;
+  return p;
+}
+
+struct Bufs {
+  float* part;
+  double* xsq;
+  uint16_t* P;
+  float* rowc;
+};
+
+Bufs carve(const Plan& p, void* ws) {
+  char* base = static_cast<char*>(ws);
+  return Bufs{reinterpret_cast<float*>(base + p.off_part),
+              reinterpret_cast<double*>(base + p.off_xsq),
+              reinterpret_cast<uint16_t*>(base + p.off_p),
+              reinterpret_cast<float*>(base + p.off_rowc)};
+}
+
+hipError_t logits_and_softmax(const Target& t, const Plan& p, const Bufs& w, int R,
+                              const float* x, int64_t ldx, bool vecx, const int32_t* step,
+                              hipStream_t s, const int* gate) {
+  dim3 g1(p.S, (R + TM - 1) / TM, (t.M + TN - 1) / TN);
+  hipError_t e = timed("gmm_logits_bf16", s, [&] {
+    gmm_logits_bf16_kernel<<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, vecx, t.mu16,
+                                                   t.d % 8 == 0, p.ksplit, w.part, w.xsq, gate);
+  });
+  if (e != hipSuccess) return e;
+  return gmm_softmax_launch(t, R, p.S, w.part, w.xsq, step, w.P, true, w.rowc, s, gate);
+}
+
+}  // namespace
+
+size_t target_ws_bytes_bf16(const Target& t, int rows) { return make_plan(t, rows).total; }
+
+hipError_t target_mean_bf16_launch(const Target& t, int R, const float* x, int64_t ldx,
+                                   const int32_t* step, float* mq, int64_t ldq, float* score,
+                                   int64_t lds, void* ws, hipStream_t s, const int* gate) {
+  const Plan p = make_plan(t, R);
+  const Bufs w = carve(p, ws);
+  const bool vecx = (ldx % 4 == 0) && aligned16(x);
+  hipError_t e = logits_and_softmax(t, p, w, R, x, ldx, vecx, step, s, gate);
+  if (e != hipSuccess) return e;
+  const bool vecq = (ldq % 4 == 0) && aligned16(mq);
+  const bool vecs = score && (lds % 4 == 0) && aligned16(score);
+  dim3 g2((t.d + TN - 1) / TN, (R + TM - 1) / TM);
+  return timed("gmm_mean_bf16", s, [&] {
+    gmm_mean_bf16_kernel<<<g2, kThreads, 0, s>>>(R, t.M, t.d, w.P, t.M % 8 == 0, t.muT16, x, ldx,
+                                                 vecx, w.rowc, mq, ldq, vecq, score, lds, vecs,
+                                                 gate);
+  });
+}
+
+hipError_t target_mean_lr_bf16_launch(const Target& t, int R, int K1, const float* x,
+                                      const int32_t* step, float* mq, const float* mp,
+                                      double* lrp, const uint32_t* rnd, uint64_t seed, void* ws,
+                                      hipStream_t s, const int* gate) {
+  const Plan p = make_plan(t, R);
+  const Bufs w = carve(p, ws);
+  const bool vecd = (t.d % 4 == 0) && aligned16(x) && aligned16(mq) && aligned16(mp);
+  hipError_t e = logits_and_softmax(t, p, w, R, x, t.d, vecd, step, s, gate);
+  if (e != hipSuccess) return e;
+  dim3 g2((t.d + TN - 1) / TN, (R + TM - 1) / TM);
+  return timed("gmm_mean_lr_bf16", s, [&] {
+    gmm_mean_lr_bf16_kernel<<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, w.P, t.M % 8 == 0, t.muT16,
+                                                    x, w.rowc, mp, mq, lrp, vecd, rnd, seed,
+                                                    gate);
+  });
+}
+
+int lr_tiles_bf16(const Target& t) { return (t.d + TN - 1) / TN; }
+
+}  // namespace sd
