@@ -27,6 +27,8 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 FP32_PEAK_TFLOPS = 157.3
+BF16_PEAK_TFLOPS = 2500.0   # dense bf16 MFMA
+GEMMS = ("gmm_logits", "gmm_mean", "gmm_mean_lr", "gmm_logits_bf16", "gmm_mean_bf16", "gmm_mean_lr_bf16")
 METRIC = "verified chain-steps/sec + mean accepted steps per block; % MFMA / HBM peak"
 
 
@@ -48,29 +50,55 @@ def _counts_from_trace(trace, N, K):
     return np.array(act), np.array(rows_verified), np.array(rows_target)
 
 
-def algorithmic_work(name, B, K, d, M, act, rows_verified, runs):
-    """(bound, total algorithmic bytes or flops) of a kernel over `runs` sampler runs.
+def algorithmic_work(name, B, K, d, M, act, rows_verified, runs, nct=1):
+    """(flops, bytes, dtype bytes) of a kernel's algorithmic work over `runs` sampler runs.
 
-    Units: the GEMMs count 2 flops per multiply-add over every row they are
-    launched on (B (K+1) rows per round plus the B rows of the one explicit
-    target call per run); the streaming kernels count the float32 bytes their
-    rows must move once (active chains only).  Rounds launched after every
-    chain has finished exit at once and count no work.
+    Units per round: the GEMMs are launched on all B (K+1) rows (2 flops per
+    multiply-add) and must move their operands and outputs once: the logits
+    GEMM reads X and mu and produces the R x M logits, the mean GEMM reads X,
+    m^p and mu and writes m^q; the explicit target call at Y_0 (one per run)
+    covers B rows.  The streaming kernels count the float32 bytes their rows
+    move once, for active chains only: advance reads the residual's two rows
+    and the cache's two rows and writes the new state, K+1 drafts and K draft
+    means.  Rounds launched after every chain has finished exit at once and
+    count no work.  Returns None for kernels without a throughput roof
+    (latency-bound scalar work).
     """
-    rows = B * (K + 1) * len(act) + B
-    if name == "gmm_logits":
-        return "mfma", 2.0 * rows * d * M * runs
-    if name in ("gmm_mean", "gmm_mean_lr"):
-        return "mfma", 2.0 * rows * M * d * runs
+    rounds = len(act)
+    R = B * (K + 1)
+    bf = name.endswith("_bf16")
+    eb = 2 if bf else 4
+    if name in ("gmm_logits", "gmm_logits_bf16"):
+        rows = R * rounds + B
+        return 2.0 * rows * d * M * runs, (rows * d * 4 + rows * M * 4 + (rounds + 1) * M * d * eb) * runs, eb
+    if name in ("gmm_mean_lr", "gmm_mean_lr_bf16"):
+        rows = R * rounds
+        return (2.0 * rows * M * d * runs,
+                (rows * d * 8 + B * K * rounds * d * 4 + rounds * M * d * eb) * runs, eb)
+    if name in ("gmm_mean", "gmm_mean_bf16"):
+        return 2.0 * B * M * d * runs, (B * d * 8 + M * d * eb) * runs, eb
+    if name == "gmm_softmax":
+        rows = R * rounds + B
+        return 0.0, rows * M * (4 + eb) * runs, eb
     if name == "logratio_reduce":
-        return "hbm", 3.0 * 4 * d * rows_verified.sum() * runs
-    if name == "draft_block":   # reads y and the cached (x, m^q) row; writes K+1 drafts, K means
-        return "hbm", 4.0 * d * (3 + (K + 1) + K) * act.sum() * runs
-    if name == "residual_commit":   # reads two rows, writes the new state
-        return "hbm", 4.0 * d * 3 * act.sum() * runs
-    if name == "advance":   # residual rows, cache rows; new state, K+1 drafts, K means
-        return "hbm", 4.0 * d * (4 + 1 + (K + 1) + K) * act.sum() * runs
-    return None, 0.0
+        return 0.0, 3.0 * 4 * d * rows_verified.sum() * runs, 4
+    if name == "draft_block":   # one per run: reads y and the cached (x, m^q) row; K+1 drafts, K means
+        return 0.0, 4.0 * d * (3 + (K + 1) + K) * B * runs, 4
+    if name == "advance":
+        return 0.0, 4.0 * d * (4 + 1 + (K + 1) + K) * act.sum() * runs, 4
+    return None
+
+
+def roof_entry(flops, nbytes, ms, eb):
+    """Binding roof of a kernel: the one its algorithmic work needs more time on."""
+    sec = ms * 1e-3
+    mf_peak = (BF16_PEAK_TFLOPS if eb == 2 else FP32_PEAK_TFLOPS) * 1e12
+    t_mfma, t_hbm = flops / mf_peak, nbytes / (HBM_PEAK_GBS * 1e9)
+    if t_mfma >= t_hbm:
+        return dict(bound="mfma", achieved=flops / sec / 1e12, unit="TFLOP/s", peak=mf_peak / 1e12,
+                    frac=t_mfma / sec, algorithmic_flops=flops, algorithmic_bytes=nbytes)
+    return dict(bound="hbm", achieved=nbytes / sec / 1e9, unit="GB/s", peak=HBM_PEAK_GBS,
+                frac=t_hbm / sec, algorithmic_flops=flops, algorithmic_bytes=nbytes)
 
 
 def run_sampler_bench(lib, name, mode, steps, warmup, profile):
@@ -79,7 +107,8 @@ def run_sampler_bench(lib, name, mode, steps, warmup, profile):
     cfg = WORKLOADS[name]
     B, K, N, d, M = cfg["B"], cfg["K"], cfg["N"], cfg["d"], cfg["M"]
     p = workload_gmm(name)
-    tgt = lib.Target(lib.schedule(N), p["mu"], p["var"], p["log_w"])
+    prec = lib.SD_BF16 if cfg["precision"] == "bf16" else lib.SD_FP32
+    tgt = lib.Target(lib.schedule(N), p["mu"], p["var"], p["log_w"], precision=prec)
     ws = torch.empty(lib.sd_sampler_workspace(tgt, B, K), dtype=torch.uint8, device="cuda")
     y = torch.empty(B, d, dtype=torch.float32, device="cuda")
     seed = 0
@@ -137,21 +166,27 @@ def roofline_of(res, steps):
     sources[name] = prof[name]
     for kname, (launches, ms) in sources.items():
         runs = steps if kname == name else 1
-        bound, work = algorithmic_work(kname, res["B"], res["K"], res["d"], res["M"], res["act"],
-                                       res["rows_verified"], runs)
         entry = dict(launches=launches, avg_us=1e3 * ms / max(launches, 1), total_ms=ms)
-        if bound == "hbm":
-            entry.update(bound="hbm", achieved=work / (ms * 1e-3) / 1e9, unit="GB/s", peak=HBM_PEAK_GBS)
-        elif bound == "mfma":
-            entry.update(bound="mfma", achieved=work / (ms * 1e-3) / 1e12, unit="TFLOP/s",
-                         peak=FP32_PEAK_TFLOPS)
-        if bound:
-            entry["frac"] = entry["achieved"] / entry["peak"]
-            entry["algorithmic_per_launch"] = work / max(launches, 1)
+        w = algorithmic_work(kname, res["B"], res["K"], res["d"], res["M"], res["act"],
+                             res["rows_verified"], runs)
+        if w is not None:
+            entry.update(roof_entry(w[0], w[1], ms, w[2]))
         table[kname] = entry
+    gem = [k for k in GEMMS if k in res["breakdown"]]
+    if gem:
+        # the denoiser's GEMMs together over the profiled run, against the matrix-core peak
+        flops = sum(algorithmic_work(k, res["B"], res["K"], res["d"], res["M"], res["act"],
+                                     res["rows_verified"], 1)[0] for k in gem)
+        ms = sum(res["breakdown"][k][1] for k in gem)
+        peak = BF16_PEAK_TFLOPS if gem[0].endswith("_bf16") else FP32_PEAK_TFLOPS
+        table["denoiser_gemms"] = dict(bound="mfma", achieved=flops / (ms * 1e-3) / 1e12, unit="TFLOP/s",
+                                       peak=peak, frac=flops / (ms * 1e-3) / 1e12 / peak, total_ms=ms)
     e = table[name]
+    per = lambda v: v / max(e["launches"], 1) if v is not None else None
     roof = dict(kernel=name, bound=e.get("bound"), achieved=e.get("achieved"), peak=e.get("peak"),
                 unit=e.get("unit"), frac=e.get("frac"), traffic=None,
+                algorithmic_per_launch=per(e.get("algorithmic_bytes") if e.get("bound") == "hbm"
+                                           else e.get("algorithmic_flops")),
                 avg_launch_us=e["avg_us"], launches=e["launches"])
     return roof, table
 
@@ -227,6 +262,11 @@ def cpu_baseline(name, budget_s):
                        f"{el:.1f} s, single-threaded NumPy float64")
 
 
+def _dtype(name):
+    from paper_2606_13426_amd.inputs import WORKLOADS
+    return "bf16 GEMM operands, f32 accumulate and states" if WORKLOADS[name].get("precision") == "bf16" else "f32"
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -264,7 +304,7 @@ def main():
     roof, table = roofline_of(res, args.steps)
     line = dict(metric=METRIC, value=res["B"] * res["N"] / res["sec"], unit="chain-steps/s", n_gpus=1,
                 steps=args.steps, warmup=args.warmup, ms_per_step=1e3 * res["sec"], higher_is_better=True,
-                scaling="weak", vs_baseline=None, dtype="f32", data="synthetic",
+                scaling="weak", vs_baseline=None, dtype=_dtype(args.workload), data="synthetic",
                 config=dict(workload=args.workload, d=res["d"], M=res["M"], B=res["B"], K=res["K"],
                             N=res["N"], verification="block", drafter="free", usample="exact",
                             parallelism="single-gpu"),
@@ -275,6 +315,21 @@ def main():
         line["token"] = dict(value=tok["B"] * tok["N"] / tok["sec"], ms_per_step=1e3 * tok["sec"],
                              mean_accepted_steps_per_block=tok["be"], rounds_per_run=tok["rounds"])
         line["verify_only"] = verify_bench(lib, args.steps, args.warmup)
+        # the bf16-denoiser workloads, each run end to end (not the headline value)
+        others = {}
+        for wl in ("latent16384", "pixel12288"):
+            if wl == args.workload:
+                continue
+            r2 = run_sampler_bench(lib, wl, lib.SD_BLOCK, 3, 1, profile=True)
+            roof2, table2 = roofline_of(r2, 3)
+            others[wl] = dict(value=r2["B"] * r2["N"] / r2["sec"], unit="chain-steps/s",
+                              ms_per_step=1e3 * r2["sec"], dtype=_dtype(wl),
+                              mean_accepted_steps_per_block=r2["be"], rounds_per_run=r2["rounds"],
+                              config=dict(d=r2["d"], M=r2["M"], B=r2["B"], K=r2["K"], N=r2["N"]),
+                              roofline=roof2, denoiser_gemms=table2.get("denoiser_gemms"),
+                              kernels={k: dict(avg_us=v["avg_us"], bound=v.get("bound"), frac=v.get("frac"))
+                                       for k, v in table2.items() if "avg_us" in v})
+        line["other_workloads"] = others
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_budget)
     print(json.dumps(line))

@@ -30,10 +30,13 @@ __global__ __launch_bounds__(kThreads) void gmm_logits_bf16_kernel(
     double* __restrict__ xsq, const int* gate) {
   if (gate && *gate == 0) return;
   __shared__ OperandLds sm;
-  // grid (splits, row tiles, column tiles), split fastest (as the float32 path)
-  const int nsplit = gridDim.x, nrt = gridDim.y;
-  const int lin = xcd_tile(nsplit * nrt * gridDim.z);
-  const int s = lin % nsplit, rt = (lin / nsplit) % nrt, ct = lin / (nsplit * nrt);
+  // grid (column tiles, row tiles, splits).  Each XCD takes a contiguous range
+  // of the tile order (column tile fastest, split slowest): the column tiles
+  // that share a block of X run together and read it once into that XCD's L2,
+  // and one XCD keeps to one k-range of mu while it walks the row tiles.
+  const int nct = gridDim.x, nrt = gridDim.y;
+  const int lin = xcd_tile(nct * nrt * gridDim.z);
+  const int ct = lin % nct, rt = (lin / nct) % nrt, s = lin / (nct * nrt);
   const int r0 = rt * TM, c0 = ct * TN;
   const int kbeg = s * ksplit, kend = min(d, kbeg + ksplit);
   f32x16 acc[2][2];
@@ -70,6 +73,23 @@ __global__ __launch_bounds__(kThreads) void gmm_logits_bf16_kernel(
       if ((threadIdx.x & 15) == 0 && row < R) xsq[(int64_t)s * R + row] = t;
     }
   }
+}
+
+// Tile of a (column tiles) x (row tiles) grid for the mean GEMM.  Its B
+// operand is the slice of mu^T of the column tile, re-read by every row tile,
+// so each XCD owns a contiguous eighth of the column tiles and walks all row
+// tiles over them (the slices stay in its L2); inside an XCD consecutive
+// workgroups take consecutive column tiles of one row tile (shared P rows).
+__device__ __forceinline__ void col_major_xcd(int nct, int nrt, int& ct, int& rt) {
+  const int L = blockIdx.x + gridDim.x * blockIdx.y;
+  if (nct % 8 != 0) {
+    ct = L % nct;
+    rt = L / nct;
+    return;
+  }
+  const int per = nct / 8, i = L / 8;
+  ct = (L % 8) * per + i % per;
+  rt = i / per;
 }
 
 // Pass p of the epilogue stages accumulator blocks qb = p of every wavefront:
@@ -129,8 +149,8 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_bf16_kernel(
   __shared__ OperandLds sm;
   __shared__ float rc[3 * TM];
   const int nct = gridDim.x;
-  const int lin = xcd_tile(nct * gridDim.y);
-  const int ct = lin % nct, rt = lin / nct;
+  int ct, rt;
+  col_major_xcd(nct, gridDim.y, ct, rt);
   const int r0 = rt * TM, c0 = ct * TN;
   load_rc(rc, rowc, r0, R);
   f32x16 acc[2][2];
@@ -180,8 +200,8 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_bf16_kernel(
   __shared__ float rc[3 * TM];
   __shared__ float gz[kMaxChains * LDO];
   const int nct = gridDim.x;
-  const int lin = xcd_tile(nct * gridDim.y);
-  const int ct = lin % nct, rt = lin / nct;
+  int ct, rt;
+  col_major_xcd(nct, gridDim.y, ct, rt);
   const int r0 = rt * TM, c0 = ct * TN;
   load_rc(rc, rowc, r0, R);
   f32x16 acc[2][2];
@@ -319,7 +339,7 @@ Bufs carve(const Plan& p, void* ws) {
 hipError_t logits_and_softmax(const Target& t, const Plan& p, const Bufs& w, int R,
                               const float* x, int64_t ldx, bool vecx, const int32_t* step,
                               hipStream_t s, const int* gate) {
-  dim3 g1(p.S, (R + TM - 1) / TM, (t.M + TN - 1) / TN);
+  dim3 g1((t.M + TN - 1) / TN, (R + TM - 1) / TM, p.S);
   hipError_t e = timed("gmm_logits_bf16", s, [&] {
     gmm_logits_bf16_kernel<<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, vecx, t.mu16,
                                                    t.d % 8 == 0, p.ksplit, w.part, w.xsq, gate);
