@@ -6,8 +6,8 @@
 // 2 x 2 layout each own a 64 x 64 sub-tile (2 x 2 blocks of 32 x 32).  k is
 // staged through LDS in chunks of 64; within a chunk, MFMA step s (< 4) takes
 // k = 16 s + 8 h + (0..7) from lane half h of both operands, so a lane reads
-// its eight values of a row as one 16-byte LDS load.  The next chunk is
-// fetched into registers while the current one is multiplied.
+// its eight values of a row as one 16-byte LDS load.  Chunks are pipelined
+// through two LDS buffers and two register sets (see tile()).
 #pragma once
 
 #include "common.hpp"
@@ -53,52 +53,80 @@ struct Chunk<uint16_t> {
   uint4 v[4];
 };
 
+// Buffer view of the (at most TM) rows of one tile of a row-major matrix:
+// reads at byte offsets past the rows that exist return zero in hardware.
+// The host guarantees TM * ld * sizeof(T) < 2^31 for the VEC path.
+constexpr uint32_t kBufferWord3 = 0x00020000;  // raw buffer, 32-bit dwords (gfx9 family)
+
+// The base and size are wavefront-uniform; readfirstlane says so to the
+// compiler, which otherwise wraps every load in a loop over distinct values.
+template <class T>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_view(const T* A, int64_t ld, int nrows, int r0) {
+  const int rows = max(0, min(nrows - r0, TM));
+  const uint64_t base = reinterpret_cast<uint64_t>(A + (int64_t)r0 * ld);
+  const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)base);
+  const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(base >> 32));
+  const int bytes = __builtin_amdgcn_readfirstlane((int)((int64_t)rows * ld * (int64_t)sizeof(T)));
+  return __builtin_amdgcn_make_buffer_rsrc(reinterpret_cast<void*>(((uint64_t)hi << 32) | lo),
+                                           (short)0, bytes, (int)kBufferWord3);
+}
+
 // Rows r0.., columns k0.. (< kend) of a row-major matrix with row stride ld;
-// out-of-range elements read as zero.  vec: rows and k0 are 16-byte aligned.
-__device__ __forceinline__ void load(const float* __restrict__ A, int64_t ld, int nrows, int r0,
-                                     int k0, int kend, bool vec, Chunk<float>& c) {
+// out-of-range elements read as zero.  VEC: rows are 16-byte aligned and the
+// k range is a whole number of chunks, so only rows can be out of range: one
+// unconditional buffer load per 16-byte piece (rows past the end read zero
+// from the view), which lets the compiler count the loads in flight.
+// Otherwise element by element.
+template <bool VEC>
+__device__ __forceinline__ void load(const float* __restrict__ A, __amdgpu_buffer_rsrc_t view,
+                                     int64_t ld, int nrows, int r0, int k0, int kend,
+                                     Chunk<float>& c) {
   const int t = threadIdx.x;
   const int kc = k0 + 4 * (t & 15);
 #pragma unroll
   for (int h = 0; h < 8; ++h) {
-    const int r = r0 + (t >> 4) + 16 * h;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < nrows) {
-      const float* p = A + (int64_t)r * ld + kc;
-      if (vec && kc + 3 < kend) {
-        v = *reinterpret_cast<const float4*>(p);
-      } else {
+    const int rr = (t >> 4) + 16 * h;
+    if constexpr (VEC) {
+      const uint32_t off = (uint32_t)((rr * (int)ld + kc) * 4);
+      c.v[h] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(view, off, 0, 0));
+    } else {
+      const int r = r0 + rr;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (r < nrows) {
+        const float* p = A + (int64_t)r * ld + kc;
         if (kc < kend) v.x = p[0];
         if (kc + 1 < kend) v.y = p[1];
         if (kc + 2 < kend) v.z = p[2];
         if (kc + 3 < kend) v.w = p[3];
       }
+      c.v[h] = v;
     }
-    c.v[h] = v;
   }
 }
 
-__device__ __forceinline__ void load(const uint16_t* __restrict__ A, int64_t ld, int nrows, int r0,
-                                     int k0, int kend, bool vec, Chunk<uint16_t>& c) {
+template <bool VEC>
+__device__ __forceinline__ void load(const uint16_t* __restrict__ A, __amdgpu_buffer_rsrc_t view,
+                                     int64_t ld, int nrows, int r0, int k0, int kend,
+                                     Chunk<uint16_t>& c) {
   const int t = threadIdx.x;
   const int kc = k0 + 8 * (t & 7);
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
-    const int r = r0 + (t >> 3) + 32 * h;
-    uint4 v = make_uint4(0u, 0u, 0u, 0u);
-    if (r < nrows) {
-      const uint16_t* p = A + (int64_t)r * ld + kc;
-      if (vec && kc + 7 < kend) {
-        v = *reinterpret_cast<const uint4*>(p);
-      } else {
-        uint32_t w[4] = {0u, 0u, 0u, 0u};
+    const int rr = (t >> 3) + 32 * h;
+    if constexpr (VEC) {
+      const uint32_t off = (uint32_t)((rr * (int)ld + kc) * 2);
+      c.v[h] = __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(view, off, 0, 0));
+    } else {
+      const int r = r0 + rr;
+      uint32_t w[4] = {0u, 0u, 0u, 0u};
+      if (r < nrows) {
+        const uint16_t* p = A + (int64_t)r * ld + kc;
 #pragma unroll
         for (int e = 0; e < 8; ++e)
           if (kc + e < kend) w[e >> 1] |= (uint32_t)p[e] << (16 * (e & 1));
-        v = make_uint4(w[0], w[1], w[2], w[3]);
       }
+      c.v[h] = make_uint4(w[0], w[1], w[2], w[3]);
     }
-    c.v[h] = v;
   }
 }
 
@@ -163,26 +191,65 @@ __device__ __forceinline__ void zero(f32x16 (&acc)[2][2]) {
 
 // Accumulate tile (r0, c0) of A[nra][.] B[nrb][.]^T over k in [kbeg, kend).
 // With SQ (float32 A only) also the float64 squares of this thread's A rows.
-template <bool SQ, class TA>
-__device__ __forceinline__ void tile(OperandLds& sm, const TA* __restrict__ A, int64_t lda,
-                                     int nra, bool veca, const uint16_t* __restrict__ Bm,
-                                     int64_t ldb, int nrb, bool vecb, int r0, int c0, int kbeg,
-                                     int kend, f32x16 (&acc)[2][2], double (&sq)[8]) {
-  Chunk<TA> ra;
-  Chunk<uint16_t> rb;
-  load(A, lda, nra, r0, kbeg, kend, veca, ra);
-  load(Bm, ldb, nrb, c0, kbeg, kend, vecb, rb);
-  for (int k0 = kbeg; k0 < kend; k0 += KC) {
-    __syncthreads();
-    store(sm.a, ra);
-    store(sm.b, rb);
-    if constexpr (SQ) add_squares(ra, sq);
-    __syncthreads();
-    if (k0 + KC < kend) {
-      load(A, lda, nra, r0, k0 + KC, kend, veca, ra);
-      load(Bm, ldb, nrb, c0, k0 + KC, kend, vecb, rb);
+// VEC: see load().
+//
+// Software pipeline: two LDS buffers and two register sets.  Step c multiplies
+// the chunk in LDS buffer c % 2, then stores chunk c + 1 (fetched two steps
+// earlier) into the other buffer and issues the global loads of chunk c + 3
+// into the register set just freed; one barrier per step.  The matrix cores
+// work on step c while chunk c + 1's loads complete, and two chunks are in
+// flight per workgroup.  The caller's first use of sm after this returns must
+// follow a barrier.
+template <bool SQ, bool VEC, class TA>
+__device__ __forceinline__ void tile(OperandLds (&sm)[2], const TA* __restrict__ A, int64_t lda,
+                                     int nra, const uint16_t* __restrict__ Bm, int64_t ldb, int nrb,
+                                     int r0, int c0, int kbeg, int kend, f32x16 (&acc)[2][2],
+                                     double (&sq)[8]) {
+  const int n = (kend - kbeg + KC - 1) / KC;
+  const __amdgpu_buffer_rsrc_t va = tile_view(A, lda, nra, r0);
+  const __amdgpu_buffer_rsrc_t vb = tile_view(Bm, ldb, nrb, c0);
+  Chunk<TA> ra0, ra1;
+  Chunk<uint16_t> rb0, rb1;
+  load<VEC>(A, va, lda, nra, r0, kbeg, kend, ra0);
+  load<VEC>(Bm, vb, ldb, nrb, c0, kbeg, kend, rb0);
+  if (n > 1) {
+    load<VEC>(A, va, lda, nra, r0, kbeg + KC, kend, ra1);
+    load<VEC>(Bm, vb, ldb, nrb, c0, kbeg + KC, kend, rb1);
+  }
+  store(sm[0].a, ra0);
+  store(sm[0].b, rb0);
+  if constexpr (SQ) add_squares(ra0, sq);
+  if (n > 2) {
+    load<VEC>(A, va, lda, nra, r0, kbeg + 2 * KC, kend, ra0);
+    load<VEC>(Bm, vb, ldb, nrb, c0, kbeg + 2 * KC, kend, rb0);
+  }
+  __syncthreads();
+  int c = 0;
+  for (; c + 2 <= n; c += 2) {
+    mma_chunk(sm[0], acc);
+    store(sm[1].a, ra1);
+    store(sm[1].b, rb1);
+    if constexpr (SQ) add_squares(ra1, sq);
+    if (c + 3 < n) {
+      load<VEC>(A, va, lda, nra, r0, kbeg + (c + 3) * KC, kend, ra1);
+      load<VEC>(Bm, vb, ldb, nrb, c0, kbeg + (c + 3) * KC, kend, rb1);
     }
-    mma_chunk(sm, acc);
+    __syncthreads();
+    mma_chunk(sm[1], acc);
+    if (c + 2 < n) {
+      store(sm[0].a, ra0);
+      store(sm[0].b, rb0);
+      if constexpr (SQ) add_squares(ra0, sq);
+    }
+    if (c + 4 < n) {
+      load<VEC>(A, va, lda, nra, r0, kbeg + (c + 4) * KC, kend, ra0);
+      load<VEC>(Bm, vb, ldb, nrb, c0, kbeg + (c + 4) * KC, kend, rb0);
+    }
+    __syncthreads();
+  }
+  if (c < n) {  // an odd last chunk, already in buffer 0
+    mma_chunk(sm[0], acc);
+    __syncthreads();
   }
 }
 

@@ -22,14 +22,16 @@ using namespace bf16;
 constexpr int LDO = 68;         // staging row stride in floats (one 64-column pass)
 constexpr int kMaxChains = 65;  // chains that 128 rows of [B][K+1] can touch (K+1 >= 2)
 
-static_assert(sizeof(float) * TM * LDO <= sizeof(OperandLds), "staging must fit the operand LDS");
+static_assert(sizeof(float) * TM * LDO <= sizeof(OperandLds), "staging must fit one operand buffer");
+static_assert(sizeof(float) * kMaxChains * LDO <= sizeof(OperandLds), "G must fit one operand buffer");
 
-__global__ __launch_bounds__(kThreads) void gmm_logits_bf16_kernel(
-    int R, int M, int d, const float* __restrict__ X, int64_t ldx, bool vecx,
-    const uint16_t* __restrict__ mu, bool vecmu, int ksplit, float* __restrict__ part,
+template <bool VEC>
+__global__ __launch_bounds__(kThreads, 2) void gmm_logits_bf16_kernel(
+    int R, int M, int d, const float* __restrict__ X, int64_t ldx,
+    const uint16_t* __restrict__ mu, int ksplit, float* __restrict__ part,
     double* __restrict__ xsq, const int* gate) {
   if (gate && *gate == 0) return;
-  __shared__ OperandLds sm;
+  __shared__ OperandLds sm[2];
   // grid (column tiles, row tiles, splits).  Each XCD takes a contiguous range
   // of the tile order (column tile fastest, split slowest): the column tiles
   // that share a block of X run together and read it once into that XCD's L2,
@@ -44,9 +46,9 @@ __global__ __launch_bounds__(kThreads) void gmm_logits_bf16_kernel(
   double sq[8] = {0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0, 0.0};
   const bool want_sq = ct == 0;
   if (want_sq)
-    tile<true>(sm, X, ldx, R, vecx, mu, d, M, vecmu, r0, c0, kbeg, kend, acc, sq);
+    tile<true, VEC>(sm, X, ldx, R, mu, d, M, r0, c0, kbeg, kend, acc, sq);
   else
-    tile<false>(sm, X, ldx, R, vecx, mu, d, M, vecmu, r0, c0, kbeg, kend, acc, sq);
+    tile<false, VEC>(sm, X, ldx, R, mu, d, M, r0, c0, kbeg, kend, acc, sq);
   float* ps = part + (int64_t)s * R * M;
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
@@ -94,8 +96,6 @@ __device__ __forceinline__ void col_major_xcd(int nct, int nrt, int& ct, int& rt
 
 // Pass p of the epilogue stages accumulator blocks qb = p of every wavefront:
 // tile columns 64 wc + 32 p + (0..31) go to staging columns 32 wc + (0..31).
-// In the epilogue thread t owns tile row t/2 and staging columns
-// 32 (t % 2) .. + 31, i.e. tile columns 64 (t % 2) + 32 p .. + 31.
 __device__ __forceinline__ void stage(float* stg, const f32x16 (&acc)[2][2], int p) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int sc = 32 * (w & 1) + (lane & 31);
@@ -105,33 +105,32 @@ __device__ __forceinline__ void stage(float* stg, const f32x16 (&acc)[2][2], int
     for (int v = 0; v < 16; ++v) stg[out_row(qa, v) * LDO + sc] = acc[qa][p][v];
 }
 
+// Epilogue layout.  Thread t owns staging columns 4 cg .. 4 cg + 3 (cg = t % 16)
+// of tile rows rg + 16 i (rg = t / 16, i < 8): tile columns
+// 64 (cg / 8) + 32 p + 4 (cg % 8) .. + 3 in pass p.  A wavefront's load of one
+// i covers four rows x 2 x 128 contiguous bytes, so global accesses are
+// whole cache lines.
+__device__ __forceinline__ int epi_col(int cg, int p) { return 64 * (cg >> 3) + 32 * p + 4 * (cg & 7); }
+
 __device__ __forceinline__ void load_rc(float* rc, const float* __restrict__ rowc, int r0, int R) {
   for (int e = threadIdx.x; e < 3 * TM; e += kThreads)
     rc[e] = r0 + e / 3 < R ? rowc[3 * (int64_t)r0 + e] : 0.f;
 }
 
-// Eight float4 of a row span starting at p (cnt valid elements from there).
-__device__ __forceinline__ void load32(const float* p, int cnt, bool vec, float4 (&v)[8]) {
-#pragma unroll
-  for (int q = 0; q < 8; ++q) {
-    const int c = cnt - 4 * q;
-    if (vec && c >= 4) {
-      v[q] = *reinterpret_cast<const float4*>(p + 4 * q);
-    } else {
-      v[q] = make_float4(c > 0 ? p[4 * q] : 0.f, c > 1 ? p[4 * q + 1] : 0.f,
-                         c > 2 ? p[4 * q + 2] : 0.f, c > 3 ? p[4 * q + 3] : 0.f);
-    }
-  }
+__device__ __forceinline__ float4 ld4(const float* p, int cnt, bool vec) {
+  if (vec && cnt >= 4) return *reinterpret_cast<const float4*>(p);
+  return make_float4(cnt > 0 ? p[0] : 0.f, cnt > 1 ? p[1] : 0.f, cnt > 2 ? p[2] : 0.f,
+                     cnt > 3 ? p[3] : 0.f);
 }
 
-__device__ __forceinline__ void store4v(float* p, int c, bool vec, float4 v) {
-  if (vec && c >= 4) {
+__device__ __forceinline__ void st4(float* p, int cnt, bool vec, float4 v) {
+  if (vec && cnt >= 4) {
     *reinterpret_cast<float4*>(p) = v;
   } else {
-    if (c > 0) p[0] = v.x;
-    if (c > 1) p[1] = v.y;
-    if (c > 2) p[2] = v.z;
-    if (c > 3) p[3] = v.w;
+    if (cnt > 0) p[0] = v.x;
+    if (cnt > 1) p[1] = v.y;
+    if (cnt > 2) p[2] = v.z;
+    if (cnt > 3) p[3] = v.w;
   }
 }
 
@@ -139,14 +138,37 @@ __device__ __forceinline__ float comp(const float4& v, int c) {
   return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w;
 }
 
+// Sum over the 16 lanes of a column group of eight per-row values, as a
+// butterfly reduce-scatter: after the exchanges at distance 8, 4 and 2 a lane
+// holds one row, i = 4 bit3 + 2 bit2 + bit1 of its lane index in the group,
+// summed over eight lanes; the last exchange completes the sum (same value
+// in lanes 2k and 2k + 1).  Fixed order, so the result is deterministic.
+__device__ __forceinline__ double reduce_rows16(const double (&v)[8], int cg) {
+  const bool b3 = cg & 8, b2 = cg & 4, b1 = cg & 2;
+  double w[4], u[2];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const double send = b3 ? v[i] : v[i + 4];
+    w[i] = (b3 ? v[i + 4] : v[i]) + __shfl_xor(send, 8);
+  }
+#pragma unroll
+  for (int i = 0; i < 2; ++i) {
+    const double send = b2 ? w[i] : w[i + 2];
+    u[i] = (b2 ? w[i + 2] : w[i]) + __shfl_xor(send, 4);
+  }
+  const double z = (b1 ? u[1] : u[0]) + __shfl_xor(b1 ? u[0] : u[1], 2);
+  return z + __shfl_xor(z, 1);
+}
+
 // Public target call: m^q = c1 x + c2 (O - rho x) (and the score if asked).
-__global__ __launch_bounds__(kThreads) void gmm_mean_bf16_kernel(
-    int R, int M, int d, const uint16_t* __restrict__ P, bool vecp,
+template <bool VEC>
+__global__ __launch_bounds__(kThreads, 2) void gmm_mean_bf16_kernel(
+    int R, int M, int d, const uint16_t* __restrict__ P,
     const uint16_t* __restrict__ muT, const float* __restrict__ X, int64_t ldx, bool vecx,
     const float* __restrict__ rowc, float* __restrict__ mq, int64_t ldq, bool vecq,
     float* __restrict__ score, int64_t lds, bool vecs, const int* gate) {
   if (gate && *gate == 0) return;
-  __shared__ OperandLds sm;
+  __shared__ OperandLds sm[2];
   __shared__ float rc[3 * TM];
   const int nct = gridDim.x;
   int ct, rt;
@@ -156,32 +178,36 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_bf16_kernel(
   f32x16 acc[2][2];
   zero(acc);
   double unused[8];
-  tile<false>(sm, P, M, R, vecp, muT, M, d, vecp, r0, c0, 0, M, acc, unused);
-  float* stg = reinterpret_cast<float*>(&sm);
-  const int lr = threadIdx.x >> 1, gsel = threadIdx.x & 1;
-  const int row = r0 + lr;
+  tile<false, VEC>(sm, P, M, R, muT, M, d, r0, c0, 0, M, acc, unused);
+  float* stg = reinterpret_cast<float*>(&sm[0]);
+  const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
-    __syncthreads();  // operand tiles (p = 0) or the previous pass are consumed
+    __syncthreads();  // the operand tiles (p = 0) or the previous pass are consumed
     stage(stg, acc, p);
     __syncthreads();
-    if (row >= R) continue;
-    const int col = c0 + 64 * gsel + 32 * p;
-    const int cnt = min(32, d - col);
+    const int col = c0 + epi_col(cg, p);
+    const int cnt = min(4, d - col);
     if (cnt <= 0) continue;
     float4 xv[8];
-    load32(X + (int64_t)row * ldx + col, cnt, vecx, xv);
-    const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
-    const float* o = &stg[lr * LDO + 32 * gsel];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const float4 ov = *reinterpret_cast<const float4*>(o + 4 * q);
-      const float4 sv = make_float4(ov.x - rho * xv[q].x, ov.y - rho * xv[q].y,
-                                    ov.z - rho * xv[q].z, ov.w - rho * xv[q].w);
-      const float4 qv = make_float4(c1 * xv[q].x + c2 * sv.x, c1 * xv[q].y + c2 * sv.y,
-                                    c1 * xv[q].z + c2 * sv.z, c1 * xv[q].w + c2 * sv.w);
-      store4v(mq + (int64_t)row * ldq + col + 4 * q, cnt - 4 * q, vecq, qv);
-      if (score) store4v(score + (int64_t)row * lds + col + 4 * q, cnt - 4 * q, vecs, sv);
+    for (int i = 0; i < 8; ++i) {
+      const int row = r0 + rg + 16 * i;
+      xv[i] = row < R ? ld4(X + (int64_t)row * ldx + col, cnt, vecx) : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int lr = rg + 16 * i, row = r0 + lr;
+      if (row >= R) continue;
+      const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
+      const float4 ov = *reinterpret_cast<const float4*>(&stg[lr * LDO + 4 * cg]);
+      const float4 x = xv[i];
+      const float4 sv = make_float4(ov.x - rho * x.x, ov.y - rho * x.y, ov.z - rho * x.z,
+                                    ov.w - rho * x.w);
+      st4(mq + (int64_t)row * ldq + col, cnt, vecq,
+          make_float4(c1 * x.x + c2 * sv.x, c1 * x.y + c2 * sv.y, c1 * x.z + c2 * sv.z,
+                      c1 * x.w + c2 * sv.w));
+      if (score) st4(score + (int64_t)row * lds + col, cnt, vecs, sv);
     }
   }
 }
@@ -190,15 +216,15 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_bf16_kernel(
 // partials: for draft rows j < K and this tile's columns, float64 sums of
 // (m^p - m^q)^2, (yhat_{j+1} - m^p)(m^p - m^q) and G (m^p - m^q), G the
 // residual's normals of the chain's round, into lrp[row][column tile][3].
-__global__ __launch_bounds__(kThreads) void gmm_mean_lr_bf16_kernel(
-    int R, int M, int d, int K1, const uint16_t* __restrict__ P, bool vecp,
+template <bool VEC>
+__global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
+    int R, int M, int d, int K1, const uint16_t* __restrict__ P,
     const uint16_t* __restrict__ muT, const float* __restrict__ X, const float* __restrict__ rowc,
     const float* __restrict__ MP, float* __restrict__ mq, double* __restrict__ lrp, bool vecd,
     const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
   if (gate && *gate == 0) return;
-  __shared__ OperandLds sm;
+  __shared__ OperandLds sm[2];
   __shared__ float rc[3 * TM];
-  __shared__ float gz[kMaxChains * LDO];
   const int nct = gridDim.x;
   int ct, rt;
   col_major_xcd(nct, gridDim.y, ct, rt);
@@ -207,79 +233,84 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_bf16_kernel(
   f32x16 acc[2][2];
   zero(acc);
   double unused[8];
-  tile<false>(sm, P, M, R, vecp, muT, M, d, vecp, r0, c0, 0, M, acc, unused);
-  float* stg = reinterpret_cast<float*>(&sm);
-  const int lr = threadIdx.x >> 1, gsel = threadIdx.x & 1;
-  const int row = r0 + lr;
-  const int b = row / K1, j = row - b * K1;
-  const bool has_row = row < R;
-  const bool has_draft = has_row && j < K1 - 1;
+  tile<false, VEC>(sm, P, M, R, muT, M, d, r0, c0, 0, M, acc, unused);
+  float* stg = reinterpret_cast<float*>(&sm[0]);
+  float* gz = reinterpret_cast<float*>(&sm[1]);
+  const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;
   const int b_first = r0 / K1;
   const int nchain = min((min(r0 + TM, R) - 1) / K1 - b_first + 1, kMaxChains);
-  double s2 = 0.0, sz = 0.0, sgd = 0.0;
+  double t2 = 0.0, tz = 0.0, tg = 0.0;  // this lane's row (see reduce_rows16), both passes
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
     __syncthreads();
     stage(stg, acc, p);
     // G of this pass's columns for every chain of the tile, four coordinates
-    // (one Philox block) per item: staging column 4 gq is tile column
-    // 64 (gq / 8) + 32 p + 4 (gq % 8)
+    // (one Philox block) per item, at the staging column of those coordinates
     for (int e = threadIdx.x; e < nchain * 16; e += kThreads) {
       const int cl = e >> 4, gq = e & 15;
       const int bb = b_first + cl;
-      const int tcol = c0 + 64 * (gq >> 3) + 32 * p + 4 * (gq & 7);
+      const int tcol = c0 + epi_col(gq, p);
       const float4 z = normals4(philox((uint32_t)(tcol >> 2), (uint32_t)bb, rnd[bb],
                                        TAG_RESID << 24, seed));
       *reinterpret_cast<float4*>(&gz[cl * LDO + 4 * gq]) = z;
     }
     __syncthreads();
-    if (!has_row) continue;
-    const int col = c0 + 64 * gsel + 32 * p;
-    const int cnt = min(32, d - col);
-    if (cnt <= 0) continue;
+    const int col = c0 + epi_col(cg, p);
+    const int cnt = max(0, min(4, d - col));
+    // every global load of the pass first, then the arithmetic
     float4 xv[8], yv[8], pv[8];
-    const float* px = X + (int64_t)row * d + col;
-    load32(px, cnt, vecd, xv);
-    if (has_draft) {
-      load32(px + d, cnt, vecd, yv);
-      load32(MP + ((int64_t)b * (K1 - 1) + j) * d + col, cnt, vecd, pv);
-    }
-    const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
-    const float* o = &stg[lr * LDO + 32 * gsel];
-    const float* g = &gz[(b - b_first) * LDO + 32 * gsel];
 #pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      const float4 ov = *reinterpret_cast<const float4*>(o + 4 * q);
-      const float4 x = xv[q];
+    for (int i = 0; i < 8; ++i) {
+      const int row = r0 + rg + 16 * i;
+      const int b = row / K1, j = row - b * K1;
+      const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+      const float* px = X + (int64_t)row * d + col;
+      xv[i] = row < R && cnt > 0 ? ld4(px, cnt, vecd) : z4;
+      const bool dr = row < R && cnt > 0 && j < K1 - 1;
+      yv[i] = dr ? ld4(px + d, cnt, vecd) : z4;
+      pv[i] = dr ? ld4(MP + ((int64_t)b * (K1 - 1) + j) * d + col, cnt, vecd) : z4;
+    }
+    double s2[8], sz[8], sgd[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      s2[i] = sz[i] = sgd[i] = 0.0;
+      const int lr = rg + 16 * i, row = r0 + lr;
+      if (row >= R || cnt == 0) continue;
+      const int b = row / K1, j = row - b * K1;
+      const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
+      const float4 ov = *reinterpret_cast<const float4*>(&stg[lr * LDO + 4 * cg]);
+      const float4 x = xv[i];
       const float4 qv = make_float4(c1 * x.x + c2 * (ov.x - rho * x.x),
                                     c1 * x.y + c2 * (ov.y - rho * x.y),
                                     c1 * x.z + c2 * (ov.z - rho * x.z),
                                     c1 * x.w + c2 * (ov.w - rho * x.w));
-      const int c = cnt - 4 * q;
-      store4v(mq + (int64_t)row * d + col + 4 * q, c, vecd, qv);
-      if (has_draft) {
-        const float4 gv = *reinterpret_cast<const float4*>(g + 4 * q);
+      st4(mq + (int64_t)row * d + col, cnt, vecd, qv);
+      if (j < K1 - 1) {
+        const float4 gv = *reinterpret_cast<const float4*>(&gz[(b - b_first) * LDO + 4 * cg]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          if (e < c) {
-            const double dd = (double)comp(pv[q], e) - (double)comp(qv, e);
-            const double zz = (double)comp(yv[q], e) - (double)comp(pv[q], e);
-            s2 = fma(dd, dd, s2);
-            sz = fma(zz, dd, sz);
-            sgd = fma((double)comp(gv, e), dd, sgd);
+          if (e < cnt) {
+            const double dd = (double)comp(pv[i], e) - (double)comp(qv, e);
+            const double zz = (double)comp(yv[i], e) - (double)comp(pv[i], e);
+            s2[i] = fma(dd, dd, s2[i]);
+            sz[i] = fma(zz, dd, sz[i]);
+            sgd[i] = fma((double)comp(gv, e), dd, sgd[i]);
           }
         }
       }
     }
+    // every lane of the group takes part (rows past R and empty columns add zeros)
+    t2 += reduce_rows16(s2, cg);
+    tz += reduce_rows16(sz, cg);
+    tg += reduce_rows16(sgd, cg);
   }
-  s2 += __shfl_xor(s2, 1);
-  sz += __shfl_xor(sz, 1);
-  sgd += __shfl_xor(sgd, 1);
-  if (gsel == 0 && has_row) {
+  const int mine = 4 * ((cg >> 3) & 1) + 2 * ((cg >> 2) & 1) + ((cg >> 1) & 1);
+  const int row = r0 + rg + 16 * mine;
+  if ((cg & 1) == 0 && row < R) {
     double* o = lrp + ((int64_t)row * nct + ct) * 3;
-    o[0] = s2;
-    o[1] = sz;
-    o[2] = sgd;
+    o[0] = t2;
+    o[1] = tz;
+    o[2] = tg;
   }
 }
 
@@ -340,9 +371,15 @@ hipError_t logits_and_softmax(const Target& t, const Plan& p, const Bufs& w, int
                               const float* x, int64_t ldx, bool vecx, const int32_t* step,
                               hipStream_t s, const int* gate) {
   dim3 g1((t.M + TN - 1) / TN, (R + TM - 1) / TM, p.S);
+  // the buffer-load path: whole chunks of k and 32-bit offsets inside a tile
+  const bool vec = vecx && t.d % KC == 0 && ldx < (int64_t)1 << 22 && t.d < 1 << 22;
   hipError_t e = timed("gmm_logits_bf16", s, [&] {
-    gmm_logits_bf16_kernel<<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, vecx, t.mu16,
-                                                   t.d % 8 == 0, p.ksplit, w.part, w.xsq, gate);
+    if (vec)
+      gmm_logits_bf16_kernel<true><<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu16, p.ksplit,
+                                                           w.part, w.xsq, gate);
+    else
+      gmm_logits_bf16_kernel<false><<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu16, p.ksplit,
+                                                            w.part, w.xsq, gate);
   });
   if (e != hipSuccess) return e;
   return gmm_softmax_launch(t, R, p.S, w.part, w.xsq, step, w.P, true, w.rowc, s, gate);
@@ -364,9 +401,14 @@ hipError_t target_mean_bf16_launch(const Target& t, int R, const float* x, int64
   const bool vecs = score && (lds % 4 == 0) && aligned16(score);
   dim3 g2((t.d + TN - 1) / TN, (R + TM - 1) / TM);
   return timed("gmm_mean_bf16", s, [&] {
-    gmm_mean_bf16_kernel<<<g2, kThreads, 0, s>>>(R, t.M, t.d, w.P, t.M % 8 == 0, t.muT16, x, ldx,
-                                                 vecx, w.rowc, mq, ldq, vecq, score, lds, vecs,
-                                                 gate);
+    if (t.M % KC == 0)
+      gmm_mean_bf16_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, w.P, t.muT16, x, ldx, vecx,
+                                                         w.rowc, mq, ldq, vecq, score, lds, vecs,
+                                                         gate);
+    else
+      gmm_mean_bf16_kernel<false><<<g2, kThreads, 0, s>>>(R, t.M, t.d, w.P, t.muT16, x, ldx, vecx,
+                                                          w.rowc, mq, ldq, vecq, score, lds, vecs,
+                                                          gate);
   });
 }
 
@@ -381,9 +423,14 @@ hipError_t target_mean_lr_bf16_launch(const Target& t, int R, int K1, const floa
   if (e != hipSuccess) return e;
   dim3 g2((t.d + TN - 1) / TN, (R + TM - 1) / TM);
   return timed("gmm_mean_lr_bf16", s, [&] {
-    gmm_mean_lr_bf16_kernel<<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, w.P, t.M % 8 == 0, t.muT16,
-                                                    x, w.rowc, mp, mq, lrp, vecd, rnd, seed,
-                                                    gate);
+    if (t.M % KC == 0)
+      gmm_mean_lr_bf16_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, w.P, t.muT16, x,
+                                                            w.rowc, mp, mq, lrp, vecd, rnd, seed,
+                                                            gate);
+    else
+      gmm_mean_lr_bf16_kernel<false><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, w.P, t.muT16, x,
+                                                             w.rowc, mp, mq, lrp, vecd, rnd, seed,
+                                                             gate);
   });
 }
 
