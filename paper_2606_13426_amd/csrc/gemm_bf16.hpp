@@ -198,8 +198,10 @@ __device__ __forceinline__ void zero(f32x16 (&acc)[2][2]) {
 // earlier) into the other buffer and issues the global loads of chunk c + 3
 // into the register set just freed; one barrier per step.  The matrix cores
 // work on step c while chunk c + 1's loads complete, and two chunks are in
-// flight per workgroup.  The caller's first use of sm after this returns must
-// follow a barrier.
+// flight per workgroup.  The steady state (more than four chunks) has no
+// conditional loads, so the compiler's wait before each store counts exactly
+// the newer loads; the last chunks and short ranges run without prefetch.
+// The caller's first use of sm after this returns must follow a barrier.
 template <bool SQ, bool VEC, class TA>
 __device__ __forceinline__ void tile(OperandLds (&sm)[2], const TA* __restrict__ A, int64_t lda,
                                      int nra, const uint16_t* __restrict__ Bm, int64_t ldb, int nrb,
@@ -210,47 +212,58 @@ __device__ __forceinline__ void tile(OperandLds (&sm)[2], const TA* __restrict__
   const __amdgpu_buffer_rsrc_t vb = tile_view(Bm, ldb, nrb, c0);
   Chunk<TA> ra0, ra1;
   Chunk<uint16_t> rb0, rb1;
-  load<VEC>(A, va, lda, nra, r0, kbeg, kend, ra0);
-  load<VEC>(Bm, vb, ldb, nrb, c0, kbeg, kend, rb0);
-  if (n > 1) {
-    load<VEC>(A, va, lda, nra, r0, kbeg + KC, kend, ra1);
-    load<VEC>(Bm, vb, ldb, nrb, c0, kbeg + KC, kend, rb1);
-  }
-  store(sm[0].a, ra0);
-  store(sm[0].b, rb0);
-  if constexpr (SQ) add_squares(ra0, sq);
-  if (n > 2) {
-    load<VEC>(A, va, lda, nra, r0, kbeg + 2 * KC, kend, ra0);
-    load<VEC>(Bm, vb, ldb, nrb, c0, kbeg + 2 * KC, kend, rb0);
-  }
-  __syncthreads();
-  int c = 0;
-  for (; c + 2 <= n; c += 2) {
-    mma_chunk(sm[0], acc);
-    store(sm[1].a, ra1);
-    store(sm[1].b, rb1);
-    if constexpr (SQ) add_squares(ra1, sq);
-    if (c + 3 < n) {
-      load<VEC>(A, va, lda, nra, r0, kbeg + (c + 3) * KC, kend, ra1);
-      load<VEC>(Bm, vb, ldb, nrb, c0, kbeg + (c + 3) * KC, kend, rb1);
+  auto ld = [&](int c, Chunk<TA>& a, Chunk<uint16_t>& b) {
+    load<VEC>(A, va, lda, nra, r0, kbeg + c * KC, kend, a);
+    load<VEC>(Bm, vb, ldb, nrb, c0, kbeg + c * KC, kend, b);
+  };
+  auto st = [&](OperandLds& buf, const Chunk<TA>& a, const Chunk<uint16_t>& b) {
+    store(buf.a, a);
+    store(buf.b, b);
+    if constexpr (SQ) add_squares(a, sq);
+  };
+  if (n > 4) {
+    ld(0, ra0, rb0);
+    ld(1, ra1, rb1);
+    st(sm[0], ra0, rb0);
+    ld(2, ra0, rb0);
+    __syncthreads();
+    int c = 0;
+    for (; c + 4 < n; c += 2) {
+      mma_chunk(sm[0], acc);
+      st(sm[1], ra1, rb1);
+      ld(c + 3, ra1, rb1);
+      __syncthreads();
+      mma_chunk(sm[1], acc);
+      st(sm[0], ra0, rb0);
+      ld(c + 4, ra0, rb0);
+      __syncthreads();
     }
+    // chunk c is in buffer 0, c + 1 in (ra1, rb1), c + 2 in (ra0, rb0); 3 or 4 remain
+    mma_chunk(sm[0], acc);
+    st(sm[1], ra1, rb1);
+    const bool four = c + 3 < n;
+    if (four) ld(c + 3, ra1, rb1);
     __syncthreads();
     mma_chunk(sm[1], acc);
-    if (c + 2 < n) {
-      store(sm[0].a, ra0);
-      store(sm[0].b, rb0);
-      if constexpr (SQ) add_squares(ra0, sq);
-    }
-    if (c + 4 < n) {
-      load<VEC>(A, va, lda, nra, r0, kbeg + (c + 4) * KC, kend, ra0);
-      load<VEC>(Bm, vb, ldb, nrb, c0, kbeg + (c + 4) * KC, kend, rb0);
-    }
+    st(sm[0], ra0, rb0);
     __syncthreads();
-  }
-  if (c < n) {  // an odd last chunk, already in buffer 0
     mma_chunk(sm[0], acc);
+    if (four) {
+      st(sm[1], ra1, rb1);
+      __syncthreads();
+      mma_chunk(sm[1], acc);
+    }
     __syncthreads();
+    return;
   }
+  // up to four chunks, one at a time
+  for (int c = 0; c < n; ++c) {
+    ld(c, ra0, rb0);
+    st(sm[c & 1], ra0, rb0);
+    __syncthreads();
+    mma_chunk(sm[c & 1], acc);
+  }
+  __syncthreads();
 }
 
 // Row of accumulator element v of block qa, and column of block qb, of this

@@ -17,8 +17,10 @@
 // MFMA s, so each lane reads its 32 k-values as eight 16-byte LDS reads.
 #include <vector>
 
+#include "bufio.hpp"
 #include "common.hpp"
 #include "philox.hpp"
+#include "rowsum.hpp"
 
 namespace sd {
 namespace {
@@ -39,27 +41,38 @@ struct TileLds {
 // Load rows r0..r0+63, columns k0..k0+63 (< kend) of a row-major matrix into
 // four float4 registers per thread: thread t covers rows t/16 + 16 h (h < 4)
 // and columns k0 + 4 (t % 16) .. + 3; out-of-range elements read as zero.
-__device__ __forceinline__ void load_chunk(const float* __restrict__ A, int64_t ld, int nrows,
-                                           int r0, int k0, int kend, bool vec, float4 (&reg)[4]) {
+// VEC: the k range is a whole number of chunks and rows are 16-byte aligned,
+// so each piece is one unconditional buffer load from the tile's view (rows
+// past the matrix read zero); otherwise element by element.
+template <bool VEC>
+__device__ __forceinline__ void load_chunk(const float* __restrict__ A, __amdgpu_buffer_rsrc_t view,
+                                           int64_t ld, int nrows, int r0, int k0, int kend,
+                                           float4 (&reg)[4]) {
   const int t = threadIdx.x;
   const int kc = k0 + 4 * (t & 15);
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
-    const int r = r0 + (t >> 4) + 16 * h;
-    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    if (r < nrows) {
-      const float* p = A + (int64_t)r * ld + kc;
-      if (vec && kc + 3 < kend) {
-        v = *reinterpret_cast<const float4*>(p);
-      } else {
+    const int rr = (t >> 4) + 16 * h;
+    if constexpr (VEC) {
+      reg[h] = buf_ld4(view, (uint32_t)((rr * (int)ld + kc) * 4));
+    } else {
+      const int r = r0 + rr;
+      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (r < nrows) {
+        const float* p = A + (int64_t)r * ld + kc;
         if (kc < kend) v.x = p[0];
         if (kc + 1 < kend) v.y = p[1];
         if (kc + 2 < kend) v.z = p[2];
         if (kc + 3 < kend) v.w = p[3];
       }
+      reg[h] = v;
     }
-    reg[h] = v;
   }
+}
+
+// The view of the (at most 64) rows of a tile.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile_rows(const float* A, int64_t ld, int nrows, int r0) {
+  return buf_view(A + (int64_t)r0 * ld, (int64_t)max(0, min(nrows - r0, TILE)) * ld * 4);
 }
 
 __device__ __forceinline__ void store_chunk(float* lds, const float4 (&reg)[4]) {
@@ -94,19 +107,23 @@ __device__ __forceinline__ void mma_chunk(const TileLds& sm, int wr, int wc, f32
   }
 }
 
-// Accumulate the 64x64 tile (r0, c0) of A[nra][K] * B[nrb][K]^T over k in [kbeg, kend).
+// Accumulate the 64x64 tile (r0, c0) of A[nra][K] * B[nrb][K]^T over k in [kbeg, kend),
+// starting from the first chunk already loaded into ra, rb (so that a caller
+// can issue other loads after the first chunk's: the hardware counts loads in
+// order, and the first wait then does not include them).
 // With SQ it also accumulates the float64 squares of the four A rows this thread loads.
-template <bool SQ>
-__device__ __forceinline__ void nt_tile(TileLds& sm, const float* __restrict__ A, int64_t lda,
-                                        int nra, bool veca, const float* __restrict__ Bm,
-                                        int64_t ldb, int nrb, bool vecb, int r0, int c0,
-                                        int kbeg, int kend, f32x16& acc, double (&sq)[4]) {
+template <bool SQ, bool VEC>
+__device__ __forceinline__ void nt_tile_run(TileLds& sm, const float* __restrict__ A,
+                                            __amdgpu_buffer_rsrc_t va, int64_t lda, int nra,
+                                            const float* __restrict__ Bm,
+                                            __amdgpu_buffer_rsrc_t vb, int64_t ldb, int nrb,
+                                            int r0, int c0, int kbeg, int kend, float4 (&ra)[4],
+                                            float4 (&rb)[4], f32x16& acc, double (&sq)[4]) {
   const int w = threadIdx.x >> 6;
   const int wr = w >> 1, wc = w & 1;
-  float4 ra[4], rb[4];
-  load_chunk(A, lda, nra, r0, kbeg, kend, veca, ra);
-  load_chunk(Bm, ldb, nrb, c0, kbeg, kend, vecb, rb);
-  for (int k0 = kbeg; k0 < kend; k0 += KC) {
+  // one chunk: stage it, fetch the next, multiply.  The first chunk is peeled
+  // off the loop so that its wait counts only the loads issued before it.
+  auto step = [&](int k0) {
     __syncthreads();
     store_chunk(sm.a, ra);
     store_chunk(sm.b, rb);
@@ -118,11 +135,34 @@ __device__ __forceinline__ void nt_tile(TileLds& sm, const float* __restrict__ A
     }
     __syncthreads();
     if (k0 + KC < kend) {
-      load_chunk(A, lda, nra, r0, k0 + KC, kend, veca, ra);
-      load_chunk(Bm, ldb, nrb, c0, k0 + KC, kend, vecb, rb);
+      load_chunk<VEC>(A, va, lda, nra, r0, k0 + KC, kend, ra);
+      load_chunk<VEC>(Bm, vb, ldb, nrb, c0, k0 + KC, kend, rb);
     }
     mma_chunk(sm, wr, wc, acc);
+  };
+  if (kbeg < kend) step(kbeg);
+  for (int k0 = kbeg + KC; k0 < kend; k0 += KC) step(k0);
+}
+
+__device__ __forceinline__ float4 ld4(const float* p, int cnt, bool vec) {
+  if (vec && cnt >= 4) return *reinterpret_cast<const float4*>(p);
+  return make_float4(cnt > 0 ? p[0] : 0.f, cnt > 1 ? p[1] : 0.f, cnt > 2 ? p[2] : 0.f,
+                     cnt > 3 ? p[3] : 0.f);
+}
+
+__device__ __forceinline__ void st4(float* p, int cnt, bool vec, float4 v) {
+  if (vec && cnt >= 4) {
+    *reinterpret_cast<float4*>(p) = v;
+  } else {
+    if (cnt > 0) p[0] = v.x;
+    if (cnt > 1) p[1] = v.y;
+    if (cnt > 2) p[2] = v.z;
+    if (cnt > 3) p[3] = v.w;
   }
+}
+
+__device__ __forceinline__ float comp(const float4& v, int c) {
+  return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w;
 }
 
 // Output element v of this lane's 32x32 sub-tile: row and column inside the 64x64 tile.
@@ -135,9 +175,10 @@ __device__ __forceinline__ int out_col() {
   return (w & 1) * 32 + (lane & 31);
 }
 
+template <bool VEC>
 __global__ __launch_bounds__(kThreads) void gmm_logits_kernel(
-    int R, int M, int d, const float* __restrict__ X, int64_t ldx, bool vecx,
-    const float* __restrict__ mu, bool vecmu, int ksplit, float* __restrict__ part,
+    int R, int M, int d, const float* __restrict__ X, int64_t ldx,
+    const float* __restrict__ mu, int ksplit, float* __restrict__ part,
     double* __restrict__ xsq, const int* gate) {
   if (gate && *gate == 0) return;
   __shared__ TileLds sm;
@@ -153,10 +194,14 @@ __global__ __launch_bounds__(kThreads) void gmm_logits_kernel(
   for (int v = 0; v < 16; ++v) acc[v] = 0.f;
   double sq[4] = {0.0, 0.0, 0.0, 0.0};
   const bool want_sq = ct == 0;
+  const __amdgpu_buffer_rsrc_t va = tile_rows(X, ldx, R, r0), vb = tile_rows(mu, d, M, c0);
+  float4 ra[4], rb[4];
+  load_chunk<VEC>(X, va, ldx, R, r0, kbeg, kend, ra);
+  load_chunk<VEC>(mu, vb, d, M, c0, kbeg, kend, rb);
   if (want_sq)
-    nt_tile<true>(sm, X, ldx, R, vecx, mu, d, M, vecmu, r0, c0, kbeg, kend, acc, sq);
+    nt_tile_run<true, VEC>(sm, X, va, ldx, R, mu, vb, d, M, r0, c0, kbeg, kend, ra, rb, acc, sq);
   else
-    nt_tile<false>(sm, X, ldx, R, vecx, mu, d, M, vecmu, r0, c0, kbeg, kend, acc, sq);
+    nt_tile_run<false, VEC>(sm, X, va, ldx, R, mu, vb, d, M, r0, c0, kbeg, kend, ra, rb, acc, sq);
   float* ps = part + (int64_t)s * R * M;
   const int col = c0 + out_col();
 #pragma unroll
@@ -202,18 +247,29 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_kernel(
   double xs = 0.0;
   for (int s = 0; s < S; ++s) xs += xsq[(int64_t)s * R + row];
   const double hd = 0.5 * (double)d;
+  // the split partials of x.mu_m, split by split so that the loads of one
+  // split (one per component of this lane) are in flight together
   double lg[kMaxPer];
+#pragma unroll
+  for (int i = 0; i < kMaxPer; ++i) lg[i] = 0.0;
+  for (int s = 0; s < S; ++s) {
+    const float* ps = part + ((int64_t)s * R + row) * M;
+#pragma unroll
+    for (int i = 0; i < kMaxPer; ++i) {
+      const int m = lane + 64 * i;
+      if (m < M) lg[i] += (double)ps[m];
+    }
+  }
   double mx = -INFINITY;
 #pragma unroll
   for (int i = 0; i < kMaxPer; ++i) {
     const int m = lane + 64 * i;
-    lg[i] = -INFINITY;
     if (m < M) {
-      double dot = 0.0;
-      for (int s = 0; s < S; ++s) dot += (double)part[((int64_t)s * R + row) * M + m];
       const double2 t = lsn[m];
-      lg[i] = logw[m] - hd * t.x - 0.5 * (xs - 2.0 * a * dot + a2 * musq[m]) * t.y;
+      lg[i] = logw[m] - hd * t.x - 0.5 * (xs - 2.0 * a * lg[i] + a2 * musq[m]) * t.y;
       mx = fmax(mx, lg[i]);
+    } else {
+      lg[i] = -INFINITY;
     }
   }
 #pragma unroll
@@ -253,8 +309,9 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_kernel(
   }
 }
 
+template <bool VEC>
 __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
-    int R, int M, int d, const float* __restrict__ P, bool vecp, const float* __restrict__ muT,
+    int R, int M, int d, const float* __restrict__ P, const float* __restrict__ muT,
     const float* __restrict__ X, int64_t ldx, const float* __restrict__ rowc,
     float* __restrict__ mq, int64_t ldq, float* __restrict__ score, int64_t lds,
     const int* gate) {
@@ -265,8 +322,12 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
   const int col = c0 + out_col();
   for (int e = threadIdx.x; e < 3 * TILE; e += kThreads)
     rc[e] = r0 + e / 3 < R ? rowc[3 * (int64_t)r0 + e] : 0.f;
-  // the epilogue's inputs are fetched before the contraction so that their
-  // latency overlaps it
+  // the contraction's first operand chunk, then the epilogue's inputs, whose
+  // latency then overlaps the contraction
+  const __amdgpu_buffer_rsrc_t va = tile_rows(P, M, R, r0), vb = tile_rows(muT, M, d, c0);
+  float4 ra[4], rb[4];
+  load_chunk<VEC>(P, va, M, R, r0, 0, M, ra);
+  load_chunk<VEC>(muT, vb, M, d, c0, 0, M, rb);
   float xv[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -277,7 +338,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[v] = 0.f;
   double unused[4];
-  nt_tile<false>(sm, P, M, R, vecp, muT, M, d, vecp, r0, c0, 0, M, acc, unused);
+  nt_tile_run<false, VEC>(sm, P, va, M, R, muT, vb, M, d, r0, c0, 0, M, ra, rb, acc, unused);
   if (col >= d) return;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -300,14 +361,22 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
 //   sum (m^p - m^q)^2   and   sum (yhat_{j+1} - m^p)(m^p - m^q),
 // i.e. ||Delta_{j+1}||^2 sigma^2 and Z.Delta sigma^2 (App. A.2), and
 // sum (m^p - m^q) G with the residual's G (Alg. 5), into
-// lrp[row][column tile][3]; the scan sums the tiles in a fixed order.  The
-// contraction's output is staged in LDS so that the epilogue runs
-// row-contiguous (four threads per row, sixteen columns each).
+// lrp[row][column tile][3]; the scan sums the tiles in a fixed order.
+// Epilogue layout: the contraction's output is staged in LDS and thread t
+// owns columns 4 (t % 16) .. + 3 of tile rows t / 16 + 16 i (i < 4), so a
+// wavefront's access to one i is four rows x 256 contiguous bytes; the
+// per-row sums are reduced over the 16 lanes of a row (rowsum.hpp).
+// VEC: M a whole number of chunks, d a whole number of tiles, rows 16-byte
+// aligned; every epilogue access is then an unconditional buffer access
+// through a view of the tile's rows (x: 65 rows, the last for the next draft
+// of the tile's last row; m^p: the K rows of the tile's chains; m^q: the
+// tile's rows), so rows past the block read zero and their stores drop.
+template <bool VEC>
 __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
-    int R, int M, int d, int K1, const float* __restrict__ P, bool vecp,
-    const float* __restrict__ muT, const float* __restrict__ X, const float* __restrict__ rowc,
-    const float* __restrict__ MP, float* __restrict__ mq, double* __restrict__ lrp, bool vecd,
-    const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
+    int R, int M, int d, int K1, const float* __restrict__ P, const float* __restrict__ muT,
+    const float* __restrict__ X, const float* __restrict__ rowc, const float* __restrict__ MP,
+    float* __restrict__ mq, double* __restrict__ lrp, const uint32_t* __restrict__ rnd,
+    uint64_t seed, const int* gate) {
   if (gate && *gate == 0) return;
   __shared__ TileLds sm;
   __shared__ float rc[3 * TILE];
@@ -317,121 +386,121 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
   const int lin = xcd_tile(nct * gridDim.y);
   const int ct = lin % nct, rt = lin / nct;
   const int r0 = rt * TILE, c0 = ct * TILE;
-  // Every global load of the epilogue is issued first, together with the
-  // first operand chunk, so that one memory latency covers them all: thread t
-  // owns row r0 + t/4 and columns c0 + 16 (t % 4) .. + 15 in the epilogue.
-  const int lr = threadIdx.x >> 2, cb = 16 * (threadIdx.x & 3);
-  const int row = r0 + lr;
-  const int b = row / K1, j = row - b * K1;
-  const bool has_row = row < R;
-  const bool has_draft = has_row && j < K1 - 1;
-  float xv[16], yv[16], pv[16];
+  const int K = K1 - 1, B = R / K1;
+  const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;
+  const int col = c0 + 4 * cg;
+  const int cnt = max(0, min(4, d - col));
+  const int b_first = r0 / K1;
+  const int nchain = min((min(r0 + TILE, R) - 1) / K1 - b_first + 1, TILE);
+  // the contraction's first operand chunk, then every global load of the
+  // epilogue, whose latency then overlaps the contraction
+  const __amdgpu_buffer_rsrc_t va = tile_rows(P, M, R, r0), vb = tile_rows(muT, M, d, c0);
+  float4 ra[4], rb[4];
+  load_chunk<VEC>(P, va, M, R, r0, 0, M, ra);
+  load_chunk<VEC>(muT, vb, M, d, c0, 0, M, rb);
+  // small per-row and per-chain inputs next (the epilogue's coefficients and
+  // the rounds of the residual's G), so that their waits exclude the bulk
+  // (unconditional loads from clamped indices, unused where out of range)
+  const float rcv = rowc[min(3 * (int64_t)r0 + threadIdx.x, 3 * (int64_t)R - 1)];
+  constexpr int kGItems = 3;  // ceil(16 x chains / 256): at most 33 chains meet a tile
+  uint32_t rn[kGItems];
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int col = c0 + cb + 4 * q;
-    const int cnt = col < d ? min(4, d - col) : 0;
-    const bool vec = vecd && cnt == 4;
-    const float* px = X + (int64_t)row * d + col;
-    const float* pp = MP + ((int64_t)b * (K1 - 1) + j) * d + col;
+  for (int u = 0; u < kGItems; ++u)
+    rn[u] = rnd[min(b_first + (int)((threadIdx.x + kThreads * u) >> 4), B - 1)];
+  // keep that issue order: the scheduler must not hoist the bulk loads above
+  __builtin_amdgcn_sched_barrier(0);
+  __amdgpu_buffer_rsrc_t vx, vp, vq;
+  if constexpr (VEC) {
+    vx = buf_view(X + (int64_t)r0 * d, (int64_t)min(R - r0, TILE + 1) * d * 4);
+    vp = buf_view(MP + (int64_t)b_first * K * d, (int64_t)min(B - b_first, nchain) * K * d * 4);
+    vq = buf_view(mq + (int64_t)r0 * d, (int64_t)min(R - r0, TILE) * d * 4);
+  }
+  float4 xv[4], yv[4], pv[4];
 #pragma unroll
-    for (int c = 0; c < 4; ++c) {
-      xv[4 * q + c] = 0.f;
-      yv[4 * q + c] = 0.f;
-      pv[4 * q + c] = 0.f;
-    }
-    if (has_row && cnt > 0) {
-      if (vec) {
-        const float4 a = *reinterpret_cast<const float4*>(px);
-        xv[4 * q] = a.x; xv[4 * q + 1] = a.y; xv[4 * q + 2] = a.z; xv[4 * q + 3] = a.w;
-      } else {
-        for (int c = 0; c < cnt; ++c) xv[4 * q + c] = px[c];
-      }
-    }
-    if (has_draft && cnt > 0) {
-      if (vec) {
-        const float4 a = *reinterpret_cast<const float4*>(px + d);
-        yv[4 * q] = a.x; yv[4 * q + 1] = a.y; yv[4 * q + 2] = a.z; yv[4 * q + 3] = a.w;
-        const float4 m = *reinterpret_cast<const float4*>(pp);
-        pv[4 * q] = m.x; pv[4 * q + 1] = m.y; pv[4 * q + 2] = m.z; pv[4 * q + 3] = m.w;
-      } else {
-        for (int c = 0; c < cnt; ++c) {
-          yv[4 * q + c] = px[d + c];
-          pv[4 * q + c] = pp[c];
-        }
-      }
+  for (int i = 0; i < 4; ++i) {
+    const int lr = rg + 16 * i, row = r0 + lr;
+    const int b = row / K1, j = row - b * K1;
+    if constexpr (VEC) {
+      // rows past the block and the next-draft / m^p reads of a chain's last
+      // row land past a view or are not used
+      xv[i] = buf_ld4(vx, (uint32_t)((lr * d + col) * 4));
+      yv[i] = buf_ld4(vx, (uint32_t)(((lr + 1) * d + col) * 4));
+      pv[i] = buf_ld4(vp, (uint32_t)((((b - b_first) * K + j) * d + col) * 4));
+    } else {
+      const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
+      const float* px = X + (int64_t)row * d + col;
+      xv[i] = row < R && cnt > 0 ? ld4(px, cnt, false) : z4;
+      const bool dr = row < R && cnt > 0 && j < K1 - 1;
+      yv[i] = dr ? ld4(px + d, cnt, false) : z4;
+      pv[i] = dr ? ld4(MP + ((int64_t)b * K + j) * d + col, cnt, false) : z4;
     }
   }
-  for (int e = threadIdx.x; e < 3 * TILE; e += kThreads)
-    rc[e] = r0 + e / 3 < R ? rowc[3 * (int64_t)r0 + e] : 0.f;
   f32x16 acc;
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[v] = 0.f;
   double unused[4];
-  nt_tile<false>(sm, P, M, R, vecp, muT, M, d, vecp, r0, c0, 0, M, acc, unused);
+  nt_tile_run<false, VEC>(sm, P, va, M, R, muT, vb, M, d, r0, c0, 0, M, ra, rb, acc, unused);
   __syncthreads();  // every wavefront is done with the operand tiles
   {
     const int cw = out_col();
 #pragma unroll
     for (int v = 0; v < 16; ++v) sm.a[out_row(v) * LDW + cw] = acc[v];
   }
+  if (threadIdx.x < 3 * TILE) rc[threadIdx.x] = r0 + (int)threadIdx.x / 3 < R ? rcv : 0.f;
   // G of the residual (RESID stream of each chain's current round) depends
-  // only on the chain and the coordinate: draw it once per chain of the tile
-  // into sm.b (at most 64 chains x 64 coordinates).
-  const int b_first = r0 / K1;
-  const int nchain = min((min(r0 + TILE, R) - 1) / K1 - b_first + 1, TILE);
-  for (int e = threadIdx.x; e < nchain * 16; e += kThreads) {
-    const int cl = e >> 4, gq = e & 15;
-    const int bb = b_first + cl;
-    const float4 z = normals4(philox((uint32_t)((c0 >> 2) + gq), (uint32_t)bb, rnd[bb],
-                                     TAG_RESID << 24, seed));
-    *reinterpret_cast<float4*>(&sm.b[cl * LDW + 4 * gq]) = z;
+  // only on the chain and the coordinate: drawn once per chain of the tile
+  // into sm.b (item e: chain e / 16, coordinates 4 (e % 16) ..)
+#pragma unroll
+  for (int u = 0; u < kGItems; ++u) {
+    const int e = threadIdx.x + kThreads * u;
+    if (e < nchain * 16)
+      *reinterpret_cast<float4*>(&sm.b[(e >> 4) * LDW + 4 * (e & 15)]) =
+          normals4(philox((uint32_t)((c0 >> 2) + (e & 15)), (uint32_t)(b_first + (e >> 4)), rn[u],
+                          TAG_RESID << 24, seed));
   }
   __syncthreads();
-  double s2 = 0.0, sz = 0.0, sgd = 0.0;
-  if (has_row) {
+  double s2[4], sz[4], sgd[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    s2[i] = sz[i] = sgd[i] = 0.0;
+    const int lr = rg + 16 * i, row = r0 + lr;
+    const int b = row / K1, j = row - b * K1;
     const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
-    const float* gz = &sm.b[(b - b_first) * LDW];
+    const float4 ov = *reinterpret_cast<const float4*>(&sm.a[lr * LDW + 4 * cg]);
+    const float4 x = xv[i];
+    const float4 qv = make_float4(c1 * x.x + c2 * (ov.x - rho * x.x),
+                                  c1 * x.y + c2 * (ov.y - rho * x.y),
+                                  c1 * x.z + c2 * (ov.z - rho * x.z),
+                                  c1 * x.w + c2 * (ov.w - rho * x.w));
+    if constexpr (VEC) {
+      buf_st4(vq, (uint32_t)((lr * d + col) * 4), qv);
+    } else {
+      if (row >= R || cnt == 0) continue;
+      st4(mq + (int64_t)row * d + col, cnt, false, qv);
+    }
+    if (row < R && j < K1 - 1) {
+      const float4 gv = *reinterpret_cast<const float4*>(&sm.b[(b - b_first) * LDW + 4 * cg]);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int cl = cb + 4 * q, col = c0 + cl;
-      const int cnt = col < d ? min(4, d - col) : 0;
-      float qv[4];
-#pragma unroll
-      for (int c = 0; c < 4; ++c) {
-        const float x = xv[4 * q + c];
-        qv[c] = c1 * x + c2 * (sm.a[lr * LDW + cl + c] - rho * x);
-      }
-      float* pq = mq + (int64_t)row * d + col;
-      if (vecd && cnt == 4) {
-        *reinterpret_cast<float4*>(pq) = make_float4(qv[0], qv[1], qv[2], qv[3]);
-      } else {
-        for (int c = 0; c < cnt; ++c) pq[c] = qv[c];
-      }
-      if (has_draft) {
-#pragma unroll
-        for (int c = 0; c < 4; ++c) {
-          if (c < cnt) {
-            const double dd = (double)pv[4 * q + c] - (double)qv[c];
-            const double zz = (double)yv[4 * q + c] - (double)pv[4 * q + c];
-            s2 = fma(dd, dd, s2);
-            sz = fma(zz, dd, sz);
-            sgd = fma((double)gz[cl + c], dd, sgd);
-          }
+      for (int e = 0; e < 4; ++e) {
+        if (e < cnt) {
+          const double dd = (double)comp(pv[i], e) - (double)comp(qv, e);
+          const double zz = (double)comp(yv[i], e) - (double)comp(pv[i], e);
+          s2[i] = fma(dd, dd, s2[i]);
+          sz[i] = fma(zz, dd, sz[i]);
+          sgd[i] = fma((double)comp(gv, e), dd, sgd[i]);
         }
       }
     }
   }
-  s2 += __shfl_xor(s2, 1);
-  s2 += __shfl_xor(s2, 2);
-  sz += __shfl_xor(sz, 1);
-  sz += __shfl_xor(sz, 2);
-  sgd += __shfl_xor(sgd, 1);
-  sgd += __shfl_xor(sgd, 2);
-  if ((threadIdx.x & 3) == 0 && has_row) {
+  // every lane of the group takes part (rows past R and empty columns add zeros)
+  const double t2 = reduce_rows16<4>(s2, cg), tz = reduce_rows16<4>(sz, cg),
+               tg = reduce_rows16<4>(sgd, cg);
+  const int row = r0 + rg + 16 * row_of<4>(cg);
+  if ((cg & 3) == 0 && row < R) {
     double* o = lrp + ((int64_t)row * nct + ct) * 3;
-    o[0] = s2;
-    o[1] = sz;
-    o[2] = sgd;
+    o[0] = t2;
+    o[1] = tz;
+    o[2] = tg;
   }
 }
 
@@ -475,6 +544,24 @@ Plan make_plan(const Target& t, int R) {
   return p;
 }
 
+// The logits GEMM (buffer path when d is a whole number of chunks, rows are
+// aligned and a tile's rows fit 32-bit offsets).
+hipError_t logits_launch(const Target& t, const Plan& p, int R, const float* x, int64_t ldx,
+                         float* part, double* xsq, hipStream_t s, const int* gate) {
+  dim3 g1(p.S, (R + TILE - 1) / TILE, (t.M + TILE - 1) / TILE);
+  const bool vec = t.d % KC == 0 && ldx % 4 == 0 && aligned16(x) &&
+                   (int64_t)TILE * ldx * 4 < ((int64_t)1 << 31) &&
+                   (int64_t)TILE * t.d * 4 < ((int64_t)1 << 31);
+  return timed("gmm_logits", s, [&] {
+    if (vec)
+      gmm_logits_kernel<true><<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu, p.ksplit, part,
+                                                       xsq, gate);
+    else
+      gmm_logits_kernel<false><<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu, p.ksplit, part,
+                                                        xsq, gate);
+  });
+}
+
 }  // namespace
 
 size_t target_ws_bytes(const Target& t, int rows) {
@@ -509,21 +596,19 @@ hipError_t target_mean_launch(const Target& t, int R, const float* x, int64_t ld
   double* xsq = reinterpret_cast<double*>(base + p.off_xsq);
   float* P = reinterpret_cast<float*>(base + p.off_p);
   float* rowc = reinterpret_cast<float*>(base + p.off_rowc);
-  const bool vecx = (ldx % 4 == 0) && aligned16(x);
-  const bool vecmu = (t.d % 4 == 0);
-  const bool vecp = (t.M % 4 == 0);
-  dim3 g1(p.S, (R + TILE - 1) / TILE, (t.M + TILE - 1) / TILE);
-  hipError_t e = timed("gmm_logits", s, [&] {
-    gmm_logits_kernel<<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, vecx, t.mu, vecmu, p.ksplit,
-                                              part, xsq, gate);
-  });
+  hipError_t e = logits_launch(t, p, R, x, ldx, part, xsq, s, gate);
   if (e != hipSuccess) return e;
   e = gmm_softmax_launch(t, R, p.S, part, xsq, step, P, false, rowc, s, gate);
   if (e != hipSuccess) return e;
   dim3 g2((R + TILE - 1) / TILE, (t.d + TILE - 1) / TILE);
+  const bool vec = t.M % KC == 0 && t.M < 1 << 22;
   return timed("gmm_mean", s, [&] {
-    gmm_mean_kernel<<<g2, kThreads, 0, s>>>(R, t.M, t.d, P, vecp, t.muT, x, ldx, rowc, mq, ldq,
-                                            score, lds, gate);
+    if (vec)
+      gmm_mean_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, P, t.muT, x, ldx, rowc, mq, ldq,
+                                                    score, lds, gate);
+    else
+      gmm_mean_kernel<false><<<g2, kThreads, 0, s>>>(R, t.M, t.d, P, t.muT, x, ldx, rowc, mq, ldq,
+                                                     score, lds, gate);
   });
 }
 
@@ -539,20 +624,23 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
   double* xsq = reinterpret_cast<double*>(base + p.off_xsq);
   float* P = reinterpret_cast<float*>(base + p.off_p);
   float* rowc = reinterpret_cast<float*>(base + p.off_rowc);
-  const bool vecd = (t.d % 4 == 0) && aligned16(x) && aligned16(mq) && aligned16(mp);
-  const bool vecp = (t.M % 4 == 0);
-  dim3 g1(p.S, (R + TILE - 1) / TILE, (t.M + TILE - 1) / TILE);
-  hipError_t e = timed("gmm_logits", s, [&] {
-    gmm_logits_kernel<<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, t.d, vecd, t.mu, t.d % 4 == 0,
-                                              p.ksplit, part, xsq, gate);
-  });
+  hipError_t e = logits_launch(t, p, R, x, t.d, part, xsq, s, gate);
   if (e != hipSuccess) return e;
   e = gmm_softmax_launch(t, R, p.S, part, xsq, step, P, false, rowc, s, gate);
   if (e != hipSuccess) return e;
   dim3 g2((t.d + TILE - 1) / TILE, (R + TILE - 1) / TILE);
+  // the buffer path: whole chunks of M and tiles of d, aligned rows, and
+  // 32-bit offsets inside a tile's views
+  const bool vec = t.M % KC == 0 && t.d % TILE == 0 && aligned16(x) && aligned16(mq) &&
+                   aligned16(mp) && (int64_t)(TILE + 2 * K1 + 1) * t.d * 4 < ((int64_t)1 << 31) &&
+                   t.M < 1 << 22;
   return timed("gmm_mean_lr", s, [&] {
-    gmm_mean_lr_kernel<<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, P, vecp, t.muT, x, rowc, mp, mq,
-                                               lrp, vecd, rnd, seed, gate);
+    if (vec)
+      gmm_mean_lr_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, P, t.muT, x, rowc, mp,
+                                                       mq, lrp, rnd, seed, gate);
+    else
+      gmm_mean_lr_kernel<false><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, P, t.muT, x, rowc, mp,
+                                                        mq, lrp, rnd, seed, gate);
   });
 }
 

@@ -13,6 +13,7 @@
 #include "common.hpp"
 #include "gemm_bf16.hpp"
 #include "philox.hpp"
+#include "rowsum.hpp"
 
 namespace sd {
 namespace {
@@ -136,28 +137,6 @@ __device__ __forceinline__ void st4(float* p, int cnt, bool vec, float4 v) {
 
 __device__ __forceinline__ float comp(const float4& v, int c) {
   return c == 0 ? v.x : c == 1 ? v.y : c == 2 ? v.z : v.w;
-}
-
-// Sum over the 16 lanes of a column group of eight per-row values, as a
-// butterfly reduce-scatter: after the exchanges at distance 8, 4 and 2 a lane
-// holds one row, i = 4 bit3 + 2 bit2 + bit1 of its lane index in the group,
-// summed over eight lanes; the last exchange completes the sum (same value
-// in lanes 2k and 2k + 1).  Fixed order, so the result is deterministic.
-__device__ __forceinline__ double reduce_rows16(const double (&v)[8], int cg) {
-  const bool b3 = cg & 8, b2 = cg & 4, b1 = cg & 2;
-  double w[4], u[2];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const double send = b3 ? v[i] : v[i + 4];
-    w[i] = (b3 ? v[i + 4] : v[i]) + __shfl_xor(send, 8);
-  }
-#pragma unroll
-  for (int i = 0; i < 2; ++i) {
-    const double send = b2 ? w[i] : w[i + 2];
-    u[i] = (b2 ? w[i + 2] : w[i]) + __shfl_xor(send, 4);
-  }
-  const double z = (b1 ? u[1] : u[0]) + __shfl_xor(b1 ? u[0] : u[1], 2);
-  return z + __shfl_xor(z, 1);
 }
 
 // Public target call: m^q = c1 x + c2 (O - rho x) (and the score if asked).
@@ -300,12 +279,11 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
       }
     }
     // every lane of the group takes part (rows past R and empty columns add zeros)
-    t2 += reduce_rows16(s2, cg);
-    tz += reduce_rows16(sz, cg);
-    tg += reduce_rows16(sgd, cg);
+    t2 += reduce_rows16<8>(s2, cg);
+    tz += reduce_rows16<8>(sz, cg);
+    tg += reduce_rows16<8>(sgd, cg);
   }
-  const int mine = 4 * ((cg >> 3) & 1) + 2 * ((cg >> 2) & 1) + ((cg >> 1) & 1);
-  const int row = r0 + rg + 16 * mine;
+  const int row = r0 + rg + 16 * row_of<8>(cg);
   if ((cg & 1) == 0 && row < R) {
     double* o = lrp + ((int64_t)row * nct + ct) * 3;
     o[0] = t2;

@@ -271,17 +271,46 @@ __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
     return;
   }
   const bool valid = lane < kb;
-  double s2 = 0.0, sz = 0.0, sg = 1.0;
-  double sgd = 0.0;
-  if (valid) {
-    const double* pl = lrp + ((int64_t)b * K1 + lane) * nct * 3;
-    for (int ct = 0; ct < nct; ++ct) {
-      s2 += pl[3 * ct];
-      sz += pl[3 * ct + 1];
-      sgd += pl[3 * ct + 2];
+  // Sum the column-tile partials of each draft row: row j is spread over lpr
+  // lanes (64 / K rounded up to a power of two), each lane takes every lpr-th
+  // tile with four independent accumulators (loads in flight together), and
+  // the lanes of a row combine in a fixed xor tree; then lane j fetches row
+  // j's totals.  Fixed order throughout, so the sums are deterministic.
+  int kp = 1;
+  while (kp < K) kp <<= 1;
+  const int lpr = 64 / kp, j = lane / lpr, sub = lane % lpr;
+  double a2[4] = {0.0, 0.0, 0.0, 0.0}, az[4] = {0.0, 0.0, 0.0, 0.0}, ag[4] = {0.0, 0.0, 0.0, 0.0};
+  if (j < kb) {
+    const double* pl = lrp + ((int64_t)b * K1 + j) * nct * 3;
+    int ct = sub;
+    for (; ct + 3 * lpr < nct; ct += 4 * lpr) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const double* q = pl + 3 * (ct + u * lpr);
+        a2[u] += q[0];
+        az[u] += q[1];
+        ag[u] += q[2];
+      }
     }
-    sg = sigma[(int64_t)b * K1 + lane];
+    for (; ct < nct; ct += lpr) {
+      a2[0] += pl[3 * ct];
+      az[0] += pl[3 * ct + 1];
+      ag[0] += pl[3 * ct + 2];
+    }
   }
+  double s2 = (a2[0] + a2[1]) + (a2[2] + a2[3]);
+  double sz = (az[0] + az[1]) + (az[2] + az[3]);
+  double sgd = (ag[0] + ag[1]) + (ag[2] + ag[3]);
+  for (int o = 1; o < lpr; o <<= 1) {
+    s2 += __shfl_xor(s2, o);
+    sz += __shfl_xor(sz, o);
+    sgd += __shfl_xor(sgd, o);
+  }
+  const int src = min(lane * lpr, 63);
+  s2 = __shfl(s2, src);
+  sz = __shfl(sz, src);
+  sgd = __shfl(sgd, src);
+  const double sg = valid ? sigma[(int64_t)b * K1 + lane] : 1.0;
   const double inv = 1.0 / (sg * sg);
   const double vn = valid ? sqrt(s2 * inv) : 0.0;
   const double ell = valid ? -sz * inv - 0.5 * s2 * inv : 0.0;
