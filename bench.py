@@ -56,13 +56,14 @@ def algorithmic_work(name, B, K, d, M, act, rows_verified, runs, nct=1):
     Units per round: the GEMMs are launched on all B (K+1) rows (2 flops per
     multiply-add) and must move their operands and outputs once: the logits
     GEMM reads X and mu and produces the R x M logits, the mean GEMM reads X,
-    m^p and mu and writes m^q; the explicit target call at Y_0 (one per run)
+    each chain's cache row and mu and writes m^q (the draft means are
+    recomputed, not stored); the explicit target call at Y_0 (one per run)
     covers B rows.  The streaming kernels count the float32 bytes their rows
-    move once, for active chains only: advance reads the residual's two rows
-    and the cache's two rows and writes the new state, K+1 drafts and K draft
-    means.  Rounds launched after every chain has finished exit at once and
-    count no work.  Returns None for kernels without a throughput roof
-    (latency-bound scalar work).
+    move once, for active chains only: advance reads the residual's state,
+    mean and cache rows and the new cache's two rows, and writes the new
+    state, K+1 draft rows and the new cache row.  Rounds launched after every
+    chain has finished exit at once and count no work.  Returns None for
+    kernels without a throughput roof (latency-bound scalar work).
     """
     rounds = len(act)
     R = B * (K + 1)
@@ -74,7 +75,7 @@ def algorithmic_work(name, B, K, d, M, act, rows_verified, runs, nct=1):
     if name in ("gmm_mean_lr", "gmm_mean_lr_bf16"):
         rows = R * rounds
         return (2.0 * rows * M * d * runs,
-                (rows * d * 8 + B * K * rounds * d * 4 + rounds * M * d * eb) * runs, eb)
+                (rows * d * 8 + B * rounds * d * 4 + rounds * M * d * eb) * runs, eb)
     if name in ("gmm_mean", "gmm_mean_bf16"):
         return 2.0 * B * M * d * runs, (B * d * 8 + M * d * eb) * runs, eb
     if name == "gmm_softmax":
@@ -82,10 +83,10 @@ def algorithmic_work(name, B, K, d, M, act, rows_verified, runs, nct=1):
         return 0.0, rows * M * (4 + eb) * runs, eb
     if name == "logratio_reduce":
         return 0.0, 3.0 * 4 * d * rows_verified.sum() * runs, 4
-    if name == "draft_block":   # one per run: reads y and the cached (x, m^q) row; K+1 drafts, K means
-        return 0.0, 4.0 * d * (3 + (K + 1) + K) * B * runs, 4
+    if name == "draft_block":   # one per run: reads y and the cached (x, m^q) row; K+1 drafts, the cache row
+        return 0.0, 4.0 * d * (3 + (K + 1) + 1) * B * runs, 4
     if name == "advance":
-        return 0.0, 4.0 * d * (4 + 1 + (K + 1) + K) * act.sum() * runs, 4
+        return 0.0, 4.0 * d * (5 + 1 + (K + 1) + 1) * act.sum() * runs, 4
     return None
 
 

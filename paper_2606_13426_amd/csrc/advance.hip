@@ -10,10 +10,12 @@
 //             is that of row min(tau, K_b) of this round (Sec. 3.3), recovered
 //             from the same round's (x, m^q) rows.
 // Each thread owns four coordinates of one chain: it reads every row it needs
-// (m^p/m^q of the residual row, the cache row, the last draft) before it
-// overwrites that chain's x and m^p rows at the same coordinates, so one pass
-// replaces the separate residual, commit and draft kernels and the state
-// never leaves registers between them.
+// (x and m^q of the residual row, the cache rows, the last draft) before it
+// overwrites that chain's x rows and cache row sv = c2_c S_c at the same
+// coordinates, so one pass replaces the separate residual, commit and draft
+// kernels and the state never leaves registers between them.  The draft means
+// m^p are not stored: where the residual needs one it is recomputed from the
+// draft state and the cache with draft_mean, bit for bit.
 #include "common.hpp"
 #include "philox.hpp"
 #include "rows.hpp"
@@ -30,7 +32,7 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
     int32_t* __restrict__ knext, uint32_t* __restrict__ rnext, int32_t* __restrict__ crow_next,
     int32_t* __restrict__ cstep_next, const int32_t* __restrict__ tauv,
     const int32_t* __restrict__ rmode, const float* __restrict__ rcoef,
-    const float* __restrict__ rsig, float* __restrict__ X, float* __restrict__ MP,
+    const float* __restrict__ rsig, float* __restrict__ X, float* __restrict__ SV,
     const float* __restrict__ MQ, float* __restrict__ y, int32_t* __restrict__ step,
     double* __restrict__ sigma, int32_t* __restrict__ hist, int64_t* __restrict__ steps,
     int* act_next, int32_t* __restrict__ trace, int r_round, int trace_rounds, bool vec_ok,
@@ -76,18 +78,25 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
   const int cnt = min(4, d - e0);
   const bool vec = vec_ok && cnt == 4;
   float* xb = X + (int64_t)b * K1 * d + e0;
-  float* mb = MP + (int64_t)b * K * d + e0;
+  float* sb = SV + (int64_t)b * d + e0;
   const float* qb = MQ + (int64_t)b * K1 * d + e0;
   float yv[4];
   const int rm = rmode[b];
   if (rm == 1) {
-    float pv[4], qv[4];
-    load4(mb + (int64_t)(t - 1) * d, cnt, vec, pv);
+    // m^p of row t - 1 from its draft state and this round's cache
+    float xv[4], qv[4], sv[4];
+    load4(xb + (int64_t)(t - 1) * d, cnt, vec, xv);
     load4(qb + (int64_t)(t - 1) * d, cnt, vec, qv);
+    load4(sb, cnt, vec, sv);
+    const float4 cn = step_coef(sc, coef, k + t - 1);
+    const float c2s = cn.y * step_coef(sc, coef, cstep_cur[b]).w;
     const float sg = rsig[b], cf = rcoef[b];
     const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, TAG_RESID << 24, seed));
 #pragma unroll
-    for (int c = 0; c < 4; ++c) yv[c] = qv[c] + sg * get4(z, c) + cf * (pv[c] - qv[c]);
+    for (int c = 0; c < 4; ++c) {
+      const float pv = draft_mean(cn.x, xv[c], c2s, sv[c]);
+      yv[c] = qv[c] + sg * get4(z, c) + cf * (pv - qv[c]);
+    }
   } else if (rm == 2) {
     float qv[4];
     load4(qb + (int64_t)kb * d, cnt, vec, qv);
@@ -106,9 +115,10 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
   const float4 cc = step_coef(sc, coef, cs);
 #pragma unroll
   for (int c = 0; c < 4; ++c) sv[c] = qcv[c] - cc.x * xcv[c];  // c2_c S_c
+  store4(sb, cnt, vec, sv);
   store4(xb, cnt, vec, yv);
   draft_rows(sc, coef, K, knew, min(K, N - knew), (uint32_t)b, r + 1u, seed, g, yv, sv, cc.w, xb,
-             d, mb, d, cnt, vec);
+             d, nullptr, d, cnt, vec);
 }
 
 }  // namespace
@@ -118,17 +128,17 @@ hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int
                           const int32_t* crow_cur, const int32_t* cstep_cur, int32_t* knext,
                           uint32_t* rnext, int32_t* crow_next, int32_t* cstep_next,
                           const int32_t* tau, const int32_t* rmode, const float* rcoef,
-                          const float* rsig, float* x, float* mp, const float* mq, float* y,
+                          const float* rsig, float* x, float* sv, const float* mq, float* y,
                           int32_t* step, double* sigma, int32_t* hist, int64_t* steps,
                           int* act_next, int32_t* trace, int r, int trace_rounds, hipStream_t s,
                           const int* gate) {
   const int ng = (d + 3) / 4;
   dim3 grid((ng + kThreads - 1) / kThreads, B);
-  const bool vec = (d % 4 == 0) && aligned16(x) && aligned16(mp) && aligned16(mq) && aligned16(y);
+  const bool vec = (d % 4 == 0) && aligned16(x) && aligned16(sv) && aligned16(mq) && aligned16(y);
   return timed("advance", s, [&] {
     advance_kernel<<<grid, kThreads, 0, s>>>(sc, coef, B, K, d, seed, kcur, rcur, crow_cur,
                                              cstep_cur, knext, rnext, crow_next, cstep_next, tau,
-                                             rmode, rcoef, rsig, x, mp, mq, y, step, sigma, hist,
+                                             rmode, rcoef, rsig, x, sv, mq, y, step, sigma, hist,
                                              steps, act_next, trace, r, trace_rounds, vec, gate);
   });
 }

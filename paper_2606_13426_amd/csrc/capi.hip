@@ -345,7 +345,7 @@ sd_status sd_sample_residual(int32_t B, int32_t K, int32_t d, const float* y_dra
 namespace {
 
 struct SamplerLayout {
-  size_t y, x, mp, mq, sigma, step, k2, rnd2, crow2, cstep2, tau, rmode, rcoef, rsig, hist, steps,
+  size_t y, x, sv, mq, sigma, step, k2, rnd2, crow2, cstep2, tau, rmode, rcoef, rsig, hist, steps,
       act, nan, kb, left, dummy_i32, dummy_i64, lrp, tws, total;
   size_t tws_bytes;
   int nct;
@@ -365,7 +365,7 @@ SamplerLayout sampler_layout(const Target& t, int B, int K) {
   L.nct = lr_tiles(t);
   L.y = take(4 * Bs * d);
   L.x = take(4 * Bs * K1 * d);
-  L.mp = take(4 * Bs * K * d);
+  L.sv = take(4 * Bs * d);
   L.mq = take(4 * Bs * K1 * d);
   L.sigma = take(8 * Bs * K1);
   L.step = take(4 * Bs * K1);
@@ -424,7 +424,7 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
   auto F = [&](size_t o) { return reinterpret_cast<float*>(base + o); };
   auto I = [&](size_t o) { return reinterpret_cast<int32_t*>(base + o); };
   const int d = t.d, N = t.sc.N, K1 = K + 1;
-  float *y = F(L.y), *x = F(L.x), *mp = F(L.mp), *mq = F(L.mq), *rcoef = F(L.rcoef),
+  float *y = F(L.y), *x = F(L.x), *sv = F(L.sv), *mq = F(L.mq), *rcoef = F(L.rcoef),
         *rsig = F(L.rsig);
   double* sigma = reinterpret_cast<double*>(base + L.sigma);
   double* lrp = reinterpret_cast<double*>(base + L.lrp);
@@ -435,7 +435,7 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
   int64_t* steps = reinterpret_cast<int64_t*>(base + L.steps);
   int64_t* dummy64 = reinterpret_cast<int64_t*>(base + L.dummy_i64);
   void* tws = base + L.tws;
-  const sd_stride xs{(int64_t)K1 * d, d}, mps{(int64_t)K * d, d}, mqs{(int64_t)K1 * d, d};
+  const sd_stride xs{(int64_t)K1 * d, d}, mqs{(int64_t)K1 * d, d};
 
   // Y_0 (also row 0 of x); the one explicit target call at Y_0, whose mean
   // (row 0 of mq) seeds the Free Drafter's cached score; the round-0 rows'
@@ -458,7 +458,7 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
   SD_HIP(prepare_launch(t.sc, B, K, k2, kb, left, step, sigma, tau, dummy, dummy + B,
                         dummy + B + 1, dummy64, dummy64 + SD_MAX_BLOCK + 2, s));
   SD_HIP(draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2, cstep2, mq, mqs, k2, rnd2, seed, x,
-                             xs, mp, mps, s, nullptr));
+                             xs, sv, s, nullptr));
 
   int32_t* host_act = nullptr;
   constexpr int kLag = 3;
@@ -477,16 +477,16 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
   for (; r < max_rounds && rounds < 0; ++r) {
     const int cur = r & 1, nxt = cur ^ 1;
     const int* gate = act + cur;
-    hipError_t e = target_mean_lr_launch(t, B * K1, K1, x, step, mq, mp, lrp, rnd2 + cur * B, seed,
-                                         tws, s, gate);
+    hipError_t e = target_mean_lr_launch(t, B * K1, K1, x, step, mq, sv, cstep2 + cur * B, lrp,
+                                         rnd2 + cur * B, seed, tws, s, gate);
     if (e == hipSuccess)
       e = scan_fused_launch(B, K, d, N, (int)mode, (int)usample_mode, lrp, L.nct, sigma,
-                            k2 + cur * B, rnd2 + cur * B, seed, mp, mq, tau, rmode, rcoef, rsig,
+                            k2 + cur * B, rnd2 + cur * B, seed, tau, rmode, rcoef, rsig,
                             nanflag, act + nxt, s, gate);
     if (e == hipSuccess)
       e = advance_launch(t.sc, t.coef, B, K, d, seed, k2 + cur * B, rnd2 + cur * B,
                          crow2 + cur * B, cstep2 + cur * B, k2 + nxt * B, rnd2 + nxt * B,
-                         crow2 + nxt * B, cstep2 + nxt * B, tau, rmode, rcoef, rsig, x, mp, mq, y,
+                         crow2 + nxt * B, cstep2 + nxt * B, tau, rmode, rcoef, rsig, x, sv, mq, y,
                          step, sigma, hist, steps, act + nxt, tau_trace, r,
                          tau_trace ? trace_rounds : 0, s, gate);
     const int slot = r % (kLag + 1);

@@ -88,20 +88,22 @@ hipError_t target_mean_launch(const Target& t, int rows, const float* x, int64_t
 
 // The sampler's target call on its [B][K+1][d] block (x rows contiguous,
 // row stride d) that also leaves the verification's partial sums in
-// lrp[row][lr_tiles(t)][3] (see gmm_mean_lr_kernel); rnd = chains' rounds.
+// lrp[row][lr_tiles(t)][3] (see gmm_mean_lr_kernel); the draft means are
+// recomputed from x, the cache rows sv [B][d] and the cache steps cstep [B];
+// rnd = chains' rounds.
 hipError_t target_mean_lr_launch(const Target& t, int rows, int K1, const float* x,
-                                 const int32_t* step, float* mq, const float* mp, double* lrp,
-                                 const uint32_t* rnd, uint64_t seed, void* ws, hipStream_t s,
-                                 const int* gate);
+                                 const int32_t* step, float* mq, const float* sv,
+                                 const int32_t* cstep, double* lrp, const uint32_t* rnd,
+                                 uint64_t seed, void* ws, hipStream_t s, const int* gate);
 int lr_tiles(const Target& t);
 // bf16 versions of the three calls above (dispatched to by them).
 hipError_t target_mean_bf16_launch(const Target& t, int rows, const float* x, int64_t ldx,
                                    const int32_t* step, float* mq, int64_t ldq, float* score,
                                    int64_t lds, void* ws, hipStream_t s, const int* gate);
 hipError_t target_mean_lr_bf16_launch(const Target& t, int rows, int K1, const float* x,
-                                      const int32_t* step, float* mq, const float* mp,
-                                      double* lrp, const uint32_t* rnd, uint64_t seed, void* ws,
-                                      hipStream_t s, const int* gate);
+                                      const int32_t* step, float* mq, const float* sv,
+                                      const int32_t* cstep, double* lrp, const uint32_t* rnd,
+                                      uint64_t seed, void* ws, hipStream_t s, const int* gate);
 int lr_tiles_bf16(const Target& t);
 // Softmax over the split logits partials part[S][rows][M] (+ xsq[S][rows]):
 // P[rows][M] = r a / s2 (float32, or bf16 when p_bf16) and rowc[rows][3] =
@@ -112,10 +114,9 @@ hipError_t gmm_softmax_launch(const Target& t, int rows, int S, const float* par
 // Sampler verification on the fused partials (see scan_fused_kernel).
 hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, const double* lrp,
                              int nct, const double* sigma, const int32_t* kcur,
-                             const uint32_t* rcur, uint64_t seed, const float* mp,
-                             const float* mq, int32_t* tau, int32_t* rmode, float* rcoef,
-                             float* rsig, int* nanflag, int* act_next, hipStream_t s,
-                             const int* gate);
+                             const uint32_t* rcur, uint64_t seed, int32_t* tau, int32_t* rmode,
+                             float* rcoef, float* rsig, int* nanflag, int* act_next,
+                             hipStream_t s, const int* gate);
 // Residual, commit and the next round's Free-Drafter block, elementwise over
 // (chain, four coordinates); per-chain state is read from the *cur arrays and
 // written to the *next arrays (round parity), so no workgroup races another.
@@ -124,7 +125,7 @@ hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int
                           const int32_t* crow_cur, const int32_t* cstep_cur, int32_t* knext,
                           uint32_t* rnext, int32_t* crow_next, int32_t* cstep_next,
                           const int32_t* tau, const int32_t* rmode, const float* rcoef,
-                          const float* rsig, float* x, float* mp, const float* mq, float* y,
+                          const float* rsig, float* x, float* sv, const float* mq, float* y,
                           int32_t* step, double* sigma, int32_t* hist, int64_t* steps,
                           int* act_next, int32_t* trace, int r, int trace_rounds, hipStream_t s,
                           const int* gate);
@@ -136,12 +137,13 @@ hipError_t draft_launch(const Sched& sc, int B, int K, int d, const float* y, co
                         const int32_t* k, const uint32_t* rnd, uint64_t seed, float* x,
                         sd_stride xs, float* mp, sd_stride mps, hipStream_t s, const int* gate);
 // Draft whose cached score is recovered from row crow[b] of the previous
-// round's x / target means at step cstep[b] (the sampler's Free Drafter).
+// round's x / target means at step cstep[b] (the sampler's Free Drafter):
+// writes the draft rows and the cache row sv[b] = c2_c S_c ([B][d]), no means.
 hipError_t draft_cached_launch(const Sched& sc, const float4* coef, int B, int K, int d,
                                const float* y,
                                const int32_t* crow, const int32_t* cstep, const float* mqprev,
                                sd_stride mqs, const int32_t* k, const uint32_t* rnd,
-                               uint64_t seed, float* x, sd_stride xs, float* mp, sd_stride mps,
+                               uint64_t seed, float* x, sd_stride xs, float* sv,
                                hipStream_t s, const int* gate);
 hipError_t verify_launch(int B, int K, int d, int mode, const float* yd, sd_stride ys,
                          const float* mp, sd_stride mps, const float* mq, sd_stride mqs,

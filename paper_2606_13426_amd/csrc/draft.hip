@@ -43,7 +43,8 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(
     const int32_t* __restrict__ crow, const int32_t* __restrict__ cstep,
     const float* __restrict__ mqprev, int64_t qc, int64_t qr, const int32_t* __restrict__ kk,
     const uint32_t* __restrict__ rnd, uint64_t seed, float* __restrict__ x, int64_t xc,
-    int64_t xr, float* __restrict__ mp, int64_t mc, int64_t mr, bool vec_ok, const int* gate) {
+    int64_t xr, float* __restrict__ mp, int64_t mc, int64_t mr, float* __restrict__ svout,
+    bool vec_ok, const int* gate) {
   if (gate && *gate == 0) return;
   const int b = blockIdx.y;
   const int g = blockIdx.x * kThreads + threadIdx.x;
@@ -57,7 +58,7 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(
   const bool vec = vec_ok && cnt == 4;
   float yv[4], sv[4];
   float* xb = x + (int64_t)b * xc + e0;
-  float* mb = mp + (int64_t)b * mc + e0;
+  float* mb = mp ? mp + (int64_t)b * mc + e0 : nullptr;
   load4(y + (int64_t)b * d + e0, cnt, vec, yv);
   float scale = 1.0f;
   if (CACHE_FROM_MEANS) {
@@ -69,6 +70,7 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(
 #pragma unroll
     for (int c = 0; c < 4; ++c) sv[c] = qcv[c] - cc.x * xcv[c];  // c2_c S_c
     scale = cc.w;
+    if (svout) store4(svout + (int64_t)b * d + e0, cnt, vec, sv);
   } else {
     load4(cs + (int64_t)b * d + e0, cnt, vec, sv);
   }
@@ -178,7 +180,7 @@ hipError_t draft_launch(const Sched& sc, int B, int K, int d, const float* y, co
   return timed("draft_block", s, [&] {
     draft_kernel<false><<<grid, kThreads, 0, s>>>(sc, nullptr, K, d, y, cs, nullptr, nullptr, nullptr, 0, 0,
                                                   k, rnd, seed, x, xs.chain, xs.row, mp, mps.chain,
-                                                  mps.row, vec, gate);
+                                                  mps.row, nullptr, vec, gate);
   });
 }
 
@@ -186,16 +188,16 @@ hipError_t draft_cached_launch(const Sched& sc, const float4* coef, int B, int K
                                const float* y,
                                const int32_t* crow, const int32_t* cstep, const float* mqprev,
                                sd_stride mqs, const int32_t* k, const uint32_t* rnd,
-                               uint64_t seed, float* x, sd_stride xs, float* mp, sd_stride mps,
+                               uint64_t seed, float* x, sd_stride xs, float* sv,
                                hipStream_t s, const int* gate) {
   const int ng = (d + 3) / 4;
   dim3 grid((ng + kThreads - 1) / kThreads, B);
-  const bool vec = draft_vec(d, xs, mps, y, x, mp) && aligned16(mqprev) && mqs.chain % 4 == 0 &&
-                   mqs.row % 4 == 0;
+  const bool vec = draft_vec(d, xs, sd_stride{d, d}, y, x, sv) && aligned16(mqprev) &&
+                   mqs.chain % 4 == 0 && mqs.row % 4 == 0;
   return timed("draft_block", s, [&] {
     draft_kernel<true><<<grid, kThreads, 0, s>>>(sc, coef, K, d, y, nullptr, crow, cstep, mqprev,
                                                  mqs.chain, mqs.row, k, rnd, seed, x, xs.chain,
-                                                 xs.row, mp, mps.chain, mps.row, vec, gate);
+                                                 xs.row, nullptr, 0, 0, sv, vec, gate);
   });
 }
 

@@ -20,6 +20,7 @@
 #include "bufio.hpp"
 #include "common.hpp"
 #include "philox.hpp"
+#include "rows.hpp"
 #include "rowsum.hpp"
 
 namespace sd {
@@ -356,8 +357,11 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
 // The sampler's second GEMM: O = P mu with the EM epilogue, plus the partial
 // log-ratio sums of verification while the tile is on chip.  Rows are
 // (chain b, row j) of a [B][K+1][d] block: x row j is draft yhat_{k+j} (row 0
-// the state) and MP [B][K][d] holds m^p_{k+j}.  For j < K and the tile's 64
-// columns the kernel accumulates, in float64 from the float32 values,
+// the state); the draft mean m^p_{k+j} is recomputed from x row j and the
+// chain's cache row SV[b] = c2_c S_c exactly as the draft formed it
+// (draft_mean, with c2_{k+j} / c2_c from the step tables and the cache step
+// cstep[b]).  For j < K and the tile's 64 columns the kernel accumulates, in
+// float64 from the float32 values,
 //   sum (m^p - m^q)^2   and   sum (yhat_{j+1} - m^p)(m^p - m^q),
 // i.e. ||Delta_{j+1}||^2 sigma^2 and Z.Delta sigma^2 (App. A.2), and
 // sum (m^p - m^q) G with the residual's G (Alg. 5), into
@@ -369,17 +373,18 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
 // VEC: M a whole number of chunks, d a whole number of tiles, rows 16-byte
 // aligned; every epilogue access is then an unconditional buffer access
 // through a view of the tile's rows (x: 65 rows, the last for the next draft
-// of the tile's last row; m^p: the K rows of the tile's chains; m^q: the
-// tile's rows), so rows past the block read zero and their stores drop.
+// of the tile's last row; SV: the tile's chains; m^q: the tile's rows), so
+// rows past the block read zero and their stores drop.
 template <bool VEC>
 __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     int R, int M, int d, int K1, const float* __restrict__ P, const float* __restrict__ muT,
-    const float* __restrict__ X, const float* __restrict__ rowc, const float* __restrict__ MP,
-    float* __restrict__ mq, double* __restrict__ lrp, const uint32_t* __restrict__ rnd,
-    uint64_t seed, const int* gate) {
+    const float* __restrict__ X, const float* __restrict__ rowc, const float* __restrict__ SV,
+    const int32_t* __restrict__ cstep, const float4* __restrict__ coef, float* __restrict__ mq,
+    double* __restrict__ lrp, const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
   if (gate && *gate == 0) return;
   __shared__ TileLds sm;
   __shared__ float rc[3 * TILE];
+  __shared__ float cscale[TILE];  // 1 / c2 at each chain's cache step
   // grid (column tiles, row tiles): the column tile varies fastest so that
   // neighbouring workgroups stream neighbouring pieces of the same rows
   const int nct = gridDim.x;
@@ -407,12 +412,13 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
 #pragma unroll
   for (int u = 0; u < kGItems; ++u)
     rn[u] = rnd[min(b_first + (int)((threadIdx.x + kThreads * u) >> 4), B - 1)];
+  const float csv = coef[cstep[min(b_first + (int)threadIdx.x, B - 1)]].w;
   // keep that issue order: the scheduler must not hoist the bulk loads above
   __builtin_amdgcn_sched_barrier(0);
   __amdgpu_buffer_rsrc_t vx, vp, vq;
   if constexpr (VEC) {
     vx = buf_view(X + (int64_t)r0 * d, (int64_t)min(R - r0, TILE + 1) * d * 4);
-    vp = buf_view(MP + (int64_t)b_first * K * d, (int64_t)min(B - b_first, nchain) * K * d * 4);
+    vp = buf_view(SV + (int64_t)b_first * d, (int64_t)min(B - b_first, nchain) * d * 4);
     vq = buf_view(mq + (int64_t)r0 * d, (int64_t)min(R - r0, TILE) * d * 4);
   }
   float4 xv[4], yv[4], pv[4];
@@ -421,18 +427,18 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     const int lr = rg + 16 * i, row = r0 + lr;
     const int b = row / K1, j = row - b * K1;
     if constexpr (VEC) {
-      // rows past the block and the next-draft / m^p reads of a chain's last
-      // row land past a view or are not used
+      // rows past the block land past a view; the next draft of a chain's
+      // last row is loaded and not used
       xv[i] = buf_ld4(vx, (uint32_t)((lr * d + col) * 4));
       yv[i] = buf_ld4(vx, (uint32_t)(((lr + 1) * d + col) * 4));
-      pv[i] = buf_ld4(vp, (uint32_t)((((b - b_first) * K + j) * d + col) * 4));
+      pv[i] = buf_ld4(vp, (uint32_t)(((b - b_first) * d + col) * 4));
     } else {
       const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
       const float* px = X + (int64_t)row * d + col;
       xv[i] = row < R && cnt > 0 ? ld4(px, cnt, false) : z4;
       const bool dr = row < R && cnt > 0 && j < K1 - 1;
       yv[i] = dr ? ld4(px + d, cnt, false) : z4;
-      pv[i] = dr ? ld4(MP + ((int64_t)b * K + j) * d + col, cnt, false) : z4;
+      pv[i] = dr ? ld4(SV + (int64_t)b * d + col, cnt, false) : z4;
     }
   }
   f32x16 acc;
@@ -447,6 +453,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     for (int v = 0; v < 16; ++v) sm.a[out_row(v) * LDW + cw] = acc[v];
   }
   if (threadIdx.x < 3 * TILE) rc[threadIdx.x] = r0 + (int)threadIdx.x / 3 < R ? rcv : 0.f;
+  if (threadIdx.x < TILE) cscale[threadIdx.x] = csv;
   // G of the residual (RESID stream of each chain's current round) depends
   // only on the chain and the coordinate: drawn once per chain of the tile
   // into sm.b (item e: chain e / 16, coordinates 4 (e % 16) ..)
@@ -480,11 +487,13 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     }
     if (row < R && j < K1 - 1) {
       const float4 gv = *reinterpret_cast<const float4*>(&sm.b[(b - b_first) * LDW + 4 * cg]);
+      const float c2s = c2 * cscale[b - b_first];
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         if (e < cnt) {
-          const double dd = (double)comp(pv[i], e) - (double)comp(qv, e);
-          const double zz = (double)comp(yv[i], e) - (double)comp(pv[i], e);
+          const float pe = draft_mean(c1, comp(x, e), c2s, comp(pv[i], e));  // m^p
+          const double dd = (double)pe - (double)comp(qv, e);
+          const double zz = (double)comp(yv[i], e) - (double)pe;
           s2[i] = fma(dd, dd, s2[i]);
           sz[i] = fma(zz, dd, sz[i]);
           sgd[i] = fma((double)comp(gv, e), dd, sgd[i]);
@@ -613,11 +622,12 @@ hipError_t target_mean_launch(const Target& t, int R, const float* x, int64_t ld
 }
 
 hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
-                                 const int32_t* step, float* mq, const float* mp, double* lrp,
-                                 const uint32_t* rnd, uint64_t seed, void* ws, hipStream_t s,
-                                 const int* gate) {
+                                 const int32_t* step, float* mq, const float* sv,
+                                 const int32_t* cstep, double* lrp, const uint32_t* rnd,
+                                 uint64_t seed, void* ws, hipStream_t s, const int* gate) {
   if (t.prec == SD_BF16)
-    return target_mean_lr_bf16_launch(t, R, K1, x, step, mq, mp, lrp, rnd, seed, ws, s, gate);
+    return target_mean_lr_bf16_launch(t, R, K1, x, step, mq, sv, cstep, lrp, rnd, seed, ws, s,
+                                      gate);
   const Plan p = make_plan(t, R);
   char* base = static_cast<char*>(ws);
   float* part = reinterpret_cast<float*>(base + p.off_part);
@@ -632,15 +642,15 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
   // the buffer path: whole chunks of M and tiles of d, aligned rows, and
   // 32-bit offsets inside a tile's views
   const bool vec = t.M % KC == 0 && t.d % TILE == 0 && aligned16(x) && aligned16(mq) &&
-                   aligned16(mp) && (int64_t)(TILE + 2 * K1 + 1) * t.d * 4 < ((int64_t)1 << 31) &&
+                   aligned16(sv) && (int64_t)(TILE + 2) * t.d * 4 < ((int64_t)1 << 31) &&
                    t.M < 1 << 22;
   return timed("gmm_mean_lr", s, [&] {
     if (vec)
-      gmm_mean_lr_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, P, t.muT, x, rowc, mp,
-                                                       mq, lrp, rnd, seed, gate);
+      gmm_mean_lr_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, P, t.muT, x, rowc, sv,
+                                                       cstep, t.coef, mq, lrp, rnd, seed, gate);
     else
-      gmm_mean_lr_kernel<false><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, P, t.muT, x, rowc, mp,
-                                                        mq, lrp, rnd, seed, gate);
+      gmm_mean_lr_kernel<false><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, P, t.muT, x, rowc, sv,
+                                                        cstep, t.coef, mq, lrp, rnd, seed, gate);
   });
 }
 

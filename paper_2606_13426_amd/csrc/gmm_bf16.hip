@@ -13,6 +13,7 @@
 #include "common.hpp"
 #include "gemm_bf16.hpp"
 #include "philox.hpp"
+#include "rows.hpp"
 #include "rowsum.hpp"
 
 namespace sd {
@@ -195,15 +196,19 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_bf16_kernel(
 // partials: for draft rows j < K and this tile's columns, float64 sums of
 // (m^p - m^q)^2, (yhat_{j+1} - m^p)(m^p - m^q) and G (m^p - m^q), G the
 // residual's normals of the chain's round, into lrp[row][column tile][3].
+// m^p is recomputed from x row j and the chain's cache row SV[b] as the draft
+// formed it (draft_mean; c2_{k+j} / c2_c from the tables and cstep[b]).
 template <bool VEC>
 __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
     int R, int M, int d, int K1, const uint16_t* __restrict__ P,
     const uint16_t* __restrict__ muT, const float* __restrict__ X, const float* __restrict__ rowc,
-    const float* __restrict__ MP, float* __restrict__ mq, double* __restrict__ lrp, bool vecd,
+    const float* __restrict__ SV, const int32_t* __restrict__ cstep,
+    const float4* __restrict__ coef, float* __restrict__ mq, double* __restrict__ lrp, bool vecd,
     const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
   if (gate && *gate == 0) return;
   __shared__ OperandLds sm[2];
   __shared__ float rc[3 * TM];
+  __shared__ float cscale[kMaxChains];  // 1 / c2 at each chain's cache step
   const int nct = gridDim.x;
   int ct, rt;
   col_major_xcd(nct, gridDim.y, ct, rt);
@@ -212,12 +217,17 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
   f32x16 acc[2][2];
   zero(acc);
   double unused[8];
+  // the cache scale of the tile's chains, fetched before the contraction (an
+  // unconditional load from a clamped index) and staged after it
+  const int B = R / K1;
+  const float csv = coef[cstep[min(r0 / K1 + (int)threadIdx.x, B - 1)]].w;
   tile<false, VEC>(sm, P, M, R, muT, M, d, r0, c0, 0, M, acc, unused);
   float* stg = reinterpret_cast<float*>(&sm[0]);
   float* gz = reinterpret_cast<float*>(&sm[1]);
   const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;
   const int b_first = r0 / K1;
   const int nchain = min((min(r0 + TM, R) - 1) / K1 - b_first + 1, kMaxChains);
+  if ((int)threadIdx.x < nchain) cscale[threadIdx.x] = csv;
   double t2 = 0.0, tz = 0.0, tg = 0.0;  // this lane's row (see reduce_rows16), both passes
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
@@ -247,7 +257,7 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
       xv[i] = row < R && cnt > 0 ? ld4(px, cnt, vecd) : z4;
       const bool dr = row < R && cnt > 0 && j < K1 - 1;
       yv[i] = dr ? ld4(px + d, cnt, vecd) : z4;
-      pv[i] = dr ? ld4(MP + ((int64_t)b * (K1 - 1) + j) * d + col, cnt, vecd) : z4;
+      pv[i] = dr ? ld4(SV + (int64_t)b * d + col, cnt, vecd) : z4;  // the chain's cache row
     }
     double s2[8], sz[8], sgd[8];
 #pragma unroll
@@ -266,11 +276,13 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
       st4(mq + (int64_t)row * d + col, cnt, vecd, qv);
       if (j < K1 - 1) {
         const float4 gv = *reinterpret_cast<const float4*>(&gz[(b - b_first) * LDO + 4 * cg]);
+        const float c2s = c2 * cscale[b - b_first];
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           if (e < cnt) {
-            const double dd = (double)comp(pv[i], e) - (double)comp(qv, e);
-            const double zz = (double)comp(yv[i], e) - (double)comp(pv[i], e);
+            const float pe = draft_mean(c1, comp(x, e), c2s, comp(pv[i], e));  // m^p
+            const double dd = (double)pe - (double)comp(qv, e);
+            const double zz = (double)comp(yv[i], e) - (double)pe;
             s2[i] = fma(dd, dd, s2[i]);
             sz[i] = fma(zz, dd, sz[i]);
             sgd[i] = fma((double)comp(gv, e), dd, sgd[i]);
@@ -391,24 +403,24 @@ hipError_t target_mean_bf16_launch(const Target& t, int R, const float* x, int64
 }
 
 hipError_t target_mean_lr_bf16_launch(const Target& t, int R, int K1, const float* x,
-                                      const int32_t* step, float* mq, const float* mp,
-                                      double* lrp, const uint32_t* rnd, uint64_t seed, void* ws,
-                                      hipStream_t s, const int* gate) {
+                                      const int32_t* step, float* mq, const float* sv,
+                                      const int32_t* cstep, double* lrp, const uint32_t* rnd,
+                                      uint64_t seed, void* ws, hipStream_t s, const int* gate) {
   const Plan p = make_plan(t, R);
   const Bufs w = carve(p, ws);
-  const bool vecd = (t.d % 4 == 0) && aligned16(x) && aligned16(mq) && aligned16(mp);
+  const bool vecd = (t.d % 4 == 0) && aligned16(x) && aligned16(mq) && aligned16(sv);
   hipError_t e = logits_and_softmax(t, p, w, R, x, t.d, vecd, step, s, gate);
   if (e != hipSuccess) return e;
   dim3 g2((t.d + TN - 1) / TN, (R + TM - 1) / TM);
   return timed("gmm_mean_lr_bf16", s, [&] {
     if (t.M % KC == 0)
       gmm_mean_lr_bf16_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, w.P, t.muT16, x,
-                                                            w.rowc, mp, mq, lrp, vecd, rnd, seed,
-                                                            gate);
+                                                            w.rowc, sv, cstep, t.coef, mq, lrp,
+                                                            vecd, rnd, seed, gate);
     else
       gmm_mean_lr_bf16_kernel<false><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, w.P, t.muT16, x,
-                                                             w.rowc, mp, mq, lrp, vecd, rnd, seed,
-                                                             gate);
+                                                             w.rowc, sv, cstep, t.coef, mq, lrp,
+                                                             vecd, rnd, seed, gate);
   });
 }
 

@@ -35,12 +35,21 @@ __device__ __forceinline__ float4 step_coef(const Sched& sc, const float4* __res
   return make_float4((float)sched_c1(sc, n), (float)c2, (float)sched_sigma(sc, n), (float)(1.0 / c2));
 }
 
+// The Free Drafter's mean m^p = c1_n yhat + c2s sv with c2s = c2_n / c2_c and
+// sv = c2_c S_c, in one fixed sequence of float32 operations (the product,
+// then one fused multiply-add), so that every kernel that needs m^p recomputes
+// the same bits as the draft that produced yhat.
+__device__ __forceinline__ float draft_mean(float c1, float y, float c2s, float sv) {
+  return __fmaf_rn(c1, y, c2s * sv);
+}
+
 // Draft rows 1..K of one chain for coordinates e0..e0+3 (group g), starting
 // at yhat_0 = yv (already stored as row 0 by the caller) and step k with
 // K_b = kb valid drafts (Sec. 3.3):
 //   m^p_{i-1} = c1_n yhat_{i-1} + c2_n S_c,  yhat_i = m^p_{i-1} + sigma_n xi_i,
 // where c2_n S_c = (c2_n * scale) * sv; rows past K_b repeat the last draft
-// and mean so that every row the target call reads is finite.
+// and mean so that every row the target call reads is finite.  mb may be
+// null (the sampler recomputes m^p where it needs it, see draft_mean).
 __device__ __forceinline__ void draft_rows(const Sched& sc, const float4* __restrict__ coef, int K,
                                            int k, int kb, uint32_t chain, uint32_t rnd,
                                            uint64_t seed, int g, float (&yv)[4],
@@ -54,14 +63,14 @@ __device__ __forceinline__ void draft_rows(const Sched& sc, const float4* __rest
     const float4 z = normals4(philox((uint32_t)g, chain, rnd, (TAG_DRAFT << 24) | (uint32_t)i, seed));
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
-      m[c] = cf.x * yv[c] + c2 * sv[c];
+      m[c] = draft_mean(cf.x, yv[c], c2, sv[c]);
       yv[c] = m[c] + cf.z * get4(z, c);
     }
-    store4(mb + (int64_t)(i - 1) * mr, cnt, vec, m);
+    if (mb) store4(mb + (int64_t)(i - 1) * mr, cnt, vec, m);
     store4(xb + (int64_t)i * xr, cnt, vec, yv);
   }
   for (int i = kb + 1; i <= K; ++i) {
-    store4(mb + (int64_t)(i - 1) * mr, cnt, vec, m);
+    if (mb) store4(mb + (int64_t)(i - 1) * mr, cnt, vec, m);
     store4(xb + (int64_t)i * xr, cnt, vec, yv);
   }
 }

@@ -251,8 +251,8 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(
 __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
     int B, int K, int d, int N, int mode, int umode, const double* __restrict__ lrp, int nct,
     const double* __restrict__ sigma, const int32_t* __restrict__ kcur,
-    const uint32_t* __restrict__ rcur, uint64_t seed, const float* __restrict__ MP,
-    const float* __restrict__ MQ, int32_t* __restrict__ tau, int32_t* __restrict__ rmode,
+    const uint32_t* __restrict__ rcur, uint64_t seed, int32_t* __restrict__ tau,
+    int32_t* __restrict__ rmode,
     float* __restrict__ rcoef, float* __restrict__ rsig, int* nanflag, int* act_next,
     const int* gate) {
   if (blockIdx.x == 0 && threadIdx.x == 0) *act_next = 0;
@@ -368,15 +368,14 @@ hipError_t verify_launch(int B, int K, int d, int mode, const float* yd, sd_stri
 
 hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, const double* lrp,
                              int nct, const double* sigma, const int32_t* kcur,
-                             const uint32_t* rcur, uint64_t seed, const float* mp,
-                             const float* mq, int32_t* tau, int32_t* rmode, float* rcoef,
-                             float* rsig, int* nanflag, int* act_next, hipStream_t s,
-                             const int* gate) {
+                             const uint32_t* rcur, uint64_t seed, int32_t* tau, int32_t* rmode,
+                             float* rcoef, float* rsig, int* nanflag, int* act_next,
+                             hipStream_t s, const int* gate) {
   const int per = kThreads / 64;
   return timed("scan_fused", s, [&] {
     scan_fused_kernel<<<(B + per - 1) / per, kThreads, 0, s>>>(
-        B, K, d, N, mode, umode, lrp, nct, sigma, kcur, rcur, seed, mp, mq, tau, rmode, rcoef,
-        rsig, nanflag, act_next, gate);
+        B, K, d, N, mode, umode, lrp, nct, sigma, kcur, rcur, seed, tau, rmode, rcoef, rsig,
+        nanflag, act_next, gate);
   });
 }
 
