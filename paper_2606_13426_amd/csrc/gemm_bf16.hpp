@@ -256,12 +256,29 @@ __device__ __forceinline__ void tile(OperandLds (&sm)[2], const TA* __restrict__
     __syncthreads();
     return;
   }
-  // up to four chunks, one at a time
-  for (int c = 0; c < n; ++c) {
-    ld(c, ra0, rb0);
-    st(sm[c & 1], ra0, rb0);
+  // up to four chunks: the same pipeline, unrolled (uniform branches on n)
+  if (n <= 0) return;
+  ld(0, ra0, rb0);
+  if (n > 1) ld(1, ra1, rb1);
+  st(sm[0], ra0, rb0);
+  __syncthreads();
+  if (n > 2) ld(2, ra0, rb0);
+  mma_chunk(sm[0], acc);
+  if (n > 1) {
+    st(sm[1], ra1, rb1);
+    __syncthreads();  // also: chunk 0's reads of buffer 0 are done
+    if (n > 3) ld(3, ra1, rb1);
+    mma_chunk(sm[1], acc);
+  }
+  if (n > 2) {
+    st(sm[0], ra0, rb0);
+    __syncthreads();  // also: chunk 1's reads of buffer 1 are done
+    mma_chunk(sm[0], acc);
+  }
+  if (n > 3) {
+    st(sm[1], ra1, rb1);
     __syncthreads();
-    mma_chunk(sm[c & 1], acc);
+    mma_chunk(sm[1], acc);
   }
   __syncthreads();
 }

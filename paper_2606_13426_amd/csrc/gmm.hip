@@ -412,7 +412,9 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
 #pragma unroll
   for (int u = 0; u < kGItems; ++u)
     rn[u] = rnd[min(b_first + (int)((threadIdx.x + kThreads * u) >> 4), B - 1)];
-  const float csv = coef[cstep[min(b_first + (int)threadIdx.x, B - 1)]].w;
+  // (the step index only: the table lookup that depends on it waits until
+  // after the contraction, so that no wait here covers the bulk loads)
+  const int csi = cstep[min(b_first + (int)threadIdx.x, B - 1)];
   // keep that issue order: the scheduler must not hoist the bulk loads above
   __builtin_amdgcn_sched_barrier(0);
   __amdgpu_buffer_rsrc_t vx, vp, vq;
@@ -453,7 +455,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     for (int v = 0; v < 16; ++v) sm.a[out_row(v) * LDW + cw] = acc[v];
   }
   if (threadIdx.x < 3 * TILE) rc[threadIdx.x] = r0 + (int)threadIdx.x / 3 < R ? rcv : 0.f;
-  if (threadIdx.x < TILE) cscale[threadIdx.x] = csv;
+  if (threadIdx.x < TILE) cscale[threadIdx.x] = coef[csi].w;
   // G of the residual (RESID stream of each chain's current round) depends
   // only on the chain and the coordinate: drawn once per chain of the tile
   // into sm.b (item e: chain e / 16, coordinates 4 (e % 16) ..)

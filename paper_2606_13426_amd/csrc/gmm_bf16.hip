@@ -10,6 +10,7 @@
 //                    partial sums of the sampler (as the float32 path).
 // The 128 x 128 accumulator tile is handed to the epilogue through LDS in two
 // passes of 64 columns, each over the operand buffers' storage.
+#include "bufio.hpp"
 #include "common.hpp"
 #include "gemm_bf16.hpp"
 #include "philox.hpp"
@@ -192,6 +193,101 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_bf16_kernel(
   }
 }
 
+// The aligned epilogue of the sampler's mean GEMM (d a whole number of tiles,
+// rows 16-byte aligned, at least eight rows per chain for the cache-row
+// loads: K + 1 >= 8).  Thread t owns staging columns 4 (t % 16) .. + 3 of the
+// eight consecutive tile rows 8 (t / 16) .. + 7, so the next draft yhat_{j+1}
+// of a row is the x of the thread's next row (one extra load for the last),
+// and the eight rows meet at most two chains (two cache-row loads).  Every
+// global load of both passes is issued before the first store (stores and
+// loads share one in-order counter), through buffer views of the tile's rows
+// (rows past the block read zero; their stores drop).
+__device__ __forceinline__ void mean_lr_epilogue_vec(
+    float* stg, float* gz, const float* cscale, const float* rc, const f32x16 (&acc)[2][2], int R,
+    int d, int K1, int r0, int c0, int ct, int nct, int b_first, int nchain,
+    const float* __restrict__ X, const float* __restrict__ SV, float* __restrict__ mq,
+    double* __restrict__ lrp, const uint32_t* __restrict__ rnd, uint64_t seed) {
+  const int cg = threadIdx.x & 15, lr0 = 8 * (threadIdx.x >> 4);
+  const int B = R / K1;
+  const __amdgpu_buffer_rsrc_t vx = buf_view(X + (int64_t)r0 * d, (int64_t)min(R - r0, TM + 1) * d * 4);
+  const __amdgpu_buffer_rsrc_t vs = buf_view(SV + (int64_t)b_first * d, (int64_t)min(B - b_first, nchain) * d * 4);
+  const __amdgpu_buffer_rsrc_t vq = buf_view(mq + (int64_t)r0 * d, (int64_t)min(R - r0, TM) * d * 4);
+  const int bl = (r0 + lr0) / K1, bh = min((r0 + lr0 + 7) / K1, B);  // chains of the eight rows
+  // the chains' rounds for the G draws (items e = t + 256 u: chain e / 16)
+  constexpr int kMaxChainsVec = TM / 8 + 2;  // chains that 128 rows can touch with K + 1 >= 8
+  constexpr int kGItems = (kMaxChainsVec * 16 + kThreads - 1) / kThreads;
+  uint32_t rn[kGItems];
+#pragma unroll
+  for (int u = 0; u < kGItems; ++u)
+    rn[u] = rnd[min(b_first + (int)((threadIdx.x + kThreads * u) >> 4), B - 1)];
+  float4 xv[2][9], sl[2], sh[2];
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    const int col = c0 + epi_col(cg, p);
+#pragma unroll
+    for (int i = 0; i < 9; ++i) xv[p][i] = buf_ld4(vx, (uint32_t)(((lr0 + i) * d + col) * 4));
+    sl[p] = buf_ld4(vs, (uint32_t)(((bl - b_first) * d + col) * 4));
+    sh[p] = buf_ld4(vs, (uint32_t)(((bh - b_first) * d + col) * 4));
+  }
+  double t2 = 0.0, tz = 0.0, tg = 0.0;  // this lane's row (see reduce_rows16), both passes
+#pragma unroll
+  for (int p = 0; p < 2; ++p) {
+    __syncthreads();  // the operand tiles (p = 0) or the previous pass are consumed
+    stage(stg, acc, p);
+#pragma unroll
+    for (int u = 0; u < kGItems; ++u) {
+      const int e = threadIdx.x + kThreads * u;
+      if (e < nchain * 16) {
+        const int tcol = c0 + epi_col(e & 15, p);
+        *reinterpret_cast<float4*>(&gz[(e >> 4) * LDO + 4 * (e & 15)]) =
+            normals4(philox((uint32_t)(tcol >> 2), (uint32_t)(b_first + (e >> 4)), rn[u],
+                            TAG_RESID << 24, seed));
+      }
+    }
+    __syncthreads();
+    const int col = c0 + epi_col(cg, p);
+    double s2[8], sz[8], sgd[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      s2[i] = sz[i] = sgd[i] = 0.0;
+      const int lr = lr0 + i, row = r0 + lr;
+      const int b = row / K1, j = row - b * K1;
+      const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
+      const float4 ov = *reinterpret_cast<const float4*>(&stg[lr * LDO + 4 * cg]);
+      const float4 x = xv[p][i], y = xv[p][i + 1];
+      const float4 qv = make_float4(c1 * x.x + c2 * (ov.x - rho * x.x),
+                                    c1 * x.y + c2 * (ov.y - rho * x.y),
+                                    c1 * x.z + c2 * (ov.z - rho * x.z),
+                                    c1 * x.w + c2 * (ov.w - rho * x.w));
+      buf_st4(vq, (uint32_t)((lr * d + col) * 4), qv);
+      if (row < R && j < K1 - 1) {
+        const float4 sv = b == bl ? sl[p] : sh[p];
+        const float4 gv = *reinterpret_cast<const float4*>(&gz[(b - b_first) * LDO + 4 * cg]);
+        const float c2s = c2 * cscale[b - b_first];
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float pe = draft_mean(c1, comp(x, e), c2s, comp(sv, e));  // m^p
+          const double dd = (double)pe - (double)comp(qv, e);
+          const double zz = (double)comp(y, e) - (double)pe;
+          s2[i] = fma(dd, dd, s2[i]);
+          sz[i] = fma(zz, dd, sz[i]);
+          sgd[i] = fma((double)comp(gv, e), dd, sgd[i]);
+        }
+      }
+    }
+    t2 += reduce_rows16<8>(s2, cg);
+    tz += reduce_rows16<8>(sz, cg);
+    tg += reduce_rows16<8>(sgd, cg);
+  }
+  const int row = r0 + lr0 + row_of<8>(cg);
+  if ((cg & 1) == 0 && row < R) {
+    double* o = lrp + ((int64_t)row * nct + ct) * 3;
+    o[0] = t2;
+    o[1] = tz;
+    o[2] = tg;
+  }
+}
+
 // The sampler's mean GEMM on its [B][K+1][d] block with the verification
 // partials: for draft rows j < K and this tile's columns, float64 sums of
 // (m^p - m^q)^2, (yhat_{j+1} - m^p)(m^p - m^q) and G (m^p - m^q), G the
@@ -217,17 +313,23 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
   f32x16 acc[2][2];
   zero(acc);
   double unused[8];
-  // the cache scale of the tile's chains, fetched before the contraction (an
-  // unconditional load from a clamped index) and staged after it
+  // the cache steps of the tile's chains, fetched before the contraction (an
+  // unconditional load from a clamped index; the table lookup that depends on
+  // it comes after, so that no early wait stalls the workgroup)
   const int B = R / K1;
-  const float csv = coef[cstep[min(r0 / K1 + (int)threadIdx.x, B - 1)]].w;
+  const int csi = cstep[min(r0 / K1 + (int)threadIdx.x, B - 1)];
   tile<false, VEC>(sm, P, M, R, muT, M, d, r0, c0, 0, M, acc, unused);
   float* stg = reinterpret_cast<float*>(&sm[0]);
   float* gz = reinterpret_cast<float*>(&sm[1]);
   const int cg = threadIdx.x & 15, rg = threadIdx.x >> 4;
   const int b_first = r0 / K1;
   const int nchain = min((min(r0 + TM, R) - 1) / K1 - b_first + 1, kMaxChains);
-  if ((int)threadIdx.x < nchain) cscale[threadIdx.x] = csv;
+  if ((int)threadIdx.x < nchain) cscale[threadIdx.x] = coef[csi].w;
+  if constexpr (VEC) {
+    mean_lr_epilogue_vec(stg, gz, cscale, rc, acc, R, d, K1, r0, c0, ct, nct, b_first, nchain, X,
+                         SV, mq, lrp, rnd, seed);
+    return;
+  }
   double t2 = 0.0, tz = 0.0, tg = 0.0;  // this lane's row (see reduce_rows16), both passes
 #pragma unroll
   for (int p = 0; p < 2; ++p) {
@@ -412,8 +514,12 @@ hipError_t target_mean_lr_bf16_launch(const Target& t, int R, int K1, const floa
   hipError_t e = logits_and_softmax(t, p, w, R, x, t.d, vecd, step, s, gate);
   if (e != hipSuccess) return e;
   dim3 g2((t.d + TN - 1) / TN, (R + TM - 1) / TM);
+  // the buffer path: whole chunks of M, whole tiles of d, aligned rows, at
+  // least eight rows per chain, 32-bit offsets inside a tile's views
+  const bool vec = t.M % KC == 0 && t.d % TN == 0 && vecd && K1 >= 8 &&
+                   (int64_t)(TM + 2) * t.d * 4 < ((int64_t)1 << 31);
   return timed("gmm_mean_lr_bf16", s, [&] {
-    if (t.M % KC == 0)
+    if (vec)
       gmm_mean_lr_bf16_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, w.P, t.muT16, x,
                                                             w.rowc, sv, cstep, t.coef, mq, lrp,
                                                             vecd, rnd, seed, gate);
