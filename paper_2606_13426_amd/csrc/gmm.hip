@@ -423,18 +423,27 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     vp = buf_view(SV + (int64_t)b_first * d, (int64_t)min(B - b_first, nchain) * d * 4);
     vq = buf_view(mq + (int64_t)r0 * d, (int64_t)min(R - r0, TILE) * d * 4);
   }
+  // VEC: the thread's rows are the four consecutive tile rows 4 rg + i, so the
+  // next draft of a row is the x of the next one (one extra load for the
+  // last) and the rows meet at most two chains (K + 1 >= 4: two cache-row
+  // loads); otherwise rows rg + 16 i
+  const int lrb = VEC ? 4 * rg : rg, lstep = VEC ? 1 : 16;
   float4 xv[4], yv[4], pv[4];
+  float4 xnext, svl, svh;  // VEC: x of the row after the four, cache rows of their chains
+  const int bl = (r0 + lrb) / K1;
+  if constexpr (VEC) {
+    // rows past the block land past a view
+#pragma unroll
+    for (int i = 0; i < 4; ++i) xv[i] = buf_ld4(vx, (uint32_t)(((lrb + i) * d + col) * 4));
+    xnext = buf_ld4(vx, (uint32_t)(((lrb + 4) * d + col) * 4));
+    svl = buf_ld4(vp, (uint32_t)(((bl - b_first) * d + col) * 4));
+    svh = buf_ld4(vp, (uint32_t)((((r0 + lrb + 3) / K1 - b_first) * d + col) * 4));
+  }
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int lr = rg + 16 * i, row = r0 + lr;
     const int b = row / K1, j = row - b * K1;
-    if constexpr (VEC) {
-      // rows past the block land past a view; the next draft of a chain's
-      // last row is loaded and not used
-      xv[i] = buf_ld4(vx, (uint32_t)((lr * d + col) * 4));
-      yv[i] = buf_ld4(vx, (uint32_t)(((lr + 1) * d + col) * 4));
-      pv[i] = buf_ld4(vp, (uint32_t)(((b - b_first) * d + col) * 4));
-    } else {
+    if constexpr (!VEC) {
       const float4 z4 = make_float4(0.f, 0.f, 0.f, 0.f);
       const float* px = X + (int64_t)row * d + col;
       xv[i] = row < R && cnt > 0 ? ld4(px, cnt, false) : z4;
@@ -472,11 +481,19 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     s2[i] = sz[i] = sgd[i] = 0.0;
-    const int lr = rg + 16 * i, row = r0 + lr;
+    const int lr = lrb + lstep * i, row = r0 + lr;
     const int b = row / K1, j = row - b * K1;
     const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
     const float4 ov = *reinterpret_cast<const float4*>(&sm.a[lr * LDW + 4 * cg]);
     const float4 x = xv[i];
+    float4 y, sv;
+    if constexpr (VEC) {
+      y = i < 3 ? xv[i < 3 ? i + 1 : 3] : xnext;
+      sv = b == bl ? svl : svh;
+    } else {
+      y = yv[i];
+      sv = pv[i];
+    }
     const float4 qv = make_float4(c1 * x.x + c2 * (ov.x - rho * x.x),
                                   c1 * x.y + c2 * (ov.y - rho * x.y),
                                   c1 * x.z + c2 * (ov.z - rho * x.z),
@@ -493,9 +510,9 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         if (e < cnt) {
-          const float pe = draft_mean(c1, comp(x, e), c2s, comp(pv[i], e));  // m^p
+          const float pe = draft_mean(c1, comp(x, e), c2s, comp(sv, e));  // m^p
           const double dd = (double)pe - (double)comp(qv, e);
-          const double zz = (double)comp(yv[i], e) - (double)pe;
+          const double zz = (double)comp(y, e) - (double)pe;
           s2[i] = fma(dd, dd, s2[i]);
           sz[i] = fma(zz, dd, sz[i]);
           sgd[i] = fma((double)comp(gv, e), dd, sgd[i]);
@@ -506,7 +523,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
   // every lane of the group takes part (rows past R and empty columns add zeros)
   const double t2 = reduce_rows16<4>(s2, cg), tz = reduce_rows16<4>(sz, cg),
                tg = reduce_rows16<4>(sgd, cg);
-  const int row = r0 + rg + 16 * row_of<4>(cg);
+  const int row = r0 + lrb + lstep * row_of<4>(cg);
   if ((cg & 3) == 0 && row < R) {
     double* o = lrp + ((int64_t)row * nct + ct) * 3;
     o[0] = t2;
@@ -641,11 +658,11 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
   e = gmm_softmax_launch(t, R, p.S, part, xsq, step, P, false, rowc, s, gate);
   if (e != hipSuccess) return e;
   dim3 g2((t.d + TILE - 1) / TILE, (R + TILE - 1) / TILE);
-  // the buffer path: whole chunks of M and tiles of d, aligned rows, and
-  // 32-bit offsets inside a tile's views
+  // the buffer path: whole chunks of M and tiles of d, aligned rows, at least
+  // four rows per chain, and 32-bit offsets inside a tile's views
   const bool vec = t.M % KC == 0 && t.d % TILE == 0 && aligned16(x) && aligned16(mq) &&
-                   aligned16(sv) && (int64_t)(TILE + 2) * t.d * 4 < ((int64_t)1 << 31) &&
-                   t.M < 1 << 22;
+                   aligned16(sv) && K1 >= 4 &&
+                   (int64_t)(TILE + 2) * t.d * 4 < ((int64_t)1 << 31) && t.M < 1 << 22;
   return timed("gmm_mean_lr", s, [&] {
     if (vec)
       gmm_mean_lr_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, P, t.muT, x, rowc, sv,
