@@ -532,6 +532,84 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
   }
 }
 
+// The softmax for M <= 64 (M % 4 == 0): sixteen lanes per row, four
+// components per lane read as one float4 per split, four rows per wavefront;
+// the same arithmetic as gmm_softmax_kernel with 16-lane reductions.
+__global__ __launch_bounds__(kThreads) void gmm_softmax_small_kernel(
+    int R, int M, int d, int S, const float* __restrict__ part, const double* __restrict__ xsq,
+    const int32_t* __restrict__ step, Sched sc, const double2* __restrict__ ls,
+    const double* __restrict__ logw, const double* __restrict__ musq, const float4* __restrict__ coef,
+    float* __restrict__ P, float* __restrict__ rowc, const int* gate) {
+  if (gate && *gate == 0) return;
+  const int q = threadIdx.x & 15;
+  const int row = blockIdx.x * (kThreads / 16) + (threadIdx.x >> 4);
+  const bool on = row < R;
+  const int rr = on ? row : R - 1;  // lanes of a missing row follow the last one (no stores)
+  const int n = step[rr];
+  const double a = sched_signal(sc, n), a2 = a * a, hd = 0.5 * (double)d;
+  double xs = 0.0;
+  for (int sp = 0; sp < S; ++sp) xs += xsq[(int64_t)sp * R + rr];
+  const int m0 = 4 * q;
+  const bool has = m0 < M;
+  double dot[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int sp = 0; sp < S; ++sp) {
+    if (has) {
+      const float4 v = *reinterpret_cast<const float4*>(part + ((int64_t)sp * R + rr) * M + m0);
+      dot[0] += (double)v.x;
+      dot[1] += (double)v.y;
+      dot[2] += (double)v.z;
+      dot[3] += (double)v.w;
+    }
+  }
+  const double2* lsn = ls + (int64_t)n * M;
+  double lg[4];
+  double mx = -INFINITY;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    lg[c] = -INFINITY;
+    if (has) {
+      const int m = m0 + c;
+      const double2 t = lsn[m];
+      lg[c] = logw[m] - hd * t.x - 0.5 * (xs - 2.0 * a * dot[c] + a2 * musq[m]) * t.y;
+      mx = fmax(mx, lg[c]);
+    }
+  }
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) mx = fmax(mx, __shfl_xor(mx, o));
+  float e[4];
+  float sum = 0.0f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    e[c] = has ? __expf((float)(lg[c] - mx)) : 0.0f;
+    sum += e[c];
+  }
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) sum += __shfl_xor(sum, o);
+  const double inv = 1.0 / (double)sum;
+  double rho = 0.0;
+  float pv[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    pv[c] = 0.0f;
+    if (has) {
+      const double rm = (double)e[c] * inv;
+      const double is2 = lsn[m0 + c].y;
+      pv[c] = (float)(rm * a * is2);
+      rho += rm * is2;
+    }
+  }
+  if (on && has)
+    *reinterpret_cast<float4*>(P + (int64_t)row * M + m0) = make_float4(pv[0], pv[1], pv[2], pv[3]);
+#pragma unroll
+  for (int o = 8; o > 0; o >>= 1) rho += __shfl_xor(rho, o);
+  if (q == 0 && on) {
+    const float4 cf = coef[n];
+    rowc[3 * (int64_t)row + 0] = cf.x;
+    rowc[3 * (int64_t)row + 1] = cf.y;
+    rowc[3 * (int64_t)row + 2] = (float)rho;
+  }
+}
+
 struct Plan {
   int S, ksplit;
   size_t off_part, off_xsq, off_p, off_rowc, total;
@@ -599,6 +677,14 @@ size_t target_ws_bytes(const Target& t, int rows) {
 hipError_t gmm_softmax_launch(const Target& t, int R, int S, const float* part, const double* xsq,
                               const int32_t* step, void* P, bool p_bf16, float* rowc,
                               hipStream_t s, const int* gate) {
+  if (!p_bf16 && t.M <= 64 && t.M % 4 == 0) {
+    const int nbs = (R + kThreads / 16 - 1) / (kThreads / 16);
+    return timed("gmm_softmax", s, [&] {
+      gmm_softmax_small_kernel<<<nbs, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc,
+                                                        t.ls, t.logw, t.musq, t.coef,
+                                                        static_cast<float*>(P), rowc, gate);
+    });
+  }
   const int per = kThreads / 64;
   const int nb = (R + per - 1) / per;
   return timed("gmm_softmax", s, [&] {
