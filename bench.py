@@ -31,6 +31,30 @@ BF16_PEAK_TFLOPS = 2500.0   # dense bf16 MFMA
 GEMMS = ("gmm_logits", "gmm_mean", "gmm_mean_lr", "gmm_logits_bf16", "gmm_mean_bf16", "gmm_mean_lr_bf16")
 METRIC = "verified chain-steps/sec + mean accepted steps per block; % MFMA / HBM peak"
 
+# HBM bytes per launch of a workload's dominant kernel from two rocprofv3 passes
+# (FETCH_SIZE x 2.000 and WRITE_SIZE x 1.000, the factors a 1 GiB device copy
+# gives; profiles/sampler_pixel3072_hbm_traffic.md), valid for the library
+# sources whose digest (source_digest()) was recorded with them.
+MEASURED_TRAFFIC = {
+    ("pixel3072", "gmm_mean_lr"): dict(bytes=(137.0 + 122.0) * 1e6,
+                                       sources="602518ae4561d73d4e5e8580bde67cf5747ab880"),
+}
+
+
+def source_digest():
+    """sha1 over the library's HIP sources, headers and C header (names and contents)."""
+    import glob
+    import hashlib
+    h = hashlib.sha1()
+    files = sorted(glob.glob(os.path.join(ROOT, "paper_2606_13426_amd", "csrc", "*.hip")) +
+                   glob.glob(os.path.join(ROOT, "paper_2606_13426_amd", "csrc", "*.hpp")) +
+                   [os.path.join(ROOT, "include", "specdiff.h")])
+    for f in files:
+        h.update(os.path.basename(f).encode())
+        with open(f, "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
 
 def _counts_from_trace(trace, N, K):
     """Per round: active chains, verified draft rows and drafted rows, from the tau trace."""
@@ -303,6 +327,9 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     res = run_sampler_bench(lib, args.workload, lib.SD_BLOCK, args.steps, args.warmup, profile=True)
     roof, table = roofline_of(res, args.steps)
+    meas = MEASURED_TRAFFIC.get((args.workload, roof["kernel"])) if roof else None
+    if roof and meas and meas["sources"] == source_digest():
+        roof["traffic"] = meas["bytes"]
     line = dict(metric=METRIC, value=res["B"] * res["N"] / res["sec"], unit="chain-steps/s", n_gpus=1,
                 steps=args.steps, warmup=args.warmup, ms_per_step=1e3 * res["sec"], higher_is_better=True,
                 scaling="weak", vs_baseline=None, dtype=_dtype(args.workload), data="synthetic",
