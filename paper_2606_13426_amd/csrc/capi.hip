@@ -460,18 +460,27 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
   SD_HIP(draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2, cstep2, mq, mqs, k2, rnd2, seed, x,
                              xs, sv, s, nullptr));
 
+  // Round r's scan publishes round r - 1's active flag into slot (r - 1) of
+  // a mapped host array; the host reads round r - kLag's flag once round
+  // r - kLag + 1 has finished, so the queue runs kLag rounds ahead of it.
   int32_t* host_act = nullptr;
-  constexpr int kLag = 3;
-  hipEvent_t ev[kLag + 1];
-  SD_HIP(hipHostMalloc(reinterpret_cast<void**>(&host_act), sizeof(int32_t) * (kLag + 1), hipHostMallocDefault));
-  for (int i = 0; i <= kLag; ++i) {
+  int32_t* host_act_dev = nullptr;
+  constexpr int kLag = 3, kSlots = kLag + 1;
+  hipEvent_t ev[kSlots];
+  SD_HIP(hipHostMalloc(reinterpret_cast<void**>(&host_act), sizeof(int32_t) * kSlots, hipHostMallocDefault));
+  if (hipHostGetDevicePointer(reinterpret_cast<void**>(&host_act_dev), host_act, 0) != hipSuccess) {
+    (void)hipHostFree(host_act);
+    set_error("sd_run_sampler: host flag not mapped");
+    return SD_EHIP;
+  }
+  for (int i = 0; i < kSlots; ++i) {
     host_act[i] = -1;
     (void)hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
   }
   sd_status st = SD_OK;
   int64_t rounds = -1;
   // a round advances every active chain by at least one step, so at most N
-  // rounds have work; the queue runs kLag rounds ahead of the flag it reads
+  // rounds have work
   const int max_rounds = N + 1 + kLag;
   int r = 0;
   for (; r < max_rounds && rounds < 0; ++r) {
@@ -479,20 +488,18 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
     const int* gate = act + cur;
     hipError_t e = target_mean_lr_launch(t, B * K1, K1, x, step, mq, sv, cstep2 + cur * B, lrp,
                                          rnd2 + cur * B, seed, tws, s, gate);
+    int32_t* publish = r >= 1 ? host_act_dev + (r - 1) % kSlots : nullptr;
     if (e == hipSuccess)
       e = scan_fused_launch(B, K, d, N, (int)mode, (int)usample_mode, lrp, L.nct, sigma,
                             k2 + cur * B, rnd2 + cur * B, seed, tau, rmode, rcoef, rsig,
-                            nanflag, act + nxt, s, gate);
+                            nanflag, act + nxt, publish, s, gate);
     if (e == hipSuccess)
       e = advance_launch(t.sc, t.coef, B, K, d, seed, k2 + cur * B, rnd2 + cur * B,
                          crow2 + cur * B, cstep2 + cur * B, k2 + nxt * B, rnd2 + nxt * B,
                          crow2 + nxt * B, cstep2 + nxt * B, tau, rmode, rcoef, rsig, x, sv, mq, y,
                          step, sigma, hist, steps, act + nxt, tau_trace, r,
                          tau_trace ? trace_rounds : 0, s, gate);
-    const int slot = r % (kLag + 1);
-    if (e == hipSuccess)
-      e = hipMemcpyAsync(&host_act[slot], act + nxt, sizeof(int32_t), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipEventRecord(ev[slot], s);
+    if (e == hipSuccess) e = hipEventRecord(ev[r % kSlots], s);
     if (e != hipSuccess) {
       set_error("sd_run_sampler: launch failed in round %d: %s", r, hipGetErrorString(e));
       st = SD_EHIP;
@@ -500,25 +507,34 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
     }
     const int back = r - kLag;
     if (back >= 0) {
-      const int bs = back % (kLag + 1);
-      if (hipEventSynchronize(ev[bs]) != hipSuccess) {
+      if (hipEventSynchronize(ev[(back + 1) % kSlots]) != hipSuccess) {
         set_error("sd_run_sampler: event wait failed");
         st = SD_EHIP;
         break;
       }
-      if (host_act[bs] == 0) rounds = back + 1;
+      if (host_act[back % kSlots] == 0) rounds = back + 1;
     }
   }
   if (st == SD_OK && rounds < 0) {
-    for (int back = r - kLag < 0 ? 0 : r - kLag; back < r; ++back) {
-      const int bs = back % (kLag + 1);
-      (void)hipEventSynchronize(ev[bs]);
-      if (host_act[bs] == 0) {
+    // the flags of the last kLag launched rounds; the last one has no later
+    // scan to publish it, so it is copied
+    const int first = r - kLag < 0 ? 0 : r - kLag;
+    if (r >= 1) {
+      const int last = r - 1;
+      if (hipMemcpyAsync(&host_act[last % kSlots], act + ((last & 1) ^ 1), sizeof(int32_t),
+                         hipMemcpyDeviceToHost, s) != hipSuccess ||
+          hipStreamSynchronize(s) != hipSuccess) {
+        set_error("sd_run_sampler: flag copy failed");
+        st = SD_EHIP;
+      }
+    }
+    for (int back = first; st == SD_OK && back < r; ++back) {
+      if (host_act[back % kSlots] == 0) {
         rounds = back + 1;
         break;
       }
     }
-    if (rounds < 0) {
+    if (st == SD_OK && rounds < 0) {
       set_error("sd_run_sampler: chains still active after %d rounds", r);
       st = SD_EHIP;
     }
@@ -554,7 +570,7 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
     }
   }
   (void)hipStreamSynchronize(s);
-  for (int i = 0; i <= kLag; ++i) (void)hipEventDestroy(ev[i]);
+  for (int i = 0; i < kSlots; ++i) (void)hipEventDestroy(ev[i]);
   (void)hipHostFree(host_act);
   return st;
 }

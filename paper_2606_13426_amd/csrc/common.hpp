@@ -116,7 +116,7 @@ hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, co
                              int nct, const double* sigma, const int32_t* kcur,
                              const uint32_t* rcur, uint64_t seed, int32_t* tau, int32_t* rmode,
                              float* rcoef, float* rsig, int* nanflag, int* act_next,
-                             hipStream_t s, const int* gate);
+                             int* host_prev, hipStream_t s, const int* gate);
 // Residual, commit and the next round's Free-Drafter block, elementwise over
 // (chain, four coordinates); per-chain state is read from the *cur arrays and
 // written to the *next arrays (round parity), so no workgroup races another.

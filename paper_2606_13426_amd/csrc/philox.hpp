@@ -53,22 +53,25 @@ __device__ __forceinline__ double uniform64(uint32_t w) {
 // without losing the small-radius tail.  For u < 1/2, u is exact in float32.
 // For u >= 1/2, t = 1 - u = (2^24 - 1 - m + 0.5) 2^-24 is exact, w = fl(1 - t)
 // and ln u = ln w + (u - w)/w with u - w = -((w - 1) + t) exact, so one logf
-// serves both halves (no divergent branch).
+// serves both halves (no divergent branch).  The correction is below one ulp
+// of ln w, so the hardware reciprocal (about 1 ulp) is exact enough for it.
 __device__ __forceinline__ float neg2log_u24(uint32_t w) {
   const uint32_t m = w >> 8;
   const bool hi = m >= (1u << 23);
   const float t = ((float)((1u << 24) - 1u - m) + 0.5f) * 0x1p-24f;
   const float wv = hi ? 1.0f - t : ((float)m + 0.5f) * 0x1p-24f;
-  const float corr = hi ? -((wv - 1.0f) + t) / wv : 0.0f;
+  const float corr = hi ? -((wv - 1.0f) + t) * __builtin_amdgcn_rcpf(wv) : 0.0f;
   return -2.0f * (logf(wv) + corr);
 }
 
 // Box-Muller on (w0, w1) and (w2, w3): radius sqrt(-2 ln u_a), angle 2 pi u_b.
 // The hardware sine and cosine take their argument in revolutions, so they
-// evaluate sin(2 pi u_b), cos(2 pi u_b) directly on u_b in (0, 1).
+// evaluate sin(2 pi u_b), cos(2 pi u_b) directly on u_b in (0, 1); the radius
+// uses the hardware square root (about 1 ulp; the argument is a normal
+// float32 of at most 2 ln 2^25, so no range scaling is needed).
 __device__ __forceinline__ float4 normals4(uint4 w) {
-  const float ra = sqrtf(neg2log_u24(w.x));
-  const float rc = sqrtf(neg2log_u24(w.z));
+  const float ra = __builtin_amdgcn_sqrtf(neg2log_u24(w.x));
+  const float rc = __builtin_amdgcn_sqrtf(neg2log_u24(w.z));
   const float ub = ((float)(w.y >> 8) + 0.5f) * 0x1p-24f;
   const float ud = ((float)(w.w >> 8) + 0.5f) * 0x1p-24f;
   return make_float4(ra * __builtin_amdgcn_cosf(ub), ra * __builtin_amdgcn_sinf(ub),

@@ -247,15 +247,24 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(
 //   rmode 1: y = m^q + sigma G + rcoef (m^p - m^q),  rcoef = (U - e.G)/||Delta||
 //   rmode 2: y = m^q_{K_b} + sigma xi'  (full accept, target draw)
 //   rmode 3: y = yhat_{K_b}             (full accept that reaches step N)
-// It also clears the next round's active flag before looking at its gate.
+// It also clears the next round's active flag before looking at its gate,
+// and copies the gate (whether any chain was still active after the previous
+// round) to host_prev, a flag in mapped host memory that the host polls, so
+// that no separate device-to-host copy is queued per round.
 __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
     int B, int K, int d, int N, int mode, int umode, const double* __restrict__ lrp, int nct,
     const double* __restrict__ sigma, const int32_t* __restrict__ kcur,
     const uint32_t* __restrict__ rcur, uint64_t seed, int32_t* __restrict__ tau,
     int32_t* __restrict__ rmode,
     float* __restrict__ rcoef, float* __restrict__ rsig, int* nanflag, int* act_next,
-    const int* gate) {
-  if (blockIdx.x == 0 && threadIdx.x == 0) *act_next = 0;
+    int* host_prev, const int* gate) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    *act_next = 0;
+    if (host_prev) {
+      *host_prev = gate ? *gate : 1;
+      __threadfence_system();
+    }
+  }
   if (gate && *gate == 0) return;
   const int lane = threadIdx.x & 63;
   const int b = blockIdx.x * (kThreads / 64) + (threadIdx.x >> 6);
@@ -370,12 +379,12 @@ hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, co
                              int nct, const double* sigma, const int32_t* kcur,
                              const uint32_t* rcur, uint64_t seed, int32_t* tau, int32_t* rmode,
                              float* rcoef, float* rsig, int* nanflag, int* act_next,
-                             hipStream_t s, const int* gate) {
+                             int* host_prev, hipStream_t s, const int* gate) {
   const int per = kThreads / 64;
   return timed("scan_fused", s, [&] {
     scan_fused_kernel<<<(B + per - 1) / per, kThreads, 0, s>>>(
         B, K, d, N, mode, umode, lrp, nct, sigma, kcur, rcur, seed, tau, rmode, rcoef, rsig,
-        nanflag, act_next, gate);
+        nanflag, act_next, host_prev, gate);
   });
 }
 
