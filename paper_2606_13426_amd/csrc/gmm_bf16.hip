@@ -13,6 +13,7 @@
 #include "bufio.hpp"
 #include "common.hpp"
 #include "gemm_bf16.hpp"
+#include "gemm_bf16_wide.hpp"
 #include "philox.hpp"
 #include "rows.hpp"
 #include "rowsum.hpp"
@@ -69,6 +70,62 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_logits_bf16_kernel(
     // the 16 threads that loaded a row are 16 consecutive lanes
 #pragma unroll
     for (int h = 0; h < 8; ++h) {
+      double t = sq[h];
+      t += __shfl_xor(t, 1);
+      t += __shfl_xor(t, 2);
+      t += __shfl_xor(t, 4);
+      t += __shfl_xor(t, 8);
+      const int row = r0 + (threadIdx.x >> 4) + 16 * h;
+      if ((threadIdx.x & 15) == 0 && row < R) xsq[(int64_t)s * R + row] = t;
+    }
+  }
+}
+
+// The logits GEMM on 256 x 256 tiles (one workgroup per compute unit), for
+// the aligned case: d a whole number of chunks, rows of X 16-byte aligned.
+// Grid and tile order as gmm_logits_bf16_kernel; the ||x||^2 partials come
+// from the column tile 0 workgroups.
+__global__ __launch_bounds__(bf16w::kThreads, 1) void gmm_logits_bf16_wide_kernel(
+    int R, int M, int d, const float* __restrict__ X, int64_t ldx,
+    const uint16_t* __restrict__ mu, int ksplit, float* __restrict__ part,
+    double* __restrict__ xsq, const int* gate) {
+  using namespace bf16w;
+  if (gate && *gate == 0) return;
+  __shared__ bf16w::OperandLds sm[2];
+  const int nct = gridDim.x, nrt = gridDim.y;
+  const int lin = xcd_tile(nct * nrt * gridDim.z);
+  const int ct = lin % nct, rt = (lin / nct) % nrt, s = lin / (nct * nrt);
+  const int r0 = rt * WT, c0 = ct * WT;
+  const int kbeg = s * ksplit, kend = min(d, kbeg + ksplit);
+  bf16w::f32x16 acc[4][4];
+  bf16w::zero(acc);
+  double sq[16];
+#pragma unroll
+  for (int h = 0; h < 16; ++h) sq[h] = 0.0;
+  const __amdgpu_buffer_rsrc_t va = bf16w::tile_view(X, ldx, R, r0);
+  const __amdgpu_buffer_rsrc_t vb = bf16w::tile_view(mu, (int64_t)d, M, c0);
+  const bool want_sq = ct == 0;
+  if (want_sq)
+    bf16w::tile<true, float>(sm, va, ldx, vb, d, kbeg, kend, acc, sq);
+  else
+    bf16w::tile<false, float>(sm, va, ldx, vb, d, kbeg, kend, acc, sq);
+  float* ps = part + (int64_t)s * R * M;
+#pragma unroll
+  for (int qb = 0; qb < 4; ++qb) {
+    const int col = c0 + bf16w::out_col(qb);
+    if (col >= M) continue;
+#pragma unroll
+    for (int qa = 0; qa < 4; ++qa)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = r0 + bf16w::out_row(qa, v);
+        if (row < R) ps[(int64_t)row * M + col] = acc[qa][qb][v];
+      }
+  }
+  if (want_sq) {
+    // the 16 threads that loaded a row are 16 consecutive lanes
+#pragma unroll
+    for (int h = 0; h < 16; ++h) {
       double t = sq[h];
       t += __shfl_xor(t, 1);
       t += __shfl_xor(t, 2);
@@ -408,22 +465,29 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
 
 struct Plan {
   int S, ksplit;
+  bool wide;  // the logits GEMM may run on 256 x 256 tiles (d a whole number of chunks)
   size_t off_part, off_xsq, off_p, off_rowc, total;
 };
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Split of the logits GEMM over d, chosen as in the float32 path for
-// 128 x 128 tiles.
+// Split of the logits GEMM over d, chosen as in the float32 path: the
+// chunks per split and the splits minimise (workgroups per slot, rounded up)
+// x (chunks per workgroup), over 256 slots of one 256 x 256 workgroup per
+// compute unit when d is a whole number of chunks, else over 512 slots of two
+// 128 x 128 workgroups per compute unit.
 Plan make_plan(const Target& t, int R) {
   Plan p{};
-  const int tiles = ((R + TM - 1) / TM) * ((t.M + TN - 1) / TN);
+  p.wide = t.d % KC == 0;
+  const int tm = p.wide ? bf16w::WT : TM, tn = p.wide ? bf16w::WT : TN;
+  const int slots = p.wide ? 256 : 512;
+  const int tiles = ((R + tm - 1) / tm) * ((t.M + tn - 1) / tn);
   const int nchunks = (t.d + KC - 1) / KC;
   int best_cost = 1 << 30, best_per = nchunks;
   for (int S = 1; S <= 8 && S <= nchunks; ++S) {
     const int per = (nchunks + S - 1) / S;
     const int splits = (nchunks + per - 1) / per;
-    const int cost = ((tiles * splits + 255) / 256) * per;
+    const int cost = ((tiles * splits + slots - 1) / slots) * per;
     if (cost < best_cost) {
       best_cost = cost;
       best_per = per;
@@ -465,8 +529,14 @@ hipError_t logits_and_softmax(const Target& t, const Plan& p, const Bufs& w, int
   dim3 g1((t.M + TN - 1) / TN, (R + TM - 1) / TM, p.S);
   // the buffer-load path: whole chunks of k and 32-bit offsets inside a tile
   const bool vec = vecx && t.d % KC == 0 && ldx < (int64_t)1 << 22 && t.d < 1 << 22;
+  const bool wide = vec && p.wide && ldx < (int64_t)1 << 21 && t.d < 1 << 21;
   hipError_t e = timed("gmm_logits_bf16", s, [&] {
-    if (vec)
+    if (wide)
+      gmm_logits_bf16_wide_kernel<<<dim3((t.M + bf16w::WT - 1) / bf16w::WT,
+                                         (R + bf16w::WT - 1) / bf16w::WT, p.S),
+                                    bf16w::kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu16, p.ksplit,
+                                                             w.part, w.xsq, gate);
+    else if (vec)
       gmm_logits_bf16_kernel<true><<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu16, p.ksplit,
                                                            w.part, w.xsq, gate);
     else
