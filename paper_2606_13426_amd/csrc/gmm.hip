@@ -17,6 +17,8 @@
 // MFMA s, so each lane reads its 32 k-values as eight 16-byte LDS reads.
 #include <vector>
 
+#include <type_traits>
+
 #include "bufio.hpp"
 #include "common.hpp"
 #include "philox.hpp"
@@ -303,6 +305,117 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_kernel(
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) rho += __shfl_xor(rho, o);
   if (lane == 0) {
+    const float4 cf = coef[n];
+    rowc[3 * (int64_t)row + 0] = cf.x;
+    rowc[3 * (int64_t)row + 1] = cf.y;
+    rowc[3 * (int64_t)row + 2] = (float)rho;
+  }
+}
+
+// The softmax for M % 4 == 0, M <= 4 G: a row is spread over G lanes (G a
+// power of two, 16 .. 256) with four consecutive components per lane, so
+// every per-component input is one 16-byte load per lane (one per split for
+// the logit partials) and a workgroup holds 256 / G rows.  Arithmetic as in
+// gmm_softmax_kernel; the max, the sum and rho are reduced over the G lanes
+// (shuffles within a wavefront, then LDS across the wavefronts of a row).
+template <int G>
+__device__ __forceinline__ double group_reduce(double v, bool is_max, double* red) {
+  constexpr int W = G < 64 ? G : 64;
+#pragma unroll
+  for (int o = W / 2; o > 0; o >>= 1) {
+    const double u = __shfl_xor(v, o);
+    v = is_max ? fmax(v, u) : v + u;
+  }
+  if constexpr (G > 64) {
+    constexpr int NW = G / 64;  // wavefronts per row (one row per workgroup)
+    const int w = threadIdx.x >> 6;
+    __syncthreads();  // the previous use of red is complete
+    if ((threadIdx.x & 63) == 0) red[w] = v;
+    __syncthreads();
+    v = red[0];
+#pragma unroll
+    for (int i = 1; i < NW; ++i) v = is_max ? fmax(v, red[i]) : v + red[i];
+  }
+  return v;
+}
+
+template <int G, class TP>
+__global__ __launch_bounds__(kThreads) void gmm_softmax_quad_kernel(
+    int R, int M, int d, int S, const float* __restrict__ part, const double* __restrict__ xsq,
+    const int32_t* __restrict__ step, Sched sc, const double2* __restrict__ ls,
+    const double* __restrict__ logw, const double* __restrict__ musq, const float4* __restrict__ coef,
+    TP* __restrict__ P, float* __restrict__ rowc, const int* gate) {
+  static_assert(G >= 16 && G <= kThreads && (G & (G - 1)) == 0, "G: a power of two in 16..256");
+  if (gate && *gate == 0) return;
+  __shared__ double red[kThreads / 64];
+  constexpr int RPW = kThreads / G;
+  const int gl = threadIdx.x % G;
+  const int row = blockIdx.x * RPW + (int)threadIdx.x / G;
+  const bool on = row < R;
+  const int rr = on ? row : R - 1;  // lanes of a missing row follow the last one (no stores)
+  const int m0 = 4 * gl;
+  const bool has = m0 < M;
+  const int mc = has ? m0 : 0;  // loads of lanes past M read component 0 (unused)
+  // the partials first (independent of the step), then the step's tables
+  double dot[4] = {0.0, 0.0, 0.0, 0.0};
+  for (int sp = 0; sp < S; ++sp) {
+    const float4 v = *reinterpret_cast<const float4*>(part + ((int64_t)sp * R + rr) * M + mc);
+    dot[0] += (double)v.x;
+    dot[1] += (double)v.y;
+    dot[2] += (double)v.z;
+    dot[3] += (double)v.w;
+  }
+  double xs = 0.0;
+  for (int sp = 0; sp < S; ++sp) xs += xsq[(int64_t)sp * R + rr];
+  const int n = step[rr];
+  const double a = sched_signal(sc, n), a2 = a * a, hd = 0.5 * (double)d;
+  const double2* lsn = ls + (int64_t)n * M + mc;
+  double2 t[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) t[c] = lsn[c];
+  const double2 w01 = *reinterpret_cast<const double2*>(logw + mc);
+  const double2 w23 = *reinterpret_cast<const double2*>(logw + mc + 2);
+  const double2 q01 = *reinterpret_cast<const double2*>(musq + mc);
+  const double2 q23 = *reinterpret_cast<const double2*>(musq + mc + 2);
+  const double lw[4] = {w01.x, w01.y, w23.x, w23.y}, mq2[4] = {q01.x, q01.y, q23.x, q23.y};
+  double lg[4];
+  double mx = -INFINITY;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    lg[c] = lw[c] - hd * t[c].x - 0.5 * (xs - 2.0 * a * dot[c] + a2 * mq2[c]) * t[c].y;
+    if (has) mx = fmax(mx, lg[c]);
+  }
+  mx = group_reduce<G>(mx, true, red);
+  float e[4];
+  float sum = 0.0f;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    e[c] = has ? __expf((float)(lg[c] - mx)) : 0.0f;
+    sum += e[c];
+  }
+  const double inv = 1.0 / group_reduce<G>((double)sum, false, red);
+  double rho = 0.0;
+  float pm[4];
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const double rm = (double)e[c] * inv;
+    pm[c] = (float)(rm * a * t[c].y);
+    rho += rm * t[c].y;
+  }
+  if (on && has) {
+    if constexpr (sizeof(TP) == 2) {
+      uint2 pk;
+      pk.x = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)pm[0]) |
+             ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)pm[1]) << 16);
+      pk.y = (uint32_t)__builtin_bit_cast(uint16_t, (__bf16)pm[2]) |
+             ((uint32_t)__builtin_bit_cast(uint16_t, (__bf16)pm[3]) << 16);
+      *reinterpret_cast<uint2*>(P + (int64_t)row * M + m0) = pk;
+    } else {
+      *reinterpret_cast<float4*>(P + (int64_t)row * M + m0) = make_float4(pm[0], pm[1], pm[2], pm[3]);
+    }
+  }
+  rho = group_reduce<G>(rho, false, red);
+  if (on && gl == 0) {
     const float4 cf = coef[n];
     rowc[3 * (int64_t)row + 0] = cf.x;
     rowc[3 * (int64_t)row + 1] = cf.y;
@@ -683,6 +796,32 @@ hipError_t gmm_softmax_launch(const Target& t, int R, int S, const float* part, 
       gmm_softmax_small_kernel<<<nbs, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc,
                                                         t.ls, t.logw, t.musq, t.coef,
                                                         static_cast<float*>(P), rowc, gate);
+    });
+  }
+  if (t.M % 4 == 0 && t.M <= 4 * kThreads) {
+    // G lanes per row: the smallest power of two >= M / 4, at least 16
+    int g = 16;
+    while (4 * g < t.M) g <<= 1;
+    const int nbq = (R + kThreads / g - 1) / (kThreads / g);
+    auto launch = [&](auto gtag) {
+      constexpr int GG = decltype(gtag)::value;
+      if (p_bf16)
+        gmm_softmax_quad_kernel<GG><<<nbq, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc,
+                                                             t.ls, t.logw, t.musq, t.coef,
+                                                             static_cast<uint16_t*>(P), rowc, gate);
+      else
+        gmm_softmax_quad_kernel<GG><<<nbq, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc,
+                                                             t.ls, t.logw, t.musq, t.coef,
+                                                             static_cast<float*>(P), rowc, gate);
+    };
+    return timed("gmm_softmax", s, [&] {
+      switch (g) {
+        case 16: launch(std::integral_constant<int, 16>{}); break;
+        case 32: launch(std::integral_constant<int, 32>{}); break;
+        case 64: launch(std::integral_constant<int, 64>{}); break;
+        case 128: launch(std::integral_constant<int, 128>{}); break;
+        default: launch(std::integral_constant<int, 256>{}); break;
+      }
     });
   }
   const int per = kThreads / 64;
