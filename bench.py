@@ -37,7 +37,7 @@ METRIC = "verified chain-steps/sec + mean accepted steps per block; % MFMA / HBM
 # sources whose digest (source_digest()) was recorded with them.
 MEASURED_TRAFFIC = {
     ("pixel3072", "gmm_mean_lr"): dict(bytes=(137.0 + 122.0) * 1e6,
-                                       sources="602518ae4561d73d4e5e8580bde67cf5747ab880"),
+                                       sources="9285c08f4cbd6e3e06ed5f1b0a7db5c3952a650d"),
 }
 
 
@@ -306,6 +306,8 @@ def main():
                          "kernel of known size for scaling the HBM byte counters) and exit")
     args = ap.parse_args()
     if args.calibrate_copy:
+        # also the achievable streaming rates of this machine: a read-plus-write
+        # copy and a write-only fill of 1 GiB, timed with events (after a warm-up)
         import torch
         n = (1 << 30) // 4
         src = torch.ones(n, dtype=torch.float32, device="cuda")
@@ -313,8 +315,20 @@ def main():
         for _ in range(6):
             dst.copy_(src)
         torch.cuda.synchronize()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        ev[0].record()
+        for _ in range(10):
+            dst.copy_(src)
+        ev[1].record()
+        for _ in range(10):
+            dst.fill_(2.0)
+        ev[2].record()
+        torch.cuda.synchronize()
+        copy_s = ev[0].elapsed_time(ev[1]) / 10 / 1e3
+        fill_s = ev[1].elapsed_time(ev[2]) / 10 / 1e3
         print(json.dumps(dict(calibrate_copy_bytes_read=4 * n, calibrate_copy_bytes_written=4 * n,
-                              copies=6)))
+                              copies=6, copy_us=copy_s * 1e6, copy_read_plus_write_GBs=8 * n / copy_s / 1e9,
+                              fill_us=fill_s * 1e6, fill_write_GBs=4 * n / fill_s / 1e9)))
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): chains are independent and "
