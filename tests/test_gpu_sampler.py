@@ -80,3 +80,30 @@ def test_pixel3072_first_chains_match_oracle():
             assert_rows_close(y[b][None], ref["y"][i][None], rtol=1e-3, what=f"Y_N chain {b}")
             same += 1
     assert same >= B - 1
+
+
+# (d, M, B, K, N, seed): K > N (every block ragged, the largest K), one chain
+# with K = 1, the aligned float32 path (M = 64, d a multiple of 64), ragged d
+# with M % 4 == 0, and M = 128 (two k-chunks in the mean GEMM, the
+# four-components-per-lane softmax)
+SMALL = [(5, 3, 7, 64, 40, 1), (8, 4, 1, 1, 30, 2), (128, 64, 20, 4, 30, 3),
+         (130, 12, 9, 7, 25, 4), (256, 128, 8, 3, 20, 5)]
+
+
+@pytest.mark.parametrize("d,M,B,K,N,seed", SMALL)
+def test_small_configs_match_oracle(d, M, B, K, N, seed):
+    from paper_2606_13426_amd.inputs import make_gmm
+    p = make_gmm(d, M, mu_std=1.0, var=(0.01, 0.2), dirichlet=1.0, seed=seed)
+    tgt = _lib.Target(_lib.schedule(N), p["mu"], p["var"], p["log_w"])
+    y, stats, trace = _lib.sd_run_sampler(tgt, B, K, seed, trace_rounds=N)
+    y, trace = y.cpu().numpy(), trace.cpu().numpy()
+    ref = osamp.run_sampler(GMM(p["mu"], p["var"], p["log_w"]), Schedule(N), B, K, seed)
+    assert stats["steps"] == B * N
+    for i, b in enumerate(ref["chains"]):
+        rec = ref["trace"][i]
+        if any(info["ties"] for info in rec):
+            continue
+        taus = [info["tau"] for info in rec]
+        assert list(trace[: len(taus), b]) == taus, (b, taus, list(trace[: len(taus) + 1, b]))
+        assert np.all(trace[len(taus):, b] == 0)
+        assert_rows_close(y[b][None], ref["y"][i][None], what=f"Y_N chain {b}")
