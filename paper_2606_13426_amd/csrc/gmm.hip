@@ -617,7 +617,27 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
       if (row >= R || cnt == 0) continue;
       st4(mq + (int64_t)row * d + col, cnt, false, qv);
     }
-    if (row < R && j < K1 - 1) {
+    if constexpr (VEC) {
+      // all four columns exist; every row is computed and kept only when it
+      // is a draft row of the block (a select, no branch: rows past R read
+      // zeros and their chain index stays inside sm.b and cscale)
+      const bool keep = row < R && j < K1 - 1;
+      const float4 gv = *reinterpret_cast<const float4*>(&sm.b[(b - b_first) * LDW + 4 * cg]);
+      const float c2s = c2 * cscale[b - b_first];
+      double a2 = 0.0, az = 0.0, ag = 0.0;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const float pe = draft_mean(c1, comp(x, e), c2s, comp(sv, e));  // m^p
+        const double dd = (double)pe - (double)comp(qv, e);
+        const double zz = (double)comp(y, e) - (double)pe;
+        a2 = fma(dd, dd, a2);
+        az = fma(zz, dd, az);
+        ag = fma((double)comp(gv, e), dd, ag);
+      }
+      s2[i] = keep ? a2 : 0.0;
+      sz[i] = keep ? az : 0.0;
+      sgd[i] = keep ? ag : 0.0;
+    } else if (row < R && j < K1 - 1) {
       const float4 gv = *reinterpret_cast<const float4*>(&sm.b[(b - b_first) * LDW + 4 * cg]);
       const float c2s = c2 * cscale[b - b_first];
 #pragma unroll

@@ -317,20 +317,26 @@ __device__ __forceinline__ void mean_lr_epilogue_vec(
                                     c1 * x.z + c2 * (ov.z - rho * x.z),
                                     c1 * x.w + c2 * (ov.w - rho * x.w));
       buf_st4(vq, (uint32_t)((lr * d + col) * 4), qv);
-      if (row < R && j < K1 - 1) {
-        const float4 sv = b == bl ? sl[p] : sh[p];
-        const float4 gv = *reinterpret_cast<const float4*>(&gz[(b - b_first) * LDO + 4 * cg]);
-        const float c2s = c2 * cscale[b - b_first];
+      // every row is computed and kept only when it is a draft row of the
+      // block (a select: rows past R read zeros and their chain index stays
+      // inside gz and cscale)
+      const bool keep = row < R && j < K1 - 1;
+      const float4 sv = b == bl ? sl[p] : sh[p];
+      const float4 gv = *reinterpret_cast<const float4*>(&gz[(b - b_first) * LDO + 4 * cg]);
+      const float c2s = c2 * cscale[b - b_first];
+      double a2 = 0.0, az = 0.0, ag = 0.0;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          const float pe = draft_mean(c1, comp(x, e), c2s, comp(sv, e));  // m^p
-          const double dd = (double)pe - (double)comp(qv, e);
-          const double zz = (double)comp(y, e) - (double)pe;
-          s2[i] = fma(dd, dd, s2[i]);
-          sz[i] = fma(zz, dd, sz[i]);
-          sgd[i] = fma((double)comp(gv, e), dd, sgd[i]);
-        }
+      for (int e = 0; e < 4; ++e) {
+        const float pe = draft_mean(c1, comp(x, e), c2s, comp(sv, e));  // m^p
+        const double dd = (double)pe - (double)comp(qv, e);
+        const double zz = (double)comp(y, e) - (double)pe;
+        a2 = fma(dd, dd, a2);
+        az = fma(zz, dd, az);
+        ag = fma((double)comp(gv, e), dd, ag);
       }
+      s2[i] = keep ? a2 : 0.0;
+      sz[i] = keep ? az : 0.0;
+      sgd[i] = keep ? ag : 0.0;
     }
     t2 += reduce_rows16<8>(s2, cg);
     tz += reduce_rows16<8>(sz, cg);
