@@ -319,7 +319,10 @@ __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
   s2 = __shfl(s2, src);
   sz = __shfl(sz, src);
   sgd = __shfl(sgd, src);
-  const double sg = valid ? sigma[(int64_t)b * K1 + lane] : 1.0;
+  // sigma of rows 0..K_b (lane j holds row j); the residual's sigma is taken
+  // from these lanes below instead of a second load
+  const double sgl = lane <= kb ? sigma[(int64_t)b * K1 + lane] : 1.0;
+  const double sg = valid ? sgl : 1.0;
   const double inv = 1.0 / (sg * sg);
   const double vn = valid ? sqrt(s2 * inv) : 0.0;
   const double ell = valid ? -sz * inv - 0.5 * s2 * inv : 0.0;
@@ -329,16 +332,16 @@ __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
   const int t = D.tau;
   int rm;
   float cf = 0.f, sgo = 0.f;
+  const double st = __shfl(sgl, t <= kb ? t - 1 : kb);
   if (t <= kb) {
     const double v = __shfl(vn, t - 1);
-    const double st = sigma[(int64_t)b * K1 + (t - 1)];
     const double eG = __shfl(sgd, t - 1) / (st * v);
     rm = 1;
     cf = (float)((D.U - eG) / v);
     sgo = (float)st;
   } else if (kb + 1 <= N - k) {
     rm = 2;
-    sgo = (float)sigma[(int64_t)b * K1 + kb];
+    sgo = (float)st;
   } else {
     rm = 3;
   }
