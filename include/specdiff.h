@@ -14,9 +14,12 @@
  *  - The caller owns all memory.  The library allocates device memory only in
  *    sd_target_create (freed by sd_target_destroy); everything else lives in
  *    caller buffers, including a caller workspace sized by the *_workspace query.
+ *    sd_run_sampler also holds, for the duration of the call, 16 bytes of
+ *    mapped pinned host memory and four HIP events.
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
- *    null stream).  Only sd_run_sampler reads results back (a 4-byte counter per
- *    round and its statistics).
+ *    null stream).  Only sd_run_sampler reads results back: a per-round "any
+ *    chain active" flag that its kernels store into the mapped host memory,
+ *    and the final statistics.
  *  - Arguments are validated before any HIP call: a bad argument returns
  *    SD_EINVAL, a HIP failure SD_EHIP; sd_last_error() then describes it (a
  *    thread-local string).  Outputs are undefined after an error.

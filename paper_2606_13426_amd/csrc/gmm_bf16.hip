@@ -1,15 +1,18 @@
 // Gaussian-mixture target with bf16 operands on the matrix cores (float32
 // accumulation), for the large configurations: the same three steps as the
 // float32 path (logits GEMM split over d, float64 softmax, mean GEMM with the
-// EM epilogue) on 128 x 128 tiles of v_mfma_f32_32x32x16_bf16.
+// EM epilogue) on tiles of v_mfma_f32_32x32x16_bf16.
 //   gmm_logits_bf16: S = X mu^T, X float32 rounded to bf16 on staging, mu bf16;
 //                    ||x||^2 in float64 from the unrounded float32 values;
-//   softmax:         the float32 path's kernel, writing P in bf16;
+//                    256 x 256 tiles (gemm_bf16_wide.hpp) when d is a whole
+//                    number of chunks and rows are aligned, else 128 x 128;
+//   softmax:         the float32 path's kernels, writing P in bf16;
 //   gmm_mean_bf16 / gmm_mean_lr_bf16: O = P mu (mu^T stored as bf16) and the
 //                    epilogue in float32, the latter with the verification
 //                    partial sums of the sampler (as the float32 path).
-// The 128 x 128 accumulator tile is handed to the epilogue through LDS in two
-// passes of 64 columns, each over the operand buffers' storage.
+// The mean GEMMs' 128 x 128 accumulator tile is handed to the epilogue
+// through LDS in two passes of 64 columns, each over the operand buffers'
+// storage.
 #include "bufio.hpp"
 #include "common.hpp"
 #include "gemm_bf16.hpp"
