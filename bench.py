@@ -292,6 +292,51 @@ def _dtype(name):
     return "bf16 GEMM operands, f32 accumulate and states" if WORKLOADS[name].get("precision") == "bf16" else "f32"
 
 
+# the denoiser GEMM shapes of the workloads (m x k @ k x n) and two square
+# references, run through the vendor library (torch.mm -> hipBLASLt / rocBLAS)
+LIBRARY_GEMMS = {
+    "bf16_square_8192": (8192, 8192, 8192, "bf16", None),
+    "bf16_latent16384_logits": (2304, 16384, 1024, "bf16", ("latent16384", "gmm_logits_bf16")),
+    "bf16_latent16384_mean": (2304, 1024, 16384, "bf16", ("latent16384", "gmm_mean_lr_bf16")),
+    "bf16_pixel12288_logits": (8704, 12288, 256, "bf16", ("pixel12288", "gmm_logits_bf16")),
+    "fp32_square_4096": (4096, 4096, 4096, "f32", None),
+    "fp32_pixel3072_logits": (9216, 3072, 64, "f32", ("pixel3072", "gmm_logits")),
+    "fp32_pixel3072_mean": (9216, 64, 3072, "f32", ("pixel3072", "gmm_mean_lr")),
+}
+
+
+def library_gemms(reps=20):
+    """The same products as plain library GEMMs (row-major, contiguous
+    operands, output written), timed with events: what the vendor library
+    reaches on these shapes.  The path's own kernels do more per launch (the
+    logits kernels also round x to bf16 or accumulate ||x||^2, the mean
+    kernels stream x and m^q and the verification sums)."""
+    import torch
+    out = {}
+    for name, (m, k, n, dt, ours) in LIBRARY_GEMMS.items():
+        dtype = torch.bfloat16 if dt == "bf16" else torch.float32
+        g = torch.Generator(device="cuda").manual_seed(0)
+        a = torch.randn(m, k, device="cuda", dtype=dtype, generator=g)
+        b = torch.randn(k, n, device="cuda", dtype=dtype, generator=g)
+        c = torch.empty(m, n, device="cuda", dtype=dtype)
+        for _ in range(3):
+            torch.mm(a, b, out=c)
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        torch.cuda.synchronize()
+        ev[0].record()
+        for _ in range(reps):
+            torch.mm(a, b, out=c)
+        ev[1].record()
+        torch.cuda.synchronize()
+        sec = ev[0].elapsed_time(ev[1]) / reps / 1e3
+        peak = (BF16_PEAK_TFLOPS if dt == "bf16" else FP32_PEAK_TFLOPS) * 1e12
+        out[name] = dict(m=m, k=k, n=n, dtype=dt, us=sec * 1e6, tflops=2 * m * k * n / sec / 1e12,
+                         frac=2 * m * k * n / sec / peak,
+                         path_kernel=None if ours is None else dict(workload=ours[0], kernel=ours[1]))
+        del a, b, c
+    return out
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
@@ -304,7 +349,13 @@ def main():
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of 1 GiB five times (the reference "
                          "kernel of known size for scaling the HBM byte counters) and exit")
+    ap.add_argument("--library-gemms", action="store_true",
+                    help="only time the workloads' denoiser GEMM shapes through the vendor library "
+                         "(torch.mm) and exit")
     args = ap.parse_args()
+    if args.library_gemms:
+        print(json.dumps(dict(library_gemms=library_gemms())))
+        return
     if args.calibrate_copy:
         # also the achievable streaming rates of this machine: a read-plus-write
         # copy and a write-only fill of 1 GiB, timed with events (after a warm-up)
@@ -372,6 +423,7 @@ def main():
                               kernels={k: dict(avg_us=v["avg_us"], bound=v.get("bound"), frac=v.get("frac"))
                                        for k, v in table2.items() if "avg_us" in v})
         line["other_workloads"] = others
+        line["library_gemms"] = library_gemms()
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_budget)
     print(json.dumps(line))
