@@ -24,6 +24,9 @@ Psi is evaluated in log space: log(alpha Phi(x) - Phi(x - v))
 with the log-CDF difference taken through erfcx in the left tail (App. A.2 asks
 for stable log-space primitives; the plain difference loses all digits there).
 
+The reflection residual (Alg. 4) of sample verification is here too:
+Y = m^q + sigma (I - 2 e e^T) Z with Z the rejected step's draft noise.
+
 Parity: pinned by trapezoid integration of the unnormalised density (the
 paper's own numerical method for its residual plots), KS tests of sampled
 U against Psi, and exactness of the sampled residual in d = 1, 2, 8.
@@ -101,6 +104,18 @@ def decomposition(delta, mq, sigma, U, G):
     G = np.asarray(G, dtype=np.float64)
     z_perp = G - e * np.dot(e, G)
     return np.asarray(mq, dtype=np.float64) + sigma * (U * e + z_perp)
+
+
+def reflection(delta, z, mq, sigma):
+    """Alg. 4 (the reflection residual of sample verification): e = Delta/||Delta||,
+    Z_r = (I - 2 e e^T) Z, Y = m^q + sigma Z_r, with Z the draft noise of the
+    rejected step.  It takes no alpha: it is exact with sample (token)
+    verification only (Sec. 4's impossibility result rules it out for blocks)."""
+    delta = np.asarray(delta, dtype=np.float64)
+    e = delta / np.linalg.norm(delta)
+    z = np.asarray(z, dtype=np.float64)
+    z_r = z - 2.0 * e * np.dot(e, z)
+    return np.asarray(mq, dtype=np.float64) + sigma * z_r
 
 
 def usample_uniform(seed, chain, rnd):

@@ -21,6 +21,12 @@ coins c_j = [eta_j < h_j], c_0 = 1, tau = 1 + max{j : c_j = 1},
 alpha_res = alpha_{tau-1}.  v_j is evaluated with log-CDF primitives and a
 stable log(1 - e^x) as App. A.2 recommends.
 
+Temperature (App. "Temperature", the tempered sample and block verification
+algorithms): with p, q given the covariance omega^2 I the log ratio becomes
+ell_j / omega^2, so both recursions above take ell_j / omega^2 in place of
+ell_j; h_j keeps the untempered ||Delta_{j+1}||, and alpha_res (block) is the
+tempered alpha_{tau-1}.  omega = 1 is the exact method; omega != 1 is lossy.
+
 Readings where the paper is silent (listed in the design notes):
   * alpha_j = 1 gives h_j = 1 (the 0/0 limit v/(v + 0) with v > 0, and the
     value the block acceptance takes when nothing has been lost yet);
@@ -118,16 +124,17 @@ def coin_uniforms(seed, chain, rnd, K):
     return np.array([philox.uniform_at(seed, chain, rnd, philox.TAG_COIN, 0, j) for j in range(K)])
 
 
-def block_verify(ell, nrm2, kb, eta):
-    """Alg. 6 for one chain.
+def block_verify(ell, nrm2, kb, eta, omega=1.0):
+    """Alg. 6 for one chain (with temperature omega: the tempered block verification).
 
     ell, nrm2: [>= kb] per-step ell_j and ||Delta_j||^2 (index j-1); eta: [>= kb].
     Returns dict(tau, log_alpha_res, log_alpha[kb], log_h[kb], coins[kb]).
     """
+    w2 = float(omega) * float(omega)
     log_alpha = np.empty(kb)
     acc = 0.0
     for j in range(kb):
-        acc = min(0.0, acc + float(ell[j]))
+        acc = min(0.0, acc + float(ell[j]) / w2)
         log_alpha[j] = acc
     log_h = np.empty(kb)
     for j in range(kb):
@@ -144,9 +151,11 @@ def block_verify(ell, nrm2, kb, eta):
                 log_h=log_h, coins=coins)
 
 
-def token_verify(ell, kb, eta):
-    """Alg. 2 for one chain: independent coins against min(1, ratio)."""
-    log_a = np.array([min(0.0, float(ell[j])) for j in range(kb)])
+def token_verify(ell, kb, eta, omega=1.0):
+    """Alg. 2 for one chain: independent coins against min(1, ratio) (the
+    ratio of the omega^2-covariance densities with temperature omega)."""
+    w2 = float(omega) * float(omega)
+    log_a = np.array([min(0.0, float(ell[j]) / w2) for j in range(kb)])
     coins = np.array([math.log(float(eta[j])) < log_a[j] for j in range(kb)])
     tau = kb + 1
     for j in range(kb):
