@@ -4,7 +4,9 @@
  * The library implements the parallel verification pass of speculative
  * diffusion sampling with block verification ("Accelerating Speculative
  * Diffusions via Block Verification"), driven by the paper's Free Drafter,
- * with a closed-form Gaussian-mixture target.
+ * with a closed-form Gaussian-mixture target; and the paper's alternatives:
+ * sample (token) verification, the reflection residual, the Frozen Drafter,
+ * temperature, and the plain Euler-Maruyama chain they are measured against.
  *
  * Conventions for every entry point:
  *  - Pointers are DEVICE pointers unless the comment says "host".
@@ -42,7 +44,7 @@
 extern "C" {
 #endif
 
-#define SD_ABI_VERSION 1
+#define SD_ABI_VERSION 2
 #define SD_MAX_BLOCK 64
 
 typedef enum {
@@ -57,6 +59,14 @@ typedef enum {
 typedef enum { SD_BLOCK = 0, SD_TOKEN = 1 } sd_verify_mode;           /* Alg. 6 / Alg. 2 */
 typedef enum { SD_FP32 = 0, SD_BF16 = 1 } sd_precision;               /* denoiser GEMMs  */
 typedef enum { SD_USAMPLE_EXACT = 0, SD_USAMPLE_PAPER = 1 } sd_usample_mode; /* Alg. 7 */
+/* The residual of a rejected draft: the Decomposition residual (Prop. 1,
+ * Alg. 5) or the reflection residual (Alg. 4), which is valid with sample
+ * (token) verification only (the impossibility proposition of Sec. 4). */
+typedef enum { SD_RESIDUAL_DECOMPOSITION = 0, SD_RESIDUAL_REFLECTION = 1 } sd_residual_kind;
+/* The drafter (Sec. 3.3, eq. frozen-draft-drift): FREE reuses the target score
+ * the previous round already computed; FROZEN calls the target once per round
+ * at the state Y_k and drafts with that score. */
+typedef enum { SD_DRAFTER_FREE = 0, SD_DRAFTER_FROZEN = 1 } sd_drafter;
 
 /* VP-SDE Euler-Maruyama chain (Sec. 2): beta(s) = beta_min + s (beta_max - beta_min),
  * t_n = n/N; m^q_n(y) = c1_n y + c2_n score(y), c1_n = 1 + beta_n/(2N),
@@ -119,7 +129,9 @@ sd_status sd_init_chains(int32_t B, int32_t d, uint64_t seed, float* y, sd_strea
  *   m^p_{i-1} = c1_n yhat_{i-1} + c2_n cache_score[b],  yhat_i = m^p_{i-1} + sigma_n xi_i
  * (xi_i: DRAFT stream, slot i, round round[b]).  Writes x rows 0..K (row 0 = y[b],
  * rows K_b+1..K repeat yhat_{K_b}) and mp rows 0..K-1 (rows >= K_b repeat the last
- * mean).  Chains with k[b] >= N are left untouched.
+ * mean).  Chains with k[b] >= N are left untouched.  With cache_score = the
+ * target score at (y, k) (sd_target_mean's score output) this is the Frozen
+ * Drafter's block.
  * y, cache_score: [B][d] contiguous; x: [B][K+1][d] view; mp: [B][K][d] view. */
 sd_status sd_draft_block(const sd_schedule* sched, int32_t B, int32_t K, int32_t d,
                          const float* y, const float* cache_score, const int32_t* k,
@@ -154,6 +166,25 @@ sd_status sd_verify_block(int32_t B, int32_t K, int32_t d, sd_verify_mode mode,
                           int32_t* tau, double* log_alpha_res, double* u_res, double* delta_norm,
                           double* log_ratio, uint64_t* coins, sd_stream stream);
 
+/* sd_verify_block with temperature omega > 0 (App. "Temperature": the
+ * tempered sample and block verification algorithms): p and q get the
+ * covariance omega^2 sigma^2 I in the acceptance only, so every ell_j above
+ * becomes ell_j / omega^2 (log alpha_j, the token threshold and the block
+ * recursion), h_j keeps the untempered ||Delta_{j+1}||, log_alpha_res is the
+ * tempered log alpha_{tau-1} (block) or 0 (token), and U is drawn for that
+ * alpha_res and the untempered ||Delta_tau||.  log_ratio and delta_norm are
+ * the untempered ell_j and ||Delta_j||.  omega = 1 is sd_verify_block; any
+ * other value is lossy (the output no longer follows the target).  A
+ * non-positive or non-finite omega returns SD_EINVAL. */
+sd_status sd_verify_block_tempered(int32_t B, int32_t K, int32_t d, sd_verify_mode mode,
+                                   double omega, const float* y_draft, sd_stride ys,
+                                   const float* mp, sd_stride mps, const float* mq,
+                                   sd_stride mqs, const double* sigma, const int32_t* kb,
+                                   const uint32_t* round, uint64_t seed,
+                                   sd_usample_mode usample_mode, int32_t* tau,
+                                   double* log_alpha_res, double* u_res, double* delta_norm,
+                                   double* log_ratio, uint64_t* coins, sd_stream stream);
+
 /* -------------------------------------------------------------- residual --
  * The new state Y_{k+tau} of each chain (Alg. 8, residual calculation):
  *  - tau <= K_b: Decomposition residual (Prop. 1, Alg. 5) with alpha = alpha_res:
@@ -171,6 +202,22 @@ sd_status sd_sample_residual(int32_t B, int32_t K, int32_t d, const float* y_dra
                              const int32_t* tau, const double* u_res, const double* delta_norm,
                              const uint32_t* round, uint64_t seed, float* y_out,
                              sd_stream stream);
+
+/* The reflection residual of sample verification (Alg. 4) for the chains
+ * that rejected at tau <= K_b: with Z = (y_draft_{tau-1} - mp_{tau-1}) /
+ * sigma_{tau-1} (the draft noise of the rejected step) and e = Delta_tau /
+ * ||Delta_tau||,
+ *     y = mq_{tau-1} + sigma_{tau-1} (I - 2 e e^T) Z,
+ * computed as y_draft_{tau-1} - c (mp - mq), c = 1 + 2 (D.W)/(D.D), D = mp -
+ * mq, W = y_draft - mp, with the two sums over d in float64.  The full-accept
+ * cases (tau = K_b + 1) are those of sd_sample_residual; no U and no RESID
+ * noise are used.  Same arguments and layouts as sd_sample_residual. */
+sd_status sd_sample_residual_reflection(int32_t B, int32_t K, int32_t d, const float* y_draft,
+                                        sd_stride ys, const float* mp, sd_stride mps,
+                                        const float* mq, sd_stride mqs, const double* sigma,
+                                        const int32_t* kb, const int32_t* steps_left,
+                                        const int32_t* tau, const uint32_t* round, uint64_t seed,
+                                        float* y_out, sd_stream stream);
 
 /* --------------------------------------------------------------- sampler --
  * The full speculative sampler (Alg. 8) with the Free Drafter: Y_0 ~ N(0, I),
@@ -194,6 +241,45 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
                          sd_usample_mode usample_mode, uint64_t seed, float* y_out,
                          int32_t* tau_trace, int32_t trace_rounds, sd_stats* stats, void* ws,
                          size_t ws_bytes, sd_stream stream);
+
+/* The sampler's variants (host struct, read during the call only):
+ *  mode, usample_mode   as in sd_run_sampler;
+ *  residual             DECOMPOSITION (Alg. 5) or REFLECTION (Alg. 4; needs
+ *                       mode == SD_TOKEN, else SD_EINVAL);
+ *  drafter              FREE (the default sampler) or FROZEN: every round
+ *                       first calls the target at (Y_k, k) and drafts with
+ *                       that score, so Delta_1 = 0 and one extra target call
+ *                       on B rows is made per round;
+ *  omega                temperature > 0 of the verification (see
+ *                       sd_verify_block_tempered); 1 is exact, other values
+ *                       are lossy. */
+typedef struct {
+  sd_verify_mode mode;
+  sd_usample_mode usample_mode;
+  sd_residual_kind residual;
+  sd_drafter drafter;
+  double omega;
+} sd_sampler_options;
+
+/* sd_run_sampler with options (sd_run_sampler is this call with DECOMPOSITION,
+ * FREE and omega = 1).  Same workspace (sd_sampler_workspace), outputs and
+ * errors. */
+sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
+                            const sd_sampler_options* options, uint64_t seed, float* y_out,
+                            int32_t* tau_trace, int32_t trace_rounds, sd_stats* stats, void* ws,
+                            size_t ws_bytes, sd_stream stream);
+
+/* ------------------------------------------------------------- plain EM --
+ * The plain Euler-Maruyama chain (Sec. 2), the non-speculative baseline whose
+ * law the sampler reproduces: Y_0 ~ N(0, I) (INIT stream, as sd_run_sampler)
+ * and for n = 0..N-1
+ *     Y_{n+1} = m^q_n(Y_n) + sigma_n xi_n,   xi_n: TARGET stream, round n, slot 1,
+ * one target call on B rows per step.  y_out [B][d] holds the state during
+ * the call and Y_N at the end.  ws: >= sd_plain_em_workspace bytes, 256-byte
+ * aligned. */
+size_t sd_plain_em_workspace(sd_target target, int32_t B);
+sd_status sd_run_plain_em(sd_target target, int32_t B, uint64_t seed, float* y_out, void* ws,
+                          size_t ws_bytes, sd_stream stream);
 
 /* ------------------------------------------------------------- profiling --
  * Per-kernel timing with HIP events recorded around every launch on the

@@ -15,6 +15,8 @@ SD_OK, SD_EINVAL, SD_EHIP, SD_EUNSUPPORTED, SD_ENOMEM, SD_ENUMERIC = 0, -1, -2, 
 SD_BLOCK, SD_TOKEN = 0, 1
 SD_FP32, SD_BF16 = 0, 1
 SD_USAMPLE_EXACT, SD_USAMPLE_PAPER = 0, 1
+SD_RESIDUAL_DECOMPOSITION, SD_RESIDUAL_REFLECTION = 0, 1
+SD_DRAFTER_FREE, SD_DRAFTER_FROZEN = 0, 1
 SD_MAX_BLOCK = 64
 TAG_INIT, TAG_DRAFT, TAG_COIN, TAG_USAMPLE, TAG_RESID, TAG_TARGET = 1, 2, 3, 4, 5, 6
 
@@ -34,6 +36,11 @@ class sd_stride(ctypes.Structure):
 class sd_stats(ctypes.Structure):
     _fields_ = [("rounds", c_int64), ("chain_rounds", c_int64), ("steps", c_int64),
                 ("tau_hist", c_int64 * (SD_MAX_BLOCK + 2))]
+
+
+class sd_sampler_options(ctypes.Structure):
+    _fields_ = [("mode", c_int32), ("usample_mode", c_int32), ("residual", c_int32),
+                ("drafter", c_int32), ("omega", c_double)]
 
 
 class sd_kernel_stat(ctypes.Structure):
@@ -63,11 +70,19 @@ SIGNATURES = [
                                  c_uint64, P, S, P, S, P]),
     ("sd_verify_block", c_int32, [c_int32, c_int32, c_int32, c_int32, P, S, P, S, P, S, P, P, P,
                                   c_uint64, c_int32, P, P, P, P, P, P, P]),
+    ("sd_verify_block_tempered", c_int32, [c_int32, c_int32, c_int32, c_int32, c_double, P, S, P, S, P,
+                                           S, P, P, P, c_uint64, c_int32, P, P, P, P, P, P, P]),
     ("sd_sample_residual", c_int32, [c_int32, c_int32, c_int32, P, S, P, S, P, S, P, P, P, P, P, P, P,
                                      c_uint64, P, P]),
+    ("sd_sample_residual_reflection", c_int32, [c_int32, c_int32, c_int32, P, S, P, S, P, S, P, P, P, P,
+                                                P, c_uint64, P, P]),
     ("sd_sampler_workspace", c_size_t, [P, c_int32, c_int32]),
     ("sd_run_sampler", c_int32, [P, c_int32, c_int32, c_int32, c_int32, c_uint64, P, P, c_int32,
                                  ctypes.POINTER(sd_stats), P, c_size_t, P]),
+    ("sd_run_sampler_ex", c_int32, [P, c_int32, c_int32, ctypes.POINTER(sd_sampler_options), c_uint64, P,
+                                    P, c_int32, ctypes.POINTER(sd_stats), P, c_size_t, P]),
+    ("sd_plain_em_workspace", c_size_t, [P, c_int32]),
+    ("sd_run_plain_em", c_int32, [P, c_int32, c_uint64, P, P, c_size_t, P]),
     ("sd_profile_enable", c_int32, [c_int32]),
     ("sd_profile_only", c_int32, [c_char_p]),
     ("sd_profile_read", c_int32, [ctypes.POINTER(sd_kernel_stat), c_int32, ctypes.POINTER(c_int32)]),
@@ -190,27 +205,45 @@ def sd_draft_block(sched, y, cache_score, k, rnd, seed, x, mp):
            "sd_draft_block")
 
 
+def _verify_out(B, K, dev):
+    import torch
+    return dict(tau=torch.empty(B, dtype=torch.int32, device=dev),
+                log_alpha_res=torch.empty(B, dtype=torch.float64, device=dev),
+                u_res=torch.empty(B, dtype=torch.float64, device=dev),
+                delta_norm=torch.empty(B, K, dtype=torch.float64, device=dev),
+                log_ratio=torch.empty(B, K, dtype=torch.float64, device=dev),
+                coins=torch.empty(B, dtype=torch.int64, device=dev))
+
+
 def sd_verify_block(y_draft, mp, mq, sigma, kb, rnd, seed, mode=SD_BLOCK, usample_mode=SD_USAMPLE_EXACT,
                     out=None):
     """Views [B][K][d] (mq: [B][>=K][d]); sigma [B][K+1] float64; kb, rnd [B] int32.
 
     Returns dict of device tensors tau, log_alpha_res, u_res, delta_norm, log_ratio, coins.
     """
-    import torch
     B, K, d = y_draft.shape
-    dev = y_draft.device
     if out is None:
-        out = dict(tau=torch.empty(B, dtype=torch.int32, device=dev),
-                   log_alpha_res=torch.empty(B, dtype=torch.float64, device=dev),
-                   u_res=torch.empty(B, dtype=torch.float64, device=dev),
-                   delta_norm=torch.empty(B, K, dtype=torch.float64, device=dev),
-                   log_ratio=torch.empty(B, K, dtype=torch.float64, device=dev),
-                   coins=torch.empty(B, dtype=torch.int64, device=dev))
+        out = _verify_out(B, K, y_draft.device)
     _check(load().sd_verify_block(B, K, d, mode, _p(y_draft), stride3(y_draft), _p(mp), stride3(mp),
                                   _p(mq), stride3(mq), _p(sigma), _p(kb), _p(rnd), seed, usample_mode,
                                   _p(out["tau"]), _p(out["log_alpha_res"]), _p(out["u_res"]),
                                   _p(out["delta_norm"]), _p(out["log_ratio"]), _p(out.get("coins")),
                                   _stream()), "sd_verify_block")
+    return out
+
+
+def sd_verify_block_tempered(y_draft, mp, mq, sigma, kb, rnd, seed, omega, mode=SD_BLOCK,
+                             usample_mode=SD_USAMPLE_EXACT, out=None):
+    """sd_verify_block with temperature omega (same arguments and outputs)."""
+    B, K, d = y_draft.shape
+    if out is None:
+        out = _verify_out(B, K, y_draft.device)
+    _check(load().sd_verify_block_tempered(B, K, d, mode, float(omega), _p(y_draft), stride3(y_draft),
+                                           _p(mp), stride3(mp), _p(mq), stride3(mq), _p(sigma), _p(kb),
+                                           _p(rnd), seed, usample_mode, _p(out["tau"]),
+                                           _p(out["log_alpha_res"]), _p(out["u_res"]),
+                                           _p(out["delta_norm"]), _p(out["log_ratio"]),
+                                           _p(out.get("coins")), _stream()), "sd_verify_block_tempered")
     return out
 
 
@@ -222,8 +255,21 @@ def sd_sample_residual(y_draft, mp, mq, sigma, kb, steps_left, tau, u_res, delta
            "sd_sample_residual")
 
 
+def sd_sample_residual_reflection(y_draft, mp, mq, sigma, kb, steps_left, tau, rnd, seed, y_out):
+    B, K, d = y_draft.shape
+    _check(load().sd_sample_residual_reflection(B, K, d, _p(y_draft), stride3(y_draft), _p(mp),
+                                                stride3(mp), _p(mq), stride3(mq), _p(sigma), _p(kb),
+                                                _p(steps_left), _p(tau), _p(rnd), seed, _p(y_out),
+                                                _stream()), "sd_sample_residual_reflection")
+
+
 def sd_sampler_workspace(target, B, K):
     return load().sd_sampler_workspace(target.handle, B, K)
+
+
+def _stats_dict(st):
+    return dict(rounds=st.rounds, chain_rounds=st.chain_rounds, steps=st.steps,
+                tau_hist=[st.tau_hist[i] for i in range(SD_MAX_BLOCK + 2)])
 
 
 def sd_run_sampler(target, B, K, seed, mode=SD_BLOCK, usample_mode=SD_USAMPLE_EXACT, y_out=None,
@@ -239,9 +285,41 @@ def sd_run_sampler(target, B, K, seed, mode=SD_BLOCK, usample_mode=SD_USAMPLE_EX
     _check(load().sd_run_sampler(target.handle, B, K, mode, usample_mode, seed, _p(y_out), _p(trace),
                                  trace_rounds, ctypes.byref(st), _p(ws), ws.numel(), _stream()),
            "sd_run_sampler")
-    stats = dict(rounds=st.rounds, chain_rounds=st.chain_rounds, steps=st.steps,
-                 tau_hist=[st.tau_hist[i] for i in range(SD_MAX_BLOCK + 2)])
-    return y_out, stats, trace
+    return y_out, _stats_dict(st), trace
+
+
+def sd_run_sampler_ex(target, B, K, seed, mode=SD_BLOCK, usample_mode=SD_USAMPLE_EXACT,
+                      residual=SD_RESIDUAL_DECOMPOSITION, drafter=SD_DRAFTER_FREE, omega=1.0,
+                      y_out=None, trace_rounds=0, ws=None, device="cuda"):
+    """Alg. 8 with the sampler options (residual, drafter, temperature); returns as sd_run_sampler."""
+    import torch
+    if y_out is None:
+        y_out = torch.empty(B, target.d, dtype=torch.float32, device=device)
+    if ws is None:
+        ws = torch.empty(sd_sampler_workspace(target, B, K), dtype=torch.uint8, device=device)
+    trace = torch.zeros(trace_rounds, B, dtype=torch.int32, device=device) if trace_rounds > 0 else None
+    st = sd_stats()
+    opts = sd_sampler_options(mode, usample_mode, residual, drafter, float(omega))
+    _check(load().sd_run_sampler_ex(target.handle, B, K, ctypes.byref(opts), seed, _p(y_out), _p(trace),
+                                    trace_rounds, ctypes.byref(st), _p(ws), ws.numel(), _stream()),
+           "sd_run_sampler_ex")
+    return y_out, _stats_dict(st), trace
+
+
+def sd_plain_em_workspace(target, B):
+    return load().sd_plain_em_workspace(target.handle, B)
+
+
+def sd_run_plain_em(target, B, seed, y_out=None, ws=None, device="cuda"):
+    """The plain EM chain for B chains (N target calls); returns Y_N [B][d]."""
+    import torch
+    if y_out is None:
+        y_out = torch.empty(B, target.d, dtype=torch.float32, device=device)
+    if ws is None:
+        ws = torch.empty(sd_plain_em_workspace(target, B), dtype=torch.uint8, device=device)
+    _check(load().sd_run_plain_em(target.handle, B, seed, _p(y_out), _p(ws), ws.numel(), _stream()),
+           "sd_run_plain_em")
+    return y_out
 
 
 def sd_profile_enable(on=True):

@@ -4,6 +4,7 @@
 // scalar rcoef = (U - e.G)/||Delta||), every remaining step of the round is
 // elementwise in the coordinates:
 //   residual  y_i = m^q_i + sigma G_i + rcoef (m^p_i - m^q_i)     (Alg. 5 with e.G known)
+//             or y_i = yhat_tau,i - rcoef (m^p_i - m^q_i)          (Alg. 4, reflection)
 //             or the full-accept target draw, or the last draft at step N (Alg. 8);
 //   commit    k <- min(k + tau, N), round <- round + 1 (one thread per chain);
 //   draft     the next round's Free-Drafter block from y_i, whose cached score
@@ -16,6 +17,9 @@
 // kernels and the state never leaves registers between them.  The draft means
 // m^p are not stored: where the residual needs one it is recomputed from the
 // draft state and the cache with draft_mean, bit for bit.
+// With the Frozen Drafter the next draft needs a target call at the new state
+// first, so the kernel stops after writing the state into x row 0 and points
+// the next cache at that row and step.
 #include "common.hpp"
 #include "philox.hpp"
 #include "rows.hpp"
@@ -36,7 +40,7 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
     const float* __restrict__ MQ, float* __restrict__ y, int32_t* __restrict__ step,
     double* __restrict__ sigma, int32_t* __restrict__ hist, int64_t* __restrict__ steps,
     int* act_next, int32_t* __restrict__ trace, int r_round, int trace_rounds, bool vec_ok,
-    const int* gate) {
+    bool frozen, const int* gate) {
   if (gate && *gate == 0) return;
   const int N = sc.N, K1 = K + 1;
   const int b = blockIdx.y;
@@ -46,8 +50,8 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
   const bool active = t > 0;
   const int kb = active ? min(K, N - k) : 0;
   const int knew = active ? min(k + t, N) : k;
-  const int cr = min(t, kb);
-  const int cs = min(k + cr, N - 1);
+  const int cr = frozen ? 0 : min(t, kb);
+  const int cs = frozen ? min(knew, N - 1) : min(k + cr, N - 1);
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     if (active) {
       knext[b] = knew;
@@ -97,6 +101,21 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
       const float pv = draft_mean(cn.x, xv[c], c2s, sv[c]);
       yv[c] = qv[c] + sg * get4(z, c) + cf * (pv - qv[c]);
     }
+  } else if (rm == 4) {
+    // reflection: yhat_tau - rcoef (m^p - m^q) of row t - 1
+    float xv[4], xn[4], qv[4], sv[4];
+    load4(xb + (int64_t)(t - 1) * d, cnt, vec, xv);
+    load4(xb + (int64_t)t * d, cnt, vec, xn);
+    load4(qb + (int64_t)(t - 1) * d, cnt, vec, qv);
+    load4(sb, cnt, vec, sv);
+    const float4 cn = step_coef(sc, coef, k + t - 1);
+    const float c2s = cn.y * step_coef(sc, coef, cstep_cur[b]).w;
+    const float cf = rcoef[b];
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const float pv = draft_mean(cn.x, xv[c], c2s, sv[c]);
+      yv[c] = xn[c] - cf * (pv - qv[c]);
+    }
   } else if (rm == 2) {
     float qv[4];
     load4(qb + (int64_t)kb * d, cnt, vec, qv);
@@ -109,6 +128,10 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
   }
   store4(y + (int64_t)b * d + e0, cnt, vec, yv);
   if (knew >= N) return;
+  if (frozen) {
+    store4(xb, cnt, vec, yv);
+    return;
+  }
   float xcv[4], qcv[4], sv[4];
   load4(xb + (int64_t)cr * d, cnt, vec, xcv);
   load4(qb + (int64_t)cr * d, cnt, vec, qcv);
@@ -130,8 +153,8 @@ hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int
                           const int32_t* tau, const int32_t* rmode, const float* rcoef,
                           const float* rsig, float* x, float* sv, const float* mq, float* y,
                           int32_t* step, double* sigma, int32_t* hist, int64_t* steps,
-                          int* act_next, int32_t* trace, int r, int trace_rounds, hipStream_t s,
-                          const int* gate) {
+                          int* act_next, int32_t* trace, int r, int trace_rounds, bool frozen,
+                          hipStream_t s, const int* gate) {
   const int ng = (d + 3) / 4;
   dim3 grid((ng + kThreads - 1) / kThreads, B);
   const bool vec = (d % 4 == 0) && aligned16(x) && aligned16(sv) && aligned16(mq) && aligned16(y);
@@ -139,7 +162,8 @@ hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int
     advance_kernel<<<grid, kThreads, 0, s>>>(sc, coef, B, K, d, seed, kcur, rcur, crow_cur,
                                              cstep_cur, knext, rnext, crow_next, cstep_next, tau,
                                              rmode, rcoef, rsig, x, sv, mq, y, step, sigma, hist,
-                                             steps, act_next, trace, r, trace_rounds, vec, gate);
+                                             steps, act_next, trace, r, trace_rounds, vec,
+                                             frozen, gate);
   });
 }
 

@@ -5,6 +5,7 @@
 #include <stdio.h>
 #include <string.h>
 
+#include <algorithm>
 #include <map>
 #include <mutex>
 #include <string>
@@ -298,25 +299,51 @@ sd_status sd_draft_block(const sd_schedule* sched, int32_t B, int32_t K, int32_t
 }
 
 // ---------------------------------------------------------------- verify --
+static sd_status verify_impl(const char* fn, int32_t B, int32_t K, int32_t d, sd_verify_mode mode,
+                             double omega, const float* y_draft, sd_stride ys, const float* mp,
+                             sd_stride mps, const float* mq, sd_stride mqs, const double* sigma,
+                             const int32_t* kb, const uint32_t* round, uint64_t seed,
+                             sd_usample_mode usample_mode, int32_t* tau, double* log_alpha_res,
+                             double* u_res, double* delta_norm, double* log_ratio,
+                             uint64_t* coins, sd_stream stream) {
+  SD_CHECK_ARG(B >= 1 && d >= 1, "%s: need B >= 1 and d >= 1", fn);
+  SD_CHECK_ARG(K >= 1 && K <= SD_MAX_BLOCK, "%s: K = %d not in [1, %d]", fn, K, SD_MAX_BLOCK);
+  SD_CHECK_ARG(mode == SD_BLOCK || mode == SD_TOKEN, "%s: unknown mode", fn);
+  SD_CHECK_ARG(usample_mode == SD_USAMPLE_EXACT || usample_mode == SD_USAMPLE_PAPER, "%s: unknown usample mode", fn);
+  SD_CHECK_ARG(omega > 0.0 && isfinite(omega), "%s: omega must be positive and finite", fn);
+  SD_CHECK_ARG(y_draft && mp && mq && sigma && kb && round && tau && log_alpha_res && u_res &&
+                   delta_norm && log_ratio,
+               "%s: NULL pointer argument", fn);
+  SD_CHECK_ARG(stride_ok(ys, d, K) && stride_ok(mps, d, K) && stride_ok(mqs, d, K),
+               "%s: stride too small for [B][K][d]", fn);
+  SD_HIP(verify_launch(B, K, d, (int)mode, y_draft, ys, mp, mps, mq, mqs, sigma, kb, round, seed,
+                       (int)usample_mode, omega * omega, tau, log_alpha_res, u_res, delta_norm,
+                       log_ratio, coins, nullptr, (hipStream_t)stream, nullptr));
+  return SD_OK;
+}
+
 sd_status sd_verify_block(int32_t B, int32_t K, int32_t d, sd_verify_mode mode,
                           const float* y_draft, sd_stride ys, const float* mp, sd_stride mps,
                           const float* mq, sd_stride mqs, const double* sigma, const int32_t* kb,
                           const uint32_t* round, uint64_t seed, sd_usample_mode usample_mode,
                           int32_t* tau, double* log_alpha_res, double* u_res, double* delta_norm,
                           double* log_ratio, uint64_t* coins, sd_stream stream) {
-  SD_CHECK_ARG(B >= 1 && d >= 1, "sd_verify_block: need B >= 1 and d >= 1");
-  SD_CHECK_ARG(K >= 1 && K <= SD_MAX_BLOCK, "sd_verify_block: K = %d not in [1, %d]", K, SD_MAX_BLOCK);
-  SD_CHECK_ARG(mode == SD_BLOCK || mode == SD_TOKEN, "sd_verify_block: unknown mode");
-  SD_CHECK_ARG(usample_mode == SD_USAMPLE_EXACT || usample_mode == SD_USAMPLE_PAPER, "sd_verify_block: unknown usample mode");
-  SD_CHECK_ARG(y_draft && mp && mq && sigma && kb && round && tau && log_alpha_res && u_res &&
-                   delta_norm && log_ratio,
-               "sd_verify_block: NULL pointer argument");
-  SD_CHECK_ARG(stride_ok(ys, d, K) && stride_ok(mps, d, K) && stride_ok(mqs, d, K),
-               "sd_verify_block: stride too small for [B][K][d]");
-  SD_HIP(verify_launch(B, K, d, (int)mode, y_draft, ys, mp, mps, mq, mqs, sigma, kb, round, seed,
-                       (int)usample_mode, tau, log_alpha_res, u_res, delta_norm, log_ratio, coins,
-                       nullptr, (hipStream_t)stream, nullptr));
-  return SD_OK;
+  return verify_impl("sd_verify_block", B, K, d, mode, 1.0, y_draft, ys, mp, mps, mq, mqs, sigma,
+                     kb, round, seed, usample_mode, tau, log_alpha_res, u_res, delta_norm,
+                     log_ratio, coins, stream);
+}
+
+sd_status sd_verify_block_tempered(int32_t B, int32_t K, int32_t d, sd_verify_mode mode,
+                                   double omega, const float* y_draft, sd_stride ys,
+                                   const float* mp, sd_stride mps, const float* mq,
+                                   sd_stride mqs, const double* sigma, const int32_t* kb,
+                                   const uint32_t* round, uint64_t seed,
+                                   sd_usample_mode usample_mode, int32_t* tau,
+                                   double* log_alpha_res, double* u_res, double* delta_norm,
+                                   double* log_ratio, uint64_t* coins, sd_stream stream) {
+  return verify_impl("sd_verify_block_tempered", B, K, d, mode, omega, y_draft, ys, mp, mps, mq,
+                     mqs, sigma, kb, round, seed, usample_mode, tau, log_alpha_res, u_res,
+                     delta_norm, log_ratio, coins, stream);
 }
 
 // -------------------------------------------------------------- residual --
@@ -336,6 +363,24 @@ sd_status sd_sample_residual(int32_t B, int32_t K, int32_t d, const float* y_dra
                "sd_sample_residual: mq stride too small for [B][K+1][d]");
   SD_HIP(residual_launch(B, K, d, y_draft, ys, mp, mps, mq, mqs, sigma, kb, steps_left, tau,
                          u_res, delta_norm, round, seed, y_out, (hipStream_t)stream));
+  return SD_OK;
+}
+
+sd_status sd_sample_residual_reflection(int32_t B, int32_t K, int32_t d, const float* y_draft,
+                                        sd_stride ys, const float* mp, sd_stride mps,
+                                        const float* mq, sd_stride mqs, const double* sigma,
+                                        const int32_t* kb, const int32_t* steps_left,
+                                        const int32_t* tau, const uint32_t* round, uint64_t seed,
+                                        float* y_out, sd_stream stream) {
+  SD_CHECK_ARG(B >= 1 && d >= 1, "sd_sample_residual_reflection: need B >= 1 and d >= 1");
+  SD_CHECK_ARG(K >= 1 && K <= SD_MAX_BLOCK, "sd_sample_residual_reflection: K = %d not in [1, %d]", K, SD_MAX_BLOCK);
+  SD_CHECK_ARG(y_draft && mp && mq && sigma && kb && steps_left && tau && round && y_out,
+               "sd_sample_residual_reflection: NULL pointer argument");
+  SD_CHECK_ARG(stride_ok(ys, d, K) && stride_ok(mps, d, K), "sd_sample_residual_reflection: stride too small for [B][K][d]");
+  SD_CHECK_ARG(mqs.row >= d && mqs.chain >= (int64_t)(K + 1) * mqs.row,
+               "sd_sample_residual_reflection: mq stride too small for [B][K+1][d]");
+  SD_HIP(reflection_launch(B, K, d, y_draft, ys, mp, mps, mq, mqs, sigma, kb, steps_left, tau,
+                           round, seed, y_out, (hipStream_t)stream));
   return SD_OK;
 }
 
@@ -386,8 +431,10 @@ SamplerLayout sampler_layout(const Target& t, int B, int K) {
   L.dummy_i32 = take(4 * (Bs + 2));
   L.dummy_i64 = take(8 * (SD_MAX_BLOCK + 3));
   L.lrp = take(8 * 3 * Bs * K1 * (size_t)L.nct);
+  // the target calls on all B (K + 1) rows and, with the Frozen Drafter, on the
+  // B states alone (fewer rows may take more splits of the logits GEMM)
   const size_t rows = Bs * K1;
-  L.tws_bytes = target_ws_bytes(t, (int)rows);
+  L.tws_bytes = std::max(target_ws_bytes(t, (int)rows), target_ws_bytes(t, B));
   L.tws = take(L.tws_bytes);
   L.total = off;
   return L;
@@ -406,12 +453,34 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
                          sd_usample_mode usample_mode, uint64_t seed, float* y_out,
                          int32_t* tau_trace, int32_t trace_rounds, sd_stats* stats, void* ws,
                          size_t ws_bytes, sd_stream stream) {
+  const sd_sampler_options o{mode, usample_mode, SD_RESIDUAL_DECOMPOSITION, SD_DRAFTER_FREE, 1.0};
+  return sd_run_sampler_ex(target, B, K, &o, seed, y_out, tau_trace, trace_rounds, stats, ws,
+                           ws_bytes, stream);
+}
+
+sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
+                            const sd_sampler_options* opts, uint64_t seed, float* y_out,
+                            int32_t* tau_trace, int32_t trace_rounds, sd_stats* stats, void* ws,
+                            size_t ws_bytes, sd_stream stream) {
+  SD_CHECK_ARG(opts, "sd_run_sampler: options are NULL");
+  const sd_verify_mode mode = opts->mode;
+  const sd_usample_mode usample_mode = opts->usample_mode;
+  SD_CHECK_ARG(mode == SD_BLOCK || mode == SD_TOKEN, "sd_run_sampler: unknown mode");
+  SD_CHECK_ARG(usample_mode == SD_USAMPLE_EXACT || usample_mode == SD_USAMPLE_PAPER, "sd_run_sampler: unknown usample mode");
+  SD_CHECK_ARG(opts->residual == SD_RESIDUAL_DECOMPOSITION || opts->residual == SD_RESIDUAL_REFLECTION,
+               "sd_run_sampler: unknown residual");
+  SD_CHECK_ARG(opts->residual == SD_RESIDUAL_DECOMPOSITION || mode == SD_TOKEN,
+               "sd_run_sampler: the reflection residual needs sample (token) verification");
+  SD_CHECK_ARG(opts->drafter == SD_DRAFTER_FREE || opts->drafter == SD_DRAFTER_FROZEN,
+               "sd_run_sampler: unknown drafter");
+  SD_CHECK_ARG(opts->omega > 0.0 && isfinite(opts->omega), "sd_run_sampler: omega must be positive and finite");
   SD_CHECK_ARG(target, "sd_run_sampler: target is NULL");
   const Target& t = *reinterpret_cast<Target*>(target);
   SD_CHECK_ARG(B >= 1, "sd_run_sampler: B = %d < 1", B);
   SD_CHECK_ARG(K >= 1 && K <= SD_MAX_BLOCK, "sd_run_sampler: K = %d not in [1, %d]", K, SD_MAX_BLOCK);
-  SD_CHECK_ARG(mode == SD_BLOCK || mode == SD_TOKEN, "sd_run_sampler: unknown mode");
-  SD_CHECK_ARG(usample_mode == SD_USAMPLE_EXACT || usample_mode == SD_USAMPLE_PAPER, "sd_run_sampler: unknown usample mode");
+  const bool frozen = opts->drafter == SD_DRAFTER_FROZEN;
+  const bool reflect = opts->residual == SD_RESIDUAL_REFLECTION;
+  const double w2 = opts->omega * opts->omega;
   SD_CHECK_ARG(y_out && ws, "sd_run_sampler: y_out and ws must be non-NULL");
   SD_CHECK_ARG(!tau_trace || trace_rounds >= 0, "sd_run_sampler: trace_rounds < 0");
   SD_CHECK_ARG(((uintptr_t)ws & 255u) == 0, "sd_run_sampler: workspace must be 256-byte aligned");
@@ -439,7 +508,8 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
 
   // Y_0 (also row 0 of x); the one explicit target call at Y_0, whose mean
   // (row 0 of mq) seeds the Free Drafter's cached score; the round-0 rows'
-  // steps and sigmas; the first draft block.
+  // steps and sigmas; the first draft block.  The Frozen Drafter makes that
+  // call and draft at the start of every round instead.
   SD_HIP(fill_i32_launch(k2, 2 * (int64_t)B, 0, s));
   SD_HIP(fill_i32_launch(reinterpret_cast<int32_t*>(rnd2), 2 * (int64_t)B, 0, s));
   SD_HIP(fill_i32_launch(crow2, 2 * (int64_t)B, 0, s));
@@ -453,12 +523,14 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
   SD_HIP(fill_i32_launch(tau, B, 0, s));
   SD_HIP(fill_i32_launch(dummy, B + 2, 0, s));
   SD_HIP(init_chains_launch(B, d, seed, y, x, (int64_t)K1 * d, s));
-  SD_HIP(target_mean_launch(t, B, x, (int64_t)K1 * d, step, mq, (int64_t)K1 * d, nullptr, 0, tws,
-                            s, nullptr));
+  if (!frozen)
+    SD_HIP(target_mean_launch(t, B, x, (int64_t)K1 * d, step, mq, (int64_t)K1 * d, nullptr, 0,
+                              tws, s, nullptr));
   SD_HIP(prepare_launch(t.sc, B, K, k2, kb, left, step, sigma, tau, dummy, dummy + B,
                         dummy + B + 1, dummy64, dummy64 + SD_MAX_BLOCK + 2, s));
-  SD_HIP(draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2, cstep2, mq, mqs, k2, rnd2, seed, x,
-                             xs, sv, s, nullptr));
+  if (!frozen)
+    SD_HIP(draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2, cstep2, mq, mqs, k2, rnd2, seed,
+                               x, xs, sv, s, nullptr));
 
   // Round r's scan publishes round r - 1's active flag into slot (r - 1) of
   // a mapped host array; the host reads round r - kLag's flag once round
@@ -486,19 +558,30 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
   for (; r < max_rounds && rounds < 0; ++r) {
     const int cur = r & 1, nxt = cur ^ 1;
     const int* gate = act + cur;
-    hipError_t e = target_mean_lr_launch(t, B * K1, K1, x, step, mq, sv, cstep2 + cur * B, lrp,
-                                         rnd2 + cur * B, seed, tws, s, gate);
+    hipError_t e = hipSuccess;
+    if (frozen) {
+      // the Frozen Drafter's target call at (Y_k, k) into row 0 of m^q (the
+      // cache steps hold min(k, N - 1)), then the block drafted with that score
+      e = target_mean_launch(t, B, x, (int64_t)K1 * d, cstep2 + cur * B, mq, (int64_t)K1 * d,
+                             nullptr, 0, tws, s, gate);
+      if (e == hipSuccess)
+        e = draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2 + cur * B, cstep2 + cur * B, mq,
+                                mqs, k2 + cur * B, rnd2 + cur * B, seed, x, xs, sv, s, gate);
+    }
+    if (e == hipSuccess)
+      e = target_mean_lr_launch(t, B * K1, K1, x, step, mq, sv, cstep2 + cur * B, lrp,
+                                rnd2 + cur * B, seed, tws, s, gate);
     int32_t* publish = r >= 1 ? host_act_dev + (r - 1) % kSlots : nullptr;
     if (e == hipSuccess)
       e = scan_fused_launch(B, K, d, N, (int)mode, (int)usample_mode, lrp, L.nct, sigma,
-                            k2 + cur * B, rnd2 + cur * B, seed, tau, rmode, rcoef, rsig,
-                            nanflag, act + nxt, publish, s, gate);
+                            k2 + cur * B, rnd2 + cur * B, seed, w2, reflect, tau, rmode, rcoef,
+                            rsig, nanflag, act + nxt, publish, s, gate);
     if (e == hipSuccess)
       e = advance_launch(t.sc, t.coef, B, K, d, seed, k2 + cur * B, rnd2 + cur * B,
                          crow2 + cur * B, cstep2 + cur * B, k2 + nxt * B, rnd2 + nxt * B,
                          crow2 + nxt * B, cstep2 + nxt * B, tau, rmode, rcoef, rsig, x, sv, mq, y,
                          step, sigma, hist, steps, act + nxt, tau_trace, r,
-                         tau_trace ? trace_rounds : 0, s, gate);
+                         tau_trace ? trace_rounds : 0, frozen, s, gate);
     if (e == hipSuccess) e = hipEventRecord(ev[r % kSlots], s);
     if (e != hipSuccess) {
       set_error("sd_run_sampler: launch failed in round %d: %s", r, hipGetErrorString(e));
@@ -573,6 +656,40 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
   for (int i = 0; i < kSlots; ++i) (void)hipEventDestroy(ev[i]);
   (void)hipHostFree(host_act);
   return st;
+}
+
+// ------------------------------------------------------------- plain EM --
+static size_t em_ws_bytes(const Target& t, int B) {
+  return a256(sizeof(float) * (size_t)B * t.d) + a256(sizeof(int32_t) * (size_t)B) +
+         target_ws_bytes(t, B);
+}
+
+size_t sd_plain_em_workspace(sd_target target, int32_t B) {
+  if (!target || B < 1) return 0;
+  return em_ws_bytes(*reinterpret_cast<Target*>(target), B);
+}
+
+sd_status sd_run_plain_em(sd_target target, int32_t B, uint64_t seed, float* y_out, void* ws,
+                          size_t ws_bytes, sd_stream stream) {
+  SD_CHECK_ARG(target, "sd_run_plain_em: target is NULL");
+  const Target& t = *reinterpret_cast<Target*>(target);
+  SD_CHECK_ARG(B >= 1, "sd_run_plain_em: B = %d < 1", B);
+  SD_CHECK_ARG(y_out && ws, "sd_run_plain_em: y_out and ws must be non-NULL");
+  SD_CHECK_ARG(((uintptr_t)ws & 255u) == 0, "sd_run_plain_em: workspace must be 256-byte aligned");
+  SD_CHECK_ARG(ws_bytes >= em_ws_bytes(t, B), "sd_run_plain_em: workspace %zu < %zu bytes", ws_bytes, em_ws_bytes(t, B));
+  hipStream_t s = (hipStream_t)stream;
+  char* base = static_cast<char*>(ws);
+  float* mq = reinterpret_cast<float*>(base);
+  int32_t* step = reinterpret_cast<int32_t*>(base + a256(sizeof(float) * (size_t)B * t.d));
+  void* tws = base + a256(sizeof(float) * (size_t)B * t.d) + a256(sizeof(int32_t) * (size_t)B);
+  const int d = t.d;
+  SD_HIP(init_chains_launch(B, d, seed, y_out, nullptr, 0, s));
+  SD_HIP(fill_i32_launch(step, B, 0, s));
+  for (int n = 0; n < t.sc.N; ++n) {
+    SD_HIP(target_mean_launch(t, B, y_out, d, step, mq, d, nullptr, 0, tws, s, nullptr));
+    SD_HIP(em_noise_launch(B, d, n, (float)sched_sigma(t.sc, n), seed, mq, y_out, step, s));
+  }
+  return SD_OK;
 }
 
 // ------------------------------------------------------------- profiling --

@@ -112,14 +112,18 @@ hipError_t gmm_softmax_launch(const Target& t, int rows, int S, const float* par
                               const double* xsq, const int32_t* step, void* P, bool p_bf16,
                               float* rowc, hipStream_t s, const int* gate);
 // Sampler verification on the fused partials (see scan_fused_kernel).
+// w2 = omega^2 (temperature; 1 = exact); reflect: the reflection residual.
 hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, const double* lrp,
                              int nct, const double* sigma, const int32_t* kcur,
-                             const uint32_t* rcur, uint64_t seed, int32_t* tau, int32_t* rmode,
-                             float* rcoef, float* rsig, int* nanflag, int* act_next,
-                             int* host_prev, hipStream_t s, const int* gate);
+                             const uint32_t* rcur, uint64_t seed, double w2, bool reflect,
+                             int32_t* tau, int32_t* rmode, float* rcoef, float* rsig,
+                             int* nanflag, int* act_next, int* host_prev, hipStream_t s,
+                             const int* gate);
 // Residual, commit and the next round's Free-Drafter block, elementwise over
 // (chain, four coordinates); per-chain state is read from the *cur arrays and
 // written to the *next arrays (round parity), so no workgroup races another.
+// frozen: the Frozen Drafter drafts after its own target call, so the round
+// ends with the new state in x row 0 and the next cache at (row 0, step k).
 hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int d,
                           uint64_t seed, const int32_t* kcur, const uint32_t* rcur,
                           const int32_t* crow_cur, const int32_t* cstep_cur, int32_t* knext,
@@ -127,8 +131,8 @@ hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int
                           const int32_t* tau, const int32_t* rmode, const float* rcoef,
                           const float* rsig, float* x, float* sv, const float* mq, float* y,
                           int32_t* step, double* sigma, int32_t* hist, int64_t* steps,
-                          int* act_next, int32_t* trace, int r, int trace_rounds, hipStream_t s,
-                          const int* gate);
+                          int* act_next, int32_t* trace, int r, int trace_rounds, bool frozen,
+                          hipStream_t s, const int* gate);
 
 // ---------------------------------------------------------------- kernels --
 hipError_t init_chains_launch(int B, int d, uint64_t seed, float* y, float* x0, int64_t x0c,
@@ -148,14 +152,24 @@ hipError_t draft_cached_launch(const Sched& sc, const float4* coef, int B, int K
 hipError_t verify_launch(int B, int K, int d, int mode, const float* yd, sd_stride ys,
                          const float* mp, sd_stride mps, const float* mq, sd_stride mqs,
                          const double* sigma, const int32_t* kb, const uint32_t* rnd,
-                         uint64_t seed, int umode, int32_t* tau, double* lar, double* ures,
-                         double* dn, double* lr, uint64_t* coins, int* nanflag, hipStream_t s,
-                         const int* gate);
+                         uint64_t seed, int umode, double w2, int32_t* tau, double* lar,
+                         double* ures, double* dn, double* lr, uint64_t* coins, int* nanflag,
+                         hipStream_t s, const int* gate);
 hipError_t residual_launch(int B, int K, int d, const float* yd, sd_stride ys, const float* mp,
                            sd_stride mps, const float* mq, sd_stride mqs, const double* sigma,
                            const int32_t* kb, const int32_t* left, const int32_t* tau,
                            const double* ures, const double* dn, const uint32_t* rnd,
                            uint64_t seed, float* y, hipStream_t s);
+// The reflection residual (Alg. 4) for rejected chains, the same full-accept
+// cases as residual_launch otherwise.
+hipError_t reflection_launch(int B, int K, int d, const float* yd, sd_stride ys, const float* mp,
+                             sd_stride mps, const float* mq, sd_stride mqs, const double* sigma,
+                             const int32_t* kb, const int32_t* left, const int32_t* tau,
+                             const uint32_t* rnd, uint64_t seed, float* y, hipStream_t s);
+// One plain Euler-Maruyama step on B rows: y = mq + sigma_n xi (TARGET
+// stream, round n, slot 1), and step[b] = n + 1 for the next target call.
+hipError_t em_noise_launch(int B, int d, int n, float sigma_n, uint64_t seed, const float* mq,
+                           float* y, int32_t* step, hipStream_t s);
 // Sampler-only kernels.
 hipError_t residual_commit_launch(int B, int K, int d, int N, const float* yd, sd_stride ys,
                                   const float* mp, sd_stride mps, const float* mq, sd_stride mqs,

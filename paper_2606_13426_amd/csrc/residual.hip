@@ -8,6 +8,12 @@
 // c = (U - e.G)/||Delta||, so one float64 reduction (e.G) followed by one
 // elementwise pass suffices; G and the two rows stay in registers between the
 // passes (up to 512 threads x 4 groups of 4 coordinates).
+//
+// The reflection residual of sample verification (Alg. 4),
+//     y = m^q + sigma (I - 2 e e^T) Z,  Z = (yhat_tau - m^p) / sigma,
+// is with D = m^p - m^q and W = yhat_tau - m^p
+//     y_i = yhat_i - c D_i,  c = 1 + 2 (D.W) / (D.D),
+// two float64 reductions and one elementwise pass (reflection_row).
 #include "common.hpp"
 #include "philox.hpp"
 
@@ -91,6 +97,62 @@ __device__ void decomposition_row(int b, int d, uint32_t r, uint64_t seed, const
   }
 }
 
+// The reflection residual of one rejected chain: sums D.D and D.W over the
+// row in float64 (the thread's groups kept in registers up to kKeep), then
+// y = yhat - c D.
+__device__ void reflection_row(int d, const float* yh, const float* p, const float* q,
+                               float* out, double* red) {
+  const int ng = (d + 3) / 4;
+  const int nt = blockDim.x;
+  float gy[kKeep][4], gd[kKeep][4];
+  double a2 = 0.0, az = 0.0;
+#pragma unroll
+  for (int i = 0; i < kKeep; ++i) {
+    const int g = threadIdx.x + i * nt;
+    if (g < ng) {
+      const int e0 = 4 * g, cnt = min(4, d - e0);
+      float pv[4], qv[4];
+      ld4(yh + e0, cnt, gy[i]);
+      ld4(p + e0, cnt, pv);
+      ld4(q + e0, cnt, qv);
+#pragma unroll
+      for (int c = 0; c < 4; ++c) {
+        gd[i][c] = pv[c] - qv[c];
+        const double dd = (double)pv[c] - (double)qv[c];
+        const double ww = (double)gy[i][c] - (double)pv[c];
+        a2 = fma(dd, dd, a2);  // zero-padded lanes add zeros
+        az = fma(ww, dd, az);
+      }
+    }
+  }
+  for (int g = threadIdx.x + kKeep * nt; g < ng; g += nt) {
+    const int e0 = 4 * g, cnt = min(4, d - e0);
+    for (int c = 0; c < cnt; ++c) {
+      const double dd = (double)p[e0 + c] - (double)q[e0 + c];
+      a2 = fma(dd, dd, a2);
+      az = fma((double)yh[e0 + c] - (double)p[e0 + c], dd, az);
+    }
+  }
+  const double t2 = block_sum(a2, red);
+  __syncthreads();  // every thread has read red before it is reused
+  const double tz = block_sum(az, red);
+  const float cf = (float)(1.0 + 2.0 * tz / t2);  // t2 > 0 for a rejected step
+#pragma unroll
+  for (int i = 0; i < kKeep; ++i) {
+    const int g = threadIdx.x + i * nt;
+    if (g < ng) {
+      const int e0 = 4 * g, cnt = min(4, d - e0);
+#pragma unroll
+      for (int c = 0; c < 4; ++c)
+        if (c < cnt) out[e0 + c] = gy[i][c] - cf * gd[i][c];
+    }
+  }
+  for (int g = threadIdx.x + kKeep * nt; g < ng; g += nt) {
+    const int e0 = 4 * g, cnt = min(4, d - e0);
+    for (int c = 0; c < cnt; ++c) out[e0 + c] = yh[e0 + c] - cf * (p[e0 + c] - q[e0 + c]);
+  }
+}
+
 // With COMMIT (the sampler) the same workgroup then advances the chain:
 // k <- min(k + tau, N), round <- round + 1, and records where the Free Drafter
 // finds its cached score next round (row min(tau, K_b) of this round's target
@@ -103,7 +165,7 @@ __global__ __launch_bounds__(kMaxThreads) void residual_kernel(
     const int32_t* __restrict__ left, const int32_t* __restrict__ tauv,
     const double* __restrict__ ures, const double* __restrict__ dn, uint32_t* rnd, uint64_t seed,
     float* __restrict__ y, int32_t* kk, int32_t* crow, int32_t* cstep, int32_t* adv,
-    int32_t* trace, int r_round, int trace_rounds, const int* gate) {
+    int32_t* trace, int r_round, int trace_rounds, bool reflect, const int* gate) {
   __shared__ double red[kMaxThreads / 64];
   if (gate && *gate == 0) return;
   const int b = blockIdx.x;
@@ -117,7 +179,11 @@ __global__ __launch_bounds__(kMaxThreads) void residual_kernel(
   const uint32_t r = rnd[b];
   float* out = y + (int64_t)b * d;
   const int ng = (d + 3) / 4;
-  if (t <= kb) {
+  if (t <= kb && reflect) {
+    reflection_row(d, yd + (int64_t)b * yc + (int64_t)(t - 1) * yr,
+                   mp + (int64_t)b * pc + (int64_t)(t - 1) * pr,
+                   mq + (int64_t)b * qc + (int64_t)(t - 1) * qr, out, red);
+  } else if (t <= kb) {
     decomposition_row(b, d, r, seed, mp + (int64_t)b * pc + (int64_t)(t - 1) * pr,
                       mq + (int64_t)b * qc + (int64_t)(t - 1) * qr,
                       sigma[(int64_t)b * (K + 1) + (t - 1)], dn[(int64_t)b * K + (t - 1)], ures[b],
@@ -170,7 +236,19 @@ hipError_t residual_launch(int B, int K, int d, const float* yd, sd_stride ys, c
     residual_kernel<false><<<B, residual_threads(d), 0, s>>>(
         B, K, d, 0, yd, ys.chain, ys.row, mp, mps.chain, mps.row, mq, mqs.chain, mqs.row, sigma,
         kb, left, tau, ures, dn, const_cast<uint32_t*>(rnd), seed, y, nullptr, nullptr, nullptr,
-        nullptr, nullptr, 0, 0, nullptr);
+        nullptr, nullptr, 0, 0, false, nullptr);
+  });
+}
+
+hipError_t reflection_launch(int B, int K, int d, const float* yd, sd_stride ys, const float* mp,
+                             sd_stride mps, const float* mq, sd_stride mqs, const double* sigma,
+                             const int32_t* kb, const int32_t* left, const int32_t* tau,
+                             const uint32_t* rnd, uint64_t seed, float* y, hipStream_t s) {
+  return timed("residual_reflect", s, [&] {
+    residual_kernel<false><<<B, residual_threads(d), 0, s>>>(
+        B, K, d, 0, yd, ys.chain, ys.row, mp, mps.chain, mps.row, mq, mqs.chain, mqs.row, sigma,
+        kb, left, tau, nullptr, nullptr, const_cast<uint32_t*>(rnd), seed, y, nullptr, nullptr,
+        nullptr, nullptr, nullptr, 0, 0, true, nullptr);
   });
 }
 
@@ -184,7 +262,8 @@ hipError_t residual_commit_launch(int B, int K, int d, int N, const float* yd, s
   return timed("residual_commit", s, [&] {
     residual_kernel<true><<<B, residual_threads(d), 0, s>>>(
         B, K, d, N, yd, ys.chain, ys.row, mp, mps.chain, mps.row, mq, mqs.chain, mqs.row, sigma,
-        kb, left, tau, ures, dn, rnd, seed, y, k, crow, cstep, adv, trace, r, trace_rounds, gate);
+        kb, left, tau, ures, dn, rnd, seed, y, k, crow, cstep, adv, trace, r, trace_rounds, false,
+        gate);
   });
 }
 

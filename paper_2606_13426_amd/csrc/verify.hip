@@ -16,6 +16,11 @@
 // tests u* - 2^i), and the bisection becomes a 64-way multisection that
 // shrinks the bracket 65-fold per step until it is 1e-13 (relative) wide or
 // has collapsed in float64.
+//
+// Both scans take the temperature as w2 = omega^2 (the tempered
+// verifications of the appendix divide every ell_j by omega^2), and the
+// sampler's scan can hand the reflection residual (Alg. 4) to the next kernel
+// instead of the Decomposition residual, skipping the U draw.
 #include "common.hpp"
 #include "dmath.hpp"
 #include "philox.hpp"
@@ -154,16 +159,20 @@ __device__ double usample_paper(double u, double la, double v) {
 
 // The acceptance decision of one chain (one wavefront; lane j-1 holds ell_j
 // and ||Delta_j|| of draft step j, kb valid steps): prefix recursion, h_j,
-// coins, tau, alpha_res and, when tau <= kb, the U draw of Alg. 7.
+// coins, tau, alpha_res and, when tau <= kb and need_u, the U draw of Alg. 7.
+// Temperature omega (w2 = omega^2): the tempered verifications of the
+// appendix use ell_j / omega^2 wherever ell_j enters the acceptance, and the
+// untempered ||Delta||; w2 = 1 is the exact method.
 struct Decision {
   int tau;
   double la_res, U;
   uint64_t coins;
 };
 
-__device__ Decision decide(int mode, int umode, int kb, double ell, double vn, uint32_t b,
-                           uint32_t r, uint64_t seed, int lane) {
+__device__ Decision decide(int mode, int umode, int kb, double ell_raw, double vn, uint32_t b,
+                           uint32_t r, uint64_t seed, int lane, double w2, bool need_u) {
   const bool valid = lane < kb;
+  const double ell = ell_raw / w2;
   // prefix recursion, replayed per lane in the definition's order
   double acc = 0.0, la = 0.0;
   for (int i = 0; i < kb; ++i) {
@@ -191,7 +200,7 @@ __device__ Decision decide(int mode, int umode, int kb, double ell, double vn, u
   const double la_prev = __shfl(la, t >= 2 ? t - 2 : 0);
   const double la_res = (mode == SD_BLOCK && t >= 2) ? la_prev : 0.0;
   double U = NAN;
-  if (t <= kb) {
+  if (t <= kb && need_u) {
     const double v = __shfl(vn, t - 1);  // > 0: a rejection never lands on a zero offset
     const uint4 wu = philox(0u, b, r, TAG_USAMPLE << 24, seed);
     const double u = uniform64(wu.x);
@@ -209,7 +218,7 @@ __device__ Decision decide(int mode, int umode, int kb, double ell, double vn, u
 __global__ __launch_bounds__(kThreads) void scan_kernel(
     int B, int K, int mode, int umode, const double* __restrict__ dn,
     const double* __restrict__ lr, const int32_t* __restrict__ kbv,
-    const uint32_t* __restrict__ rnd, uint64_t seed, int32_t* __restrict__ tau,
+    const uint32_t* __restrict__ rnd, uint64_t seed, double w2, int32_t* __restrict__ tau,
     double* __restrict__ lar, double* __restrict__ ures, uint64_t* __restrict__ coins,
     int* nanflag, const int* gate) {
   if (gate && *gate == 0) return;
@@ -231,7 +240,7 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(
   const double vn = valid ? dn[(int64_t)b * K + lane] : 0.0;
   if (nanflag && __ballot(valid && !(isfinite(ell) && isfinite(vn))) != 0ull && lane == 0)
     atomicOr(nanflag, 1);
-  const Decision D = decide(mode, umode, kb, ell, vn, (uint32_t)b, rnd[b], seed, lane);
+  const Decision D = decide(mode, umode, kb, ell, vn, (uint32_t)b, rnd[b], seed, lane, w2, true);
   if (lane == 0) {
     tau[b] = D.tau;
     lar[b] = D.la_res;
@@ -247,6 +256,10 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(
 //   rmode 1: y = m^q + sigma G + rcoef (m^p - m^q),  rcoef = (U - e.G)/||Delta||
 //   rmode 2: y = m^q_{K_b} + sigma xi'  (full accept, target draw)
 //   rmode 3: y = yhat_{K_b}             (full accept that reaches step N)
+//   rmode 4: y = yhat_tau - rcoef (m^p - m^q),  rcoef = 1 + 2 D.W / D.D
+//            (reflection residual, Alg. 4: m^q + sigma (I - 2 e e^T) Z with
+//            D = m^p - m^q = sigma Delta and W = yhat_tau - m^p = sigma Z,
+//            whose two sums are the log-ratio partials of row tau - 1)
 // It also clears the next round's active flag before looking at its gate,
 // and copies the gate (whether any chain was still active after the previous
 // round) to host_prev, a flag in mapped host memory that the host polls, so
@@ -254,8 +267,8 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(
 __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
     int B, int K, int d, int N, int mode, int umode, const double* __restrict__ lrp, int nct,
     const double* __restrict__ sigma, const int32_t* __restrict__ kcur,
-    const uint32_t* __restrict__ rcur, uint64_t seed, int32_t* __restrict__ tau,
-    int32_t* __restrict__ rmode,
+    const uint32_t* __restrict__ rcur, uint64_t seed, double w2, bool reflect,
+    int32_t* __restrict__ tau, int32_t* __restrict__ rmode,
     float* __restrict__ rcoef, float* __restrict__ rsig, int* nanflag, int* act_next,
     int* host_prev, const int* gate) {
   if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -328,12 +341,17 @@ __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
   const double ell = valid ? -sz * inv - 0.5 * s2 * inv : 0.0;
   if (__ballot(valid && !(isfinite(ell) && isfinite(vn))) != 0ull && lane == 0) atomicOr(nanflag, 1);
   const uint32_t r = rcur[b];
-  const Decision D = decide(mode, umode, kb, ell, vn, (uint32_t)b, r, seed, lane);
+  const Decision D = decide(mode, umode, kb, ell, vn, (uint32_t)b, r, seed, lane, w2, !reflect);
   const int t = D.tau;
   int rm;
   float cf = 0.f, sgo = 0.f;
   const double st = __shfl(sgl, t <= kb ? t - 1 : kb);
-  if (t <= kb) {
+  const double s2t = __shfl(s2, t <= kb ? t - 1 : 0), szt = __shfl(sz, t <= kb ? t - 1 : 0);
+  if (t <= kb && reflect) {
+    // D.D > 0: a rejection never lands on a zero offset
+    rm = 4;
+    cf = (float)(1.0 + 2.0 * szt / s2t);
+  } else if (t <= kb) {
     const double v = __shfl(vn, t - 1);
     const double eG = __shfl(sgd, t - 1) / (st * v);
     rm = 1;
@@ -358,9 +376,9 @@ __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
 hipError_t verify_launch(int B, int K, int d, int mode, const float* yd, sd_stride ys,
                          const float* mp, sd_stride mps, const float* mq, sd_stride mqs,
                          const double* sigma, const int32_t* kb, const uint32_t* rnd,
-                         uint64_t seed, int umode, int32_t* tau, double* lar, double* ures,
-                         double* dn, double* lr, uint64_t* coins, int* nanflag, hipStream_t s,
-                         const int* gate) {
+                         uint64_t seed, int umode, double w2, int32_t* tau, double* lar,
+                         double* ures, double* dn, double* lr, uint64_t* coins, int* nanflag,
+                         hipStream_t s, const int* gate) {
   const bool vec = (d % 4 == 0) && ys.chain % 4 == 0 && ys.row % 4 == 0 && mps.chain % 4 == 0 &&
                    mps.row % 4 == 0 && mqs.chain % 4 == 0 && mqs.row % 4 == 0 &&
                    aligned16(yd) && aligned16(mp) && aligned16(mq);
@@ -374,20 +392,21 @@ hipError_t verify_launch(int B, int K, int d, int mode, const float* yd, sd_stri
   const int per = kThreads / 64;
   return timed("block_scan", s, [&] {
     scan_kernel<<<(B + per - 1) / per, kThreads, 0, s>>>(B, K, mode, umode, dn, lr, kb, rnd, seed,
-                                                        tau, lar, ures, coins, nanflag, gate);
+                                                        w2, tau, lar, ures, coins, nanflag, gate);
   });
 }
 
 hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, const double* lrp,
                              int nct, const double* sigma, const int32_t* kcur,
-                             const uint32_t* rcur, uint64_t seed, int32_t* tau, int32_t* rmode,
-                             float* rcoef, float* rsig, int* nanflag, int* act_next,
-                             int* host_prev, hipStream_t s, const int* gate) {
+                             const uint32_t* rcur, uint64_t seed, double w2, bool reflect,
+                             int32_t* tau, int32_t* rmode, float* rcoef, float* rsig,
+                             int* nanflag, int* act_next, int* host_prev, hipStream_t s,
+                             const int* gate) {
   const int per = kThreads / 64;
   return timed("scan_fused", s, [&] {
     scan_fused_kernel<<<(B + per - 1) / per, kThreads, 0, s>>>(
-        B, K, d, N, mode, umode, lrp, nct, sigma, kcur, rcur, seed, tau, rmode, rcoef, rsig,
-        nanflag, act_next, host_prev, gate);
+        B, K, d, N, mode, umode, lrp, nct, sigma, kcur, rcur, seed, w2, reflect, tau, rmode,
+        rcoef, rsig, nanflag, act_next, host_prev, gate);
   });
 }
 

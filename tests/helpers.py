@@ -28,7 +28,7 @@ def sigma_table(N, churn=1.0):
     return Schedule(N, churn=churn).sigma(np.arange(N + 1))
 
 
-def oracle_verify_chains(inp, chains, seed, mode, umode):
+def oracle_verify_chains(inp, chains, seed, mode, umode, omega=1.0):
     """Oracle verification of the given chains of an input dict of numpy arrays."""
     out = {}
     for b in chains:
@@ -37,7 +37,7 @@ def oracle_verify_chains(inp, chains, seed, mode, umode):
             out[b] = None
             continue
         out[b] = osamp.verify_chain(inp["y_draft"][b], inp["mp"][b], inp["mq"][b], inp["sigma"][b], kb,
-                                    seed, b, int(inp["round"][b]), mode, umode)
+                                    seed, b, int(inp["round"][b]), mode, umode, omega)
     return out
 
 

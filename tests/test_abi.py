@@ -45,7 +45,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert _lib.sd_abi_version() == 1
+    assert _lib.sd_abi_version() == 2
 
 
 def _expect_einval(status, needle):
@@ -88,6 +88,30 @@ def test_invalid_arguments_rejected_without_gpu(lib):
     _expect_einval(st, "B >= 1")
     st = lib.sd_run_sampler(null, 4, 8, 0, 0, 0, null, null, 0, null, null, 0, null)
     _expect_einval(st, "target is NULL")
+    for omega in (0.0, -1.0, float("inf"), float("nan")):
+        st = lib.sd_verify_block_tempered(4, 8, 8, 0, omega, null, s0, null, s0, null, s0, null, null,
+                                          null, 0, 0, null, null, null, null, null, null, null)
+        _expect_einval(st, "omega")
+    st = lib.sd_sample_residual_reflection(4, 0, 8, null, s0, null, s0, null, s0, null, null, null, null,
+                                           null, 0, null, null)
+    _expect_einval(st, "K = 0")
+    st = lib.sd_run_sampler_ex(null, 4, 8, None, 0, null, null, 0, null, null, 0, null)
+    _expect_einval(st, "options are NULL")
+    opts = _lib.sd_sampler_options(_lib.SD_BLOCK, 0, _lib.SD_RESIDUAL_REFLECTION, _lib.SD_DRAFTER_FREE, 1.0)
+    st = lib.sd_run_sampler_ex(null, 4, 8, ctypes.byref(opts), 0, null, null, 0, null, null, 0, null)
+    _expect_einval(st, "reflection residual needs sample")
+    opts = _lib.sd_sampler_options(_lib.SD_TOKEN, 0, _lib.SD_RESIDUAL_REFLECTION, 7, 1.0)
+    st = lib.sd_run_sampler_ex(null, 4, 8, ctypes.byref(opts), 0, null, null, 0, null, null, 0, null)
+    _expect_einval(st, "unknown drafter")
+    opts = _lib.sd_sampler_options(_lib.SD_TOKEN, 0, 0, _lib.SD_DRAFTER_FROZEN, 0.0)
+    st = lib.sd_run_sampler_ex(null, 4, 8, ctypes.byref(opts), 0, null, null, 0, null, null, 0, null)
+    _expect_einval(st, "omega")
+    opts = _lib.sd_sampler_options(_lib.SD_TOKEN, 0, _lib.SD_RESIDUAL_REFLECTION, _lib.SD_DRAFTER_FROZEN, 2.0)
+    st = lib.sd_run_sampler_ex(null, 4, 8, ctypes.byref(opts), 0, null, null, 0, null, null, 0, null)
+    _expect_einval(st, "target is NULL")
+    st = lib.sd_run_plain_em(null, 4, 0, null, null, 0, null)
+    _expect_einval(st, "target is NULL")
+    assert lib.sd_plain_em_workspace(null, 4) == 0
     st = lib.sd_init_chains(0, 3, 0, null, null)
     _expect_einval(st, "B >= 1")
     assert lib.sd_sampler_workspace(null, 4, 8) == 0
