@@ -216,6 +216,143 @@ def roofline_of(res, steps):
     return roof, table
 
 
+def _be_by_step(trace, N, nbins=10):
+    """Steps advanced per chain-round for rounds starting in each tenth of the
+    schedule (the acceptance-versus-step curve), from a tau trace [rounds][B]."""
+    R, B = trace.shape
+    k = np.zeros(B, dtype=np.int64)
+    adv = np.zeros(nbins)
+    cnt = np.zeros(nbins)
+    for r in range(R):
+        t = trace[r]
+        a = t > 0
+        if not a.any():
+            break
+        knew = np.minimum(k + t, N)
+        bins = np.minimum(k * nbins // N, nbins - 1)
+        np.add.at(adv, bins[a], (knew - k)[a])
+        np.add.at(cnt, bins[a], 1)
+        k = np.where(a, knew, k)
+    return [float(a / c) if c else None for a, c in zip(adv, cnt)]
+
+
+def variants_bench(lib, name, steps):
+    """The paper's alternatives on the same workload and seed: the three
+    residual/verification pairs of its comparison tables (reflection with
+    sample verification R, decomposition with sample verification D, block B)
+    at temperatures 0.5, 1, 2; the Frozen Drafter; and the plain
+    Euler-Maruyama chain (one target call on B rows per step), with the terms
+    of the paper's speedup decomposition (App. on Frozen and Free Drafters)
+    from per-kernel event times of one profiled run each."""
+    import torch
+    from paper_2606_13426_amd.inputs import WORKLOADS, workload_gmm
+    cfg = WORKLOADS[name]
+    B, K, N, d = cfg["B"], cfg["K"], cfg["N"], cfg["d"]
+    p = workload_gmm(name)
+    prec = lib.SD_BF16 if cfg["precision"] == "bf16" else lib.SD_FP32
+    tgt = lib.Target(lib.schedule(N), p["mu"], p["var"], p["log_w"], precision=prec)
+    ws = torch.empty(lib.sd_sampler_workspace(tgt, B, K), dtype=torch.uint8, device="cuda")
+    y = torch.empty(B, d, dtype=torch.float32, device="cuda")
+    seed = 0
+
+    def timed_runs(fn, reps):
+        fn()
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for _ in range(reps):
+            out = fn()
+        torch.cuda.synchronize()
+        return (time.perf_counter() - t0) / reps, out
+
+    def profiled(fn):
+        lib.sd_profile_only(None)
+        lib.sd_profile_enable(True)
+        fn()
+        prof = lib.sd_profile_read()
+        lib.sd_profile_enable(False)
+        return prof
+
+    def sampler(mode, residual, drafter, omega, trace_rounds=0):
+        return lambda: lib.sd_run_sampler_ex(tgt, B, K, seed, mode=mode, residual=residual, drafter=drafter,
+                                             omega=omega, y_out=y, ws=ws, trace_rounds=trace_rounds)
+
+    reps = max(2, steps // 3)
+    kinds = {"R": (lib.SD_TOKEN, lib.SD_RESIDUAL_REFLECTION), "D": (lib.SD_TOKEN, lib.SD_RESIDUAL_DECOMPOSITION),
+             "B": (lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION)}
+    table = {}
+    for omega in (0.5, 1.0, 2.0):
+        for kind, (mode, resid) in kinds.items():
+            sec, (_, st, _) = timed_runs(sampler(mode, resid, lib.SD_DRAFTER_FREE, omega), reps)
+            table[f"{kind}_omega{omega:g}"] = dict(value=B * N / sec, ms_per_run=1e3 * sec,
+                                                   mean_accepted_steps_per_block=st["steps"] / st["chain_rounds"],
+                                                   rounds_per_run=st["rounds"])
+    frozen = {}
+    for label, mode in (("block", lib.SD_BLOCK), ("token", lib.SD_TOKEN)):
+        sec, (_, st, _) = timed_runs(sampler(mode, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FROZEN, 1.0), reps)
+        frozen[label] = dict(value=B * N / sec, ms_per_run=1e3 * sec,
+                             mean_accepted_steps_per_block=st["steps"] / st["chain_rounds"],
+                             rounds_per_run=st["rounds"])
+    # the plain EM chain
+    em_ws = torch.empty(lib.sd_plain_em_workspace(tgt, B), dtype=torch.uint8, device="cuda")
+    em_sec, _ = timed_runs(lambda: lib.sd_run_plain_em(tgt, B, seed, y_out=y, ws=em_ws), reps)
+    em_prof = profiled(lambda: lib.sd_run_plain_em(tgt, B, seed, y_out=y, ws=em_ws))
+    # speedup terms, per round of the block sampler (Free and Frozen) and per EM step
+    tq1 = 1e3 * sum(v[1] for k, v in em_prof.items() if k.startswith("gmm_")) / N   # us per target call on B rows
+    free_prof = profiled(sampler(lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FREE, 1.0))
+    frz_prof = profiled(sampler(lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FROZEN, 1.0))
+    _, (_, _, trace) = timed_runs(sampler(lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FREE,
+                                          1.0, trace_rounds=N), 1)
+    be_curve = _be_by_step(trace.cpu().numpy(), N)
+
+    def terms(prof, be):
+        # per round of the lockstep sampler, from the profiled run: the target
+        # kernels (the Frozen Drafter's call on B rows included), the
+        # verification + residual + commit (+ Free-Drafter draft, fused into
+        # advance), the Frozen Drafter's separate draft kernel, and the whole
+        # round; the one-time start (Y_0, the first draft) is spread over it
+        rounds = prof["scan_fused"][0]
+        per = lambda names: 1e3 * sum(prof[k][1] for k in names if k in prof) / rounds
+        round_us = per(list(prof))
+        return dict(target_us=per([k for k in prof if k.startswith("gmm_")]),
+                    verify_residual_commit_us=per(["scan_fused", "advance"]),
+                    draft_kernel_us=per(["draft_block"]),
+                    round_us=round_us, target_over_time_q1=per([k for k in prof if k.startswith("gmm_")]) / tq1,
+                    predicted_speedup=be * tq1 / round_us)
+
+    # the latency-bound regime the paper's speedup assumes (a target call on a
+    # few rows costs about what one row costs): the same target and schedule
+    # with B = 8 chains
+    Bs = 8
+    ws_s = torch.empty(lib.sd_sampler_workspace(tgt, Bs, K), dtype=torch.uint8, device="cuda")
+    em_ws_s = torch.empty(lib.sd_plain_em_workspace(tgt, Bs), dtype=torch.uint8, device="cuda")
+    ys = torch.empty(Bs, d, dtype=torch.float32, device="cuda")
+    em_s, _ = timed_runs(lambda: lib.sd_run_plain_em(tgt, Bs, seed, y_out=ys, ws=em_ws_s), reps)
+    small = dict(B=Bs, plain_em=dict(value=Bs * N / em_s, ms_per_run=1e3 * em_s))
+    for label, mode, resid, drafter in (("block_free", lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FREE),
+                                        ("block_frozen", lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FROZEN),
+                                        ("token_reflection_free", lib.SD_TOKEN, lib.SD_RESIDUAL_REFLECTION, lib.SD_DRAFTER_FREE)):
+        sec, (_, st, _) = timed_runs(
+            lambda: lib.sd_run_sampler_ex(tgt, Bs, K, seed, mode=mode, residual=resid, drafter=drafter,
+                                          y_out=ys, ws=ws_s), reps)
+        small[label] = dict(value=Bs * N / sec, ms_per_run=1e3 * sec, speedup_vs_plain_em=em_s / sec,
+                            mean_accepted_steps_per_block=st["steps"] / st["chain_rounds"],
+                            rounds_per_run=st["rounds"])
+
+    be_free = table["B_omega1"]["mean_accepted_steps_per_block"]
+    be_frz = frozen["block"]["mean_accepted_steps_per_block"]
+    spec_ms = table["B_omega1"]["ms_per_run"]
+    return dict(
+        three_way=table, frozen_drafter=frozen,
+        plain_em=dict(value=B * N / em_sec, ms_per_run=1e3 * em_sec, target_calls=N,
+                      time_q1_us=tq1,
+                      kernels={k: dict(launches=v[0], avg_us=1e3 * v[1] / max(v[0], 1)) for k, v in em_prof.items()}),
+        speedup_vs_plain_em=dict(block_free=1e3 * em_sec / spec_ms,
+                                 block_frozen=1e3 * em_sec / frozen["block"]["ms_per_run"],
+                                 token_free=1e3 * em_sec / table["D_omega1"]["ms_per_run"]),
+        speedup_terms=dict(free=terms(free_prof, be_free), frozen=terms(frz_prof, be_frz), time_q1_us=tq1),
+        be_by_step_tenths=be_curve, small_batch=small)
+
+
 def verify_bench(lib, steps, warmup):
     """Verification-only workload: one sd_verify_block + sd_sample_residual per step."""
     import torch
@@ -352,9 +489,20 @@ def main():
     ap.add_argument("--library-gemms", action="store_true",
                     help="only time the workloads' denoiser GEMM shapes through the vendor library "
                          "(torch.mm) and exit")
+    ap.add_argument("--variants", action="store_true",
+                    help="only run the variants (reflection / decomposition / block at three "
+                         "temperatures, the Frozen Drafter, the plain EM chain) on --workload and exit")
     args = ap.parse_args()
     if args.library_gemms:
         print(json.dumps(dict(library_gemms=library_gemms())))
+        return
+    if args.variants:
+        import torch
+        from paper_2606_13426_amd import _lib as lib
+        lib.load()
+        # torch initialises the device before the library's first HIP call
+        assert torch.cuda.is_available(), "bench.py needs a GPU"
+        print(json.dumps(dict(workload=args.workload, variants=variants_bench(lib, args.workload, args.steps))))
         return
     if args.calibrate_copy:
         # also the achievable streaming rates of this machine: a read-plus-write
@@ -424,6 +572,7 @@ def main():
                                        for k, v in table2.items() if "avg_us" in v})
         line["other_workloads"] = others
         line["library_gemms"] = library_gemms()
+        line["variants"] = variants_bench(lib, args.workload, args.steps)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_budget)
     print(json.dumps(line))
