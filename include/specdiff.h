@@ -17,7 +17,7 @@
  *    sd_target_create (freed by sd_target_destroy); everything else lives in
  *    caller buffers, including a caller workspace sized by the *_workspace query.
  *    sd_run_sampler also holds, for the duration of the call, 16 bytes of
- *    mapped pinned host memory and four HIP events.
+ *    mapped pinned host memory.
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
  *    null stream).  Only sd_run_sampler reads results back: a per-round "any
  *    chain active" flag that its kernels store into the mapped host memory,

@@ -158,13 +158,10 @@ hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int
   const int ng = (d + 3) / 4;
   dim3 grid((ng + kThreads - 1) / kThreads, B);
   const bool vec = (d % 4 == 0) && aligned16(x) && aligned16(sv) && aligned16(mq) && aligned16(y);
-  return timed("advance", s, [&] {
-    advance_kernel<<<grid, kThreads, 0, s>>>(sc, coef, B, K, d, seed, kcur, rcur, crow_cur,
-                                             cstep_cur, knext, rnext, crow_next, cstep_next, tau,
-                                             rmode, rcoef, rsig, x, sv, mq, y, step, sigma, hist,
-                                             steps, act_next, trace, r, trace_rounds, vec,
-                                             frozen, gate);
-  });
+  return launch_timed("advance", advance_kernel, grid, dim3(kThreads), s, sc, coef, B, K, d, seed,
+                      kcur, rcur, crow_cur, cstep_cur, knext, rnext, crow_next, cstep_next, tau, rmode,
+                      rcoef, rsig, x, sv, mq, y, step, sigma, hist, steps, act_next, trace, r,
+                      trace_rounds, vec, frozen, gate);
 }
 
 }  // namespace sd

@@ -532,23 +532,23 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
     SD_HIP(draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2, cstep2, mq, mqs, k2, rnd2, seed,
                                x, xs, sv, s, nullptr));
 
-  // Round r's scan publishes round r - 1's active flag into slot (r - 1) of
-  // a mapped host array; the host reads round r - kLag's flag once round
-  // r - kLag + 1 has finished, so the queue runs kLag rounds ahead of it.
+  // Round r's scan publishes round r - 1's active flag, tagged with r - 1, into
+  // slot (r - 1) % kSlots of a mapped host array.  After enqueueing round r
+  // the host polls round r - kLag's slot until the tag is there (the queue
+  // stays kLag rounds ahead) and stops enqueueing at the first cleared flag.
+  // No event or copy is queued per round: a marker between rounds would
+  // hold the next round's first kernel back by several microseconds.
   int32_t* host_act = nullptr;
   int32_t* host_act_dev = nullptr;
   constexpr int kLag = 3, kSlots = kLag + 1;
-  hipEvent_t ev[kSlots];
   SD_HIP(hipHostMalloc(reinterpret_cast<void**>(&host_act), sizeof(int32_t) * kSlots, hipHostMallocDefault));
   if (hipHostGetDevicePointer(reinterpret_cast<void**>(&host_act_dev), host_act, 0) != hipSuccess) {
     (void)hipHostFree(host_act);
     set_error("sd_run_sampler: host flag not mapped");
     return SD_EHIP;
   }
-  for (int i = 0; i < kSlots; ++i) {
-    host_act[i] = -1;
-    (void)hipEventCreateWithFlags(&ev[i], hipEventDisableTiming);
-  }
+  for (int i = 0; i < kSlots; ++i) host_act[i] = -1;  // tag -1: nothing published
+  volatile int32_t* const pub = host_act;
   sd_status st = SD_OK;
   int64_t rounds = -1;
   // a round advances every active chain by at least one step, so at most N
@@ -575,14 +575,13 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
     if (e == hipSuccess)
       e = scan_fused_launch(B, K, d, N, (int)mode, (int)usample_mode, lrp, L.nct, sigma,
                             k2 + cur * B, rnd2 + cur * B, seed, w2, reflect, tau, rmode, rcoef,
-                            rsig, nanflag, act + nxt, publish, s, gate);
+                            rsig, nanflag, act + nxt, publish, r - 1, s, gate);
     if (e == hipSuccess)
       e = advance_launch(t.sc, t.coef, B, K, d, seed, k2 + cur * B, rnd2 + cur * B,
                          crow2 + cur * B, cstep2 + cur * B, k2 + nxt * B, rnd2 + nxt * B,
                          crow2 + nxt * B, cstep2 + nxt * B, tau, rmode, rcoef, rsig, x, sv, mq, y,
                          step, sigma, hist, steps, act + nxt, tau_trace, r,
                          tau_trace ? trace_rounds : 0, frozen, s, gate);
-    if (e == hipSuccess) e = hipEventRecord(ev[r % kSlots], s);
     if (e != hipSuccess) {
       set_error("sd_run_sampler: launch failed in round %d: %s", r, hipGetErrorString(e));
       st = SD_EHIP;
@@ -590,29 +589,45 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
     }
     const int back = r - kLag;
     if (back >= 0) {
-      if (hipEventSynchronize(ev[(back + 1) % kSlots]) != hipSuccess) {
-        set_error("sd_run_sampler: event wait failed");
-        st = SD_EHIP;
-        break;
+      // round back + 1's scan (enqueued) publishes round back's flag; the wait
+      // ends on the tag, or on an error or a drained stream reported by the runtime
+      volatile int32_t* slot = pub + back % kSlots;
+      int32_t v;
+      for (uint32_t spin = 1; ((v = *slot) >> 1) != back; ++spin) {
+        if ((spin & 1023u) == 0) {
+          const hipError_t q = hipStreamQuery(s);
+          // not-ready is a status, not a failure: keep it out of the launch checks
+          if (q == hipErrorNotReady) {
+            (void)hipGetLastError();
+            continue;
+          }
+          v = *slot;
+          if (q == hipSuccess && (v >> 1) == back) break;
+          set_error("sd_run_sampler: round %d's flag was not published (%s)", back,
+                    hipGetErrorString(q));
+          st = SD_EHIP;
+          break;
+        }
       }
-      if (host_act[back % kSlots] == 0) rounds = back + 1;
+      if (st != SD_OK) break;
+      if ((v & 1) == 0) rounds = back + 1;
     }
   }
   if (st == SD_OK && rounds < 0) {
-    // the flags of the last kLag launched rounds; the last one has no later
-    // scan to publish it, so it is copied
-    const int first = r - kLag < 0 ? 0 : r - kLag;
-    if (r >= 1) {
-      const int last = r - 1;
-      if (hipMemcpyAsync(&host_act[last % kSlots], act + ((last & 1) ^ 1), sizeof(int32_t),
-                         hipMemcpyDeviceToHost, s) != hipSuccess ||
-          hipStreamSynchronize(s) != hipSuccess) {
-        set_error("sd_run_sampler: flag copy failed");
-        st = SD_EHIP;
-      }
+    // every launched round finishes; the flags of rounds up to r - 2 are then
+    // in their slots, and the last round's, which no later scan publishes, is
+    // copied
+    int32_t last_flag = 1;
+    if (r >= 1 && (hipMemcpyAsync(&last_flag, act + (((r - 1) & 1) ^ 1), sizeof(int32_t),
+                                  hipMemcpyDeviceToHost, s) != hipSuccess ||
+                   hipStreamSynchronize(s) != hipSuccess)) {
+      set_error("sd_run_sampler: flag copy failed");
+      st = SD_EHIP;
     }
-    for (int back = first; st == SD_OK && back < r; ++back) {
-      if (host_act[back % kSlots] == 0) {
+    for (int back = r - kLag < 0 ? 0 : r - kLag; st == SD_OK && back < r; ++back) {
+      const int32_t v = pub[back % kSlots];
+      const int32_t flag = back == r - 1 ? last_flag : ((v >> 1) == back ? (v & 1) : 1);
+      if (flag == 0) {
         rounds = back + 1;
         break;
       }
@@ -653,7 +668,6 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
     }
   }
   (void)hipStreamSynchronize(s);
-  for (int i = 0; i < kSlots; ++i) (void)hipEventDestroy(ev[i]);
   (void)hipHostFree(host_act);
   return st;
 }

@@ -34,6 +34,29 @@ hipError_t timed(const char* name, hipStream_t s, F&& launch) {
   return e;
 }
 
+#ifdef __HIPCC__
+}  // namespace sd
+#include <hip/hip_ext.h>
+namespace sd {
+// One launch of `kernel`; when profiling is on for `name` the launch carries
+// the start and stop events in its own dispatch (hipExtLaunchKernelGGL), which
+// times the kernel alone and costs the stream less than two event records.
+template <class Kern, class... Args>
+hipError_t launch_timed(const char* name, Kern kernel, dim3 grid, dim3 block, hipStream_t s,
+                        Args... args) {
+  if (!prof_on(name)) {
+    kernel<<<grid, block, 0, s>>>(args...);
+    return hipGetLastError();
+  }
+  hipEvent_t a, b;
+  prof_events(&a, &b);
+  hipExtLaunchKernelGGL(kernel, grid, block, 0, s, a, b, 0, args...);
+  const hipError_t e = hipGetLastError();
+  prof_push(name, a, b);
+  return e;
+}
+#endif
+
 // ------------------------------------------------------------- schedule --
 struct Sched {
   int N;
@@ -117,8 +140,8 @@ hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, co
                              int nct, const double* sigma, const int32_t* kcur,
                              const uint32_t* rcur, uint64_t seed, double w2, bool reflect,
                              int32_t* tau, int32_t* rmode, float* rcoef, float* rsig,
-                             int* nanflag, int* act_next, int* host_prev, hipStream_t s,
-                             const int* gate);
+                             int* nanflag, int* act_next, int* host_prev, int pub_round,
+                             hipStream_t s, const int* gate);
 // Residual, commit and the next round's Free-Drafter block, elementwise over
 // (chain, four coordinates); per-chain state is read from the *cur arrays and
 // written to the *next arrays (round parity), so no workgroup races another.

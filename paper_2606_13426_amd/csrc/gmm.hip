@@ -791,14 +791,8 @@ hipError_t logits_launch(const Target& t, const Plan& p, int R, const float* x, 
   const bool vec = t.d % KC == 0 && ldx % 4 == 0 && aligned16(x) &&
                    (int64_t)TILE * ldx * 4 < ((int64_t)1 << 31) &&
                    (int64_t)TILE * t.d * 4 < ((int64_t)1 << 31);
-  return timed("gmm_logits", s, [&] {
-    if (vec)
-      gmm_logits_kernel<true><<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu, p.ksplit, part,
-                                                       xsq, gate);
-    else
-      gmm_logits_kernel<false><<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu, p.ksplit, part,
-                                                        xsq, gate);
-  });
+  return launch_timed("gmm_logits", vec ? gmm_logits_kernel<true> : gmm_logits_kernel<false>, g1,
+                      dim3(kThreads), s, R, t.M, t.d, x, ldx, t.mu, p.ksplit, part, xsq, gate);
 }
 
 }  // namespace
@@ -812,11 +806,9 @@ hipError_t gmm_softmax_launch(const Target& t, int R, int S, const float* part, 
                               hipStream_t s, const int* gate) {
   if (!p_bf16 && t.M <= 64 && t.M % 4 == 0) {
     const int nbs = (R + kThreads / 16 - 1) / (kThreads / 16);
-    return timed("gmm_softmax", s, [&] {
-      gmm_softmax_small_kernel<<<nbs, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc,
-                                                        t.ls, t.logw, t.musq, t.coef,
-                                                        static_cast<float*>(P), rowc, gate);
-    });
+    return launch_timed("gmm_softmax", gmm_softmax_small_kernel, dim3(nbs), dim3(kThreads), s, R,
+                        t.M, t.d, S, part, xsq, step, t.sc, t.ls, t.logw, t.musq, t.coef,
+                        static_cast<float*>(P), rowc, gate);
   }
   if (t.M % 4 == 0 && t.M <= 4 * kThreads) {
     // G lanes per row: the smallest power of two >= M / 4, at least 16
@@ -826,36 +818,30 @@ hipError_t gmm_softmax_launch(const Target& t, int R, int S, const float* part, 
     auto launch = [&](auto gtag) {
       constexpr int GG = decltype(gtag)::value;
       if (p_bf16)
-        gmm_softmax_quad_kernel<GG><<<nbq, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc,
-                                                             t.ls, t.logw, t.musq, t.coef,
-                                                             static_cast<uint16_t*>(P), rowc, gate);
-      else
-        gmm_softmax_quad_kernel<GG><<<nbq, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc,
-                                                             t.ls, t.logw, t.musq, t.coef,
-                                                             static_cast<float*>(P), rowc, gate);
+        return launch_timed("gmm_softmax", gmm_softmax_quad_kernel<GG, uint16_t>, dim3(nbq),
+                            dim3(kThreads), s, R, t.M, t.d, S, part, xsq, step, t.sc, t.ls, t.logw,
+                            t.musq, t.coef, static_cast<uint16_t*>(P), rowc, gate);
+      return launch_timed("gmm_softmax", gmm_softmax_quad_kernel<GG, float>, dim3(nbq),
+                          dim3(kThreads), s, R, t.M, t.d, S, part, xsq, step, t.sc, t.ls, t.logw,
+                          t.musq, t.coef, static_cast<float*>(P), rowc, gate);
     };
-    return timed("gmm_softmax", s, [&] {
-      switch (g) {
-        case 16: launch(std::integral_constant<int, 16>{}); break;
-        case 32: launch(std::integral_constant<int, 32>{}); break;
-        case 64: launch(std::integral_constant<int, 64>{}); break;
-        case 128: launch(std::integral_constant<int, 128>{}); break;
-        default: launch(std::integral_constant<int, 256>{}); break;
-      }
-    });
+    switch (g) {
+      case 16: return launch(std::integral_constant<int, 16>{});
+      case 32: return launch(std::integral_constant<int, 32>{});
+      case 64: return launch(std::integral_constant<int, 64>{});
+      case 128: return launch(std::integral_constant<int, 128>{});
+      default: return launch(std::integral_constant<int, 256>{});
+    }
   }
   const int per = kThreads / 64;
   const int nb = (R + per - 1) / per;
-  return timed("gmm_softmax", s, [&] {
-    if (p_bf16)
-      gmm_softmax_kernel<<<nb, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc, t.ls,
-                                                 t.logw, t.musq, t.coef,
-                                                 static_cast<uint16_t*>(P), rowc, gate);
-    else
-      gmm_softmax_kernel<<<nb, kThreads, 0, s>>>(R, t.M, t.d, S, part, xsq, step, t.sc, t.ls,
-                                                 t.logw, t.musq, t.coef, static_cast<float*>(P),
-                                                 rowc, gate);
-  });
+  if (p_bf16)
+    return launch_timed("gmm_softmax", gmm_softmax_kernel<uint16_t>, dim3(nb), dim3(kThreads), s, R,
+                        t.M, t.d, S, part, xsq, step, t.sc, t.ls, t.logw, t.musq, t.coef,
+                        static_cast<uint16_t*>(P), rowc, gate);
+  return launch_timed("gmm_softmax", gmm_softmax_kernel<float>, dim3(nb), dim3(kThreads), s, R, t.M,
+                      t.d, S, part, xsq, step, t.sc, t.ls, t.logw, t.musq, t.coef,
+                      static_cast<float*>(P), rowc, gate);
 }
 
 hipError_t target_mean_launch(const Target& t, int R, const float* x, int64_t ldx,
@@ -908,14 +894,9 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
   const bool vec = t.M % KC == 0 && t.d % TILE == 0 && aligned16(x) && aligned16(mq) &&
                    aligned16(sv) && K1 >= 4 &&
                    (int64_t)(TILE + 2) * t.d * 4 < ((int64_t)1 << 31) && t.M < 1 << 22;
-  return timed("gmm_mean_lr", s, [&] {
-    if (vec)
-      gmm_mean_lr_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, P, t.muT, x, rowc, sv,
-                                                       cstep, t.coef, mq, lrp, rnd, seed, gate);
-    else
-      gmm_mean_lr_kernel<false><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, P, t.muT, x, rowc, sv,
-                                                        cstep, t.coef, mq, lrp, rnd, seed, gate);
-  });
+  return launch_timed("gmm_mean_lr", vec ? gmm_mean_lr_kernel<true> : gmm_mean_lr_kernel<false>, g2,
+                      dim3(kThreads), s, R, t.M, t.d, K1, P, t.muT, x, rowc, sv, cstep, t.coef, mq,
+                      lrp, rnd, seed, gate);
 }
 
 int lr_tiles(const Target& t) {

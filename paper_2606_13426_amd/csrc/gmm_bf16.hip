@@ -539,19 +539,16 @@ hipError_t logits_and_softmax(const Target& t, const Plan& p, const Bufs& w, int
   // the buffer-load path: whole chunks of k and 32-bit offsets inside a tile
   const bool vec = vecx && t.d % KC == 0 && ldx < (int64_t)1 << 22 && t.d < 1 << 22;
   const bool wide = vec && p.wide && ldx < (int64_t)1 << 21 && t.d < 1 << 21;
-  hipError_t e = timed("gmm_logits_bf16", s, [&] {
-    if (wide)
-      gmm_logits_bf16_wide_kernel<<<dim3((t.M + bf16w::WT - 1) / bf16w::WT,
-                                         (R + bf16w::WT - 1) / bf16w::WT, p.S),
-                                    bf16w::kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu16, p.ksplit,
-                                                             w.part, w.xsq, gate);
-    else if (vec)
-      gmm_logits_bf16_kernel<true><<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu16, p.ksplit,
-                                                           w.part, w.xsq, gate);
-    else
-      gmm_logits_bf16_kernel<false><<<g1, kThreads, 0, s>>>(R, t.M, t.d, x, ldx, t.mu16, p.ksplit,
-                                                            w.part, w.xsq, gate);
-  });
+  hipError_t e;
+  if (wide)
+    e = launch_timed("gmm_logits_bf16", gmm_logits_bf16_wide_kernel,
+                     dim3((t.M + bf16w::WT - 1) / bf16w::WT, (R + bf16w::WT - 1) / bf16w::WT, p.S),
+                     dim3(bf16w::kThreads), s, R, t.M, t.d, x, ldx, t.mu16, p.ksplit, w.part, w.xsq,
+                     gate);
+  else
+    e = launch_timed("gmm_logits_bf16", vec ? gmm_logits_bf16_kernel<true> : gmm_logits_bf16_kernel<false>,
+                     g1, dim3(kThreads), s, R, t.M, t.d, x, ldx, t.mu16, p.ksplit, w.part, w.xsq,
+                     gate);
   if (e != hipSuccess) return e;
   return gmm_softmax_launch(t, R, p.S, w.part, w.xsq, step, w.P, true, w.rowc, s, gate);
 }
@@ -597,16 +594,10 @@ hipError_t target_mean_lr_bf16_launch(const Target& t, int R, int K1, const floa
   // least eight rows per chain, 32-bit offsets inside a tile's views
   const bool vec = t.M % KC == 0 && t.d % TN == 0 && vecd && K1 >= 8 &&
                    (int64_t)(TM + 2) * t.d * 4 < ((int64_t)1 << 31);
-  return timed("gmm_mean_lr_bf16", s, [&] {
-    if (vec)
-      gmm_mean_lr_bf16_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, w.P, t.muT16, x,
-                                                            w.rowc, sv, cstep, t.coef, mq, lrp,
-                                                            vecd, rnd, seed, gate);
-    else
-      gmm_mean_lr_bf16_kernel<false><<<g2, kThreads, 0, s>>>(R, t.M, t.d, K1, w.P, t.muT16, x,
-                                                             w.rowc, sv, cstep, t.coef, mq, lrp,
-                                                             vecd, rnd, seed, gate);
-  });
+  return launch_timed("gmm_mean_lr_bf16",
+                      vec ? gmm_mean_lr_bf16_kernel<true> : gmm_mean_lr_bf16_kernel<false>, g2,
+                      dim3(kThreads), s, R, t.M, t.d, K1, w.P, t.muT16, x, w.rowc, sv, cstep, t.coef,
+                      mq, lrp, vecd, rnd, seed, gate);
 }
 
 int lr_tiles_bf16(const Target& t) { return (t.d + TN - 1) / TN; }

@@ -261,20 +261,21 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(
 //            D = m^p - m^q = sigma Delta and W = yhat_tau - m^p = sigma Z,
 //            whose two sums are the log-ratio partials of row tau - 1)
 // It also clears the next round's active flag before looking at its gate,
-// and copies the gate (whether any chain was still active after the previous
-// round) to host_prev, a flag in mapped host memory that the host polls, so
-// that no separate device-to-host copy is queued per round.
+// and stores the gate (whether any chain was still active after the previous
+// round) tagged with that round's index, (pub_round << 1) | flag, into
+// host_prev, a word of mapped host memory that the host polls, so that
+// neither a device-to-host copy nor an event is queued per round.
 __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
     int B, int K, int d, int N, int mode, int umode, const double* __restrict__ lrp, int nct,
     const double* __restrict__ sigma, const int32_t* __restrict__ kcur,
     const uint32_t* __restrict__ rcur, uint64_t seed, double w2, bool reflect,
     int32_t* __restrict__ tau, int32_t* __restrict__ rmode,
     float* __restrict__ rcoef, float* __restrict__ rsig, int* nanflag, int* act_next,
-    int* host_prev, const int* gate) {
+    int* host_prev, int pub_round, const int* gate) {
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     *act_next = 0;
     if (host_prev) {
-      *host_prev = gate ? *gate : 1;
+      __atomic_store_n(host_prev, (pub_round << 1) | (gate ? *gate : 1), __ATOMIC_RELAXED);
       __threadfence_system();
     }
   }
@@ -400,14 +401,12 @@ hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, co
                              int nct, const double* sigma, const int32_t* kcur,
                              const uint32_t* rcur, uint64_t seed, double w2, bool reflect,
                              int32_t* tau, int32_t* rmode, float* rcoef, float* rsig,
-                             int* nanflag, int* act_next, int* host_prev, hipStream_t s,
-                             const int* gate) {
+                             int* nanflag, int* act_next, int* host_prev, int pub_round,
+                             hipStream_t s, const int* gate) {
   const int per = kThreads / 64;
-  return timed("scan_fused", s, [&] {
-    scan_fused_kernel<<<(B + per - 1) / per, kThreads, 0, s>>>(
-        B, K, d, N, mode, umode, lrp, nct, sigma, kcur, rcur, seed, w2, reflect, tau, rmode,
-        rcoef, rsig, nanflag, act_next, host_prev, gate);
-  });
+  return launch_timed("scan_fused", scan_fused_kernel, dim3((B + per - 1) / per), dim3(kThreads), s,
+                      B, K, d, N, mode, umode, lrp, nct, sigma, kcur, rcur, seed, w2, reflect, tau,
+                      rmode, rcoef, rsig, nanflag, act_next, host_prev, pub_round, gate);
 }
 
 }  // namespace sd
