@@ -12,6 +12,7 @@
 #include <vector>
 
 #include "common.hpp"
+#include "gemm_split.hpp"
 
 namespace sd {
 
@@ -181,7 +182,9 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
   bool ok = (bf ? hipMalloc(&t->mu16, sizeof(uint16_t) * M * D) == hipSuccess &&
                       hipMalloc(&t->muT16, sizeof(uint16_t) * M * D) == hipSuccess
                 : hipMalloc(&t->mu, sizeof(float) * M * D) == hipSuccess &&
-                      hipMalloc(&t->muT, sizeof(float) * M * D) == hipSuccess) &&
+                      hipMalloc(&t->muT, sizeof(float) * M * D) == hipSuccess &&
+                      hipMalloc(&t->mu_split, sizeof(uint16_t) * 3 * M * D) == hipSuccess &&
+                      hipMalloc(&t->muT_split, sizeof(uint16_t) * 3 * M * D) == hipSuccess) &&
             hipMalloc(&t->ls, sizeof(double2) * M * (size_t)sched->n_steps) == hipSuccess &&
             hipMalloc(&t->logw, sizeof(double) * M) == hipSuccess &&
             hipMalloc(&t->musq, sizeof(double) * M) == hipSuccess &&
@@ -204,8 +207,15 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
          hipMemcpy(t->muT16, hT.data(), sizeof(uint16_t) * M * D, hipMemcpyHostToDevice) ==
              hipSuccess;
   } else {
-    ok = hipMemcpy(t->mu, mu, sizeof(float) * M * D, hipMemcpyHostToDevice) == hipSuccess &&
-         hipMemcpy(t->muT, muT.data(), sizeof(float) * M * D, hipMemcpyHostToDevice) ==
+    const size_t n = M * D;
+    std::vector<uint16_t> sp(3 * n), spT(3 * n);
+    split::split_host(mu, n, sp.data(), sp.data() + n, sp.data() + 2 * n);
+    split::split_host(muT.data(), n, spT.data(), spT.data() + n, spT.data() + 2 * n);
+    ok = hipMemcpy(t->mu, mu, sizeof(float) * n, hipMemcpyHostToDevice) == hipSuccess &&
+         hipMemcpy(t->muT, muT.data(), sizeof(float) * n, hipMemcpyHostToDevice) == hipSuccess &&
+         hipMemcpy(t->mu_split, sp.data(), sizeof(uint16_t) * 3 * n, hipMemcpyHostToDevice) ==
+             hipSuccess &&
+         hipMemcpy(t->muT_split, spT.data(), sizeof(uint16_t) * 3 * n, hipMemcpyHostToDevice) ==
              hipSuccess;
   }
   ok = ok &&
@@ -244,6 +254,8 @@ sd_status sd_target_destroy(sd_target target) {
   Target* t = reinterpret_cast<Target*>(target);
   if (t->mu) (void)hipFree(t->mu);
   if (t->muT) (void)hipFree(t->muT);
+  if (t->mu_split) (void)hipFree(t->mu_split);
+  if (t->muT_split) (void)hipFree(t->muT_split);
   if (t->mu16) (void)hipFree(t->mu16);
   if (t->muT16) (void)hipFree(t->muT16);
   if (t->ls) (void)hipFree(t->ls);

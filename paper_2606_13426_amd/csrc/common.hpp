@@ -94,6 +94,11 @@ struct Target {
   float* muT;     // [d][M]
   uint16_t* mu16;   // [M][d] bf16 (round to nearest even), bf16 precision only
   uint16_t* muT16;  // [d][M] bf16, bf16 precision only
+  // float32 precision: the exact three-term bf16 splits of mu and mu^T
+  // (planes hi, mid, lo, each [M][d] resp. [d][M]) for the matrix-core
+  // contractions of gemm_split.hpp
+  uint16_t* mu_split;   // [3][M][d]
+  uint16_t* muT_split;  // [3][d][M]
   double* logw;   // [M]
   double* musq;   // [M] ||mu_m||^2 (float64 from the float32 means)
   float4* coef;   // [N+1] per step: (c1_n, c2_n, sigma_n, 1/c2_n) rounded to float32

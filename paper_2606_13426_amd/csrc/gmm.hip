@@ -21,6 +21,7 @@
 
 #include "bufio.hpp"
 #include "common.hpp"
+#include "gemm_split.hpp"
 #include "philox.hpp"
 #include "rows.hpp"
 #include "rowsum.hpp"
@@ -224,6 +225,61 @@ __global__ __launch_bounds__(kThreads) void gmm_logits_kernel(
       const int row = r0 + (threadIdx.x >> 4) + 16 * h;
       if ((threadIdx.x & 15) == 0 && row < R) xsq[(int64_t)s * R + row] = t;
     }
+  }
+}
+
+// The logits GEMM of the aligned float32 path on the bf16 matrix cores
+// (gemm_split.hpp): X rows split in registers, mu from its pre-split planes;
+// the same tile order, outputs and float64 ||x||^2 as gmm_logits_kernel.
+static_assert(split::kLdsBytes <= (int)sizeof(TileLds), "the split planes reuse the float32 tile's LDS");
+
+// (four wavefronts per SIMD: 128 registers, the accumulators in VGPRs)
+__global__ __launch_bounds__(kThreads, 4) void gmm_logits_split_kernel(
+    int R, int M, int d, const float* __restrict__ X, int64_t ldx,
+    const uint16_t* __restrict__ musplit, int ksplit, float* __restrict__ part,
+    double* __restrict__ xsq, const int* gate) {
+  if (gate && *gate == 0) return;
+  __shared__ TileLds sm;
+  const int nsplit = gridDim.x, nrt = gridDim.y;
+  const int lin = xcd_tile(nsplit * nrt * gridDim.z);
+  const int s = lin % nsplit, rt = (lin / nsplit) % nrt, ct = lin / (nsplit * nrt);
+  const int r0 = rt * TILE, c0 = ct * TILE;
+  const int kbeg = s * ksplit, kend = min(d, kbeg + ksplit);
+  const size_t plane = (size_t)M * d;
+  const __amdgpu_buffer_rsrc_t va = tile_rows(X, ldx, R, r0);
+  const __amdgpu_buffer_rsrc_t vb[3] = {split::plane_rows(musplit, d, M, c0),
+                                        split::plane_rows(musplit + plane, d, M, c0),
+                                        split::plane_rows(musplit + 2 * plane, d, M, c0)};
+  split::Acc acc;
+  split::zero(acc);
+  double sq = 0.0;
+  split::AChunk ra;
+  split::BChunk rb;
+  split::load_b(vb, d, kbeg, rb);
+  split::load_a(va, ldx, kbeg, ra);
+  uint16_t* lds = reinterpret_cast<uint16_t*>(&sm);
+  const bool want_sq = ct == 0;
+  if (want_sq)
+    split::tile_run<true>(lds, va, ldx, vb, d, kbeg, kend, ra, rb, acc, sq);
+  else
+    split::tile_run<false>(lds, va, ldx, vb, d, kbeg, kend, ra, rb, acc, sq);
+  float* ps = part + (int64_t)s * R * M;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int col = c0 + split::out_col(b);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = r0 + split::out_row(j);
+      if (row < R && col < M) ps[(int64_t)row * M + col] = acc.c[b][j];
+    }
+  }
+  if (want_sq) {
+    // the four lanes of a row are l % 16 + 16 q
+    sq += __shfl_xor(sq, 16);
+    sq += __shfl_xor(sq, 32);
+    const int lane = threadIdx.x & 63;
+    const int row = r0 + 16 * (threadIdx.x >> 6) + lane;
+    if (lane < 16 && row < R) xsq[(int64_t)s * R + row] = sq;
   }
 }
 
@@ -488,12 +544,16 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
 // through a view of the tile's rows (x: 65 rows, the last for the next draft
 // of the tile's last row; SV: the tile's chains; m^q: the tile's rows), so
 // rows past the block read zero and their stores drop.
-template <bool VEC>
+// SPLIT (with VEC): the contraction on the bf16 matrix cores from the
+// pre-split planes of mu^T (gemm_split.hpp), P split in registers.
+template <bool VEC, bool SPLIT>
 __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     int R, int M, int d, int K1, const float* __restrict__ P, const float* __restrict__ muT,
-    const float* __restrict__ X, const float* __restrict__ rowc, const float* __restrict__ SV,
+    const uint16_t* __restrict__ muTs, const float* __restrict__ X,
+    const float* __restrict__ rowc, const float* __restrict__ SV,
     const int32_t* __restrict__ cstep, const float4* __restrict__ coef, float* __restrict__ mq,
     double* __restrict__ lrp, const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
+  static_assert(!SPLIT || VEC, "the split contraction needs the aligned path");
   if (gate && *gate == 0) return;
   __shared__ TileLds sm;
   __shared__ float rc[3 * TILE];
@@ -514,8 +574,19 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
   // epilogue, whose latency then overlaps the contraction
   const __amdgpu_buffer_rsrc_t va = tile_rows(P, M, R, r0), vb = tile_rows(muT, M, d, c0);
   float4 ra[4], rb[4];
-  load_chunk<VEC>(P, va, M, R, r0, 0, M, ra);
-  load_chunk<VEC>(muT, vb, M, d, c0, 0, M, rb);
+  split::AChunk sa;
+  split::BChunk sb;
+  __amdgpu_buffer_rsrc_t vbs[3];
+  if constexpr (SPLIT) {
+    const size_t plane = (size_t)M * d;
+#pragma unroll
+    for (int p = 0; p < 3; ++p) vbs[p] = split::plane_rows(muTs + p * plane, M, d, c0);
+    split::load_b(vbs, M, 0, sb);
+    split::load_a(va, M, 0, sa);
+  } else {
+    load_chunk<VEC>(P, va, M, R, r0, 0, M, ra);
+    load_chunk<VEC>(muT, vb, M, d, c0, 0, M, rb);
+  }
   // small per-row and per-chain inputs next (the epilogue's coefficients and
   // the rounds of the residual's G), so that their waits exclude the bulk
   // (unconditional loads from clamped indices, unused where out of range)
@@ -565,13 +636,24 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
       pv[i] = dr ? ld4(SV + (int64_t)b * d + col, cnt, false) : z4;
     }
   }
-  f32x16 acc;
+  if constexpr (SPLIT) {
+    split::Acc acc;
+    split::zero(acc);
+    double unused = 0.0;
+    split::tile_run<false>(reinterpret_cast<uint16_t*>(&sm), va, M, vbs, M, 0, M, sa, sb, acc,
+                           unused);
+    __syncthreads();  // every wavefront is done with the operand planes
 #pragma unroll
-  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
-  double unused[4];
-  nt_tile_run<false, VEC>(sm, P, va, M, R, muT, vb, M, d, r0, c0, 0, M, ra, rb, acc, unused);
-  __syncthreads();  // every wavefront is done with the operand tiles
-  {
+    for (int b = 0; b < 4; ++b)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) sm.a[split::out_row(j) * LDW + split::out_col(b)] = acc.c[b][j];
+  } else {
+    f32x16 acc;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+    double unused[4];
+    nt_tile_run<false, VEC>(sm, P, va, M, R, muT, vb, M, d, r0, c0, 0, M, ra, rb, acc, unused);
+    __syncthreads();  // every wavefront is done with the operand tiles
     const int cw = out_col();
 #pragma unroll
     for (int v = 0; v < 16; ++v) sm.a[out_row(v) * LDW + cw] = acc[v];
@@ -791,6 +873,9 @@ hipError_t logits_launch(const Target& t, const Plan& p, int R, const float* x, 
   const bool vec = t.d % KC == 0 && ldx % 4 == 0 && aligned16(x) &&
                    (int64_t)TILE * ldx * 4 < ((int64_t)1 << 31) &&
                    (int64_t)TILE * t.d * 4 < ((int64_t)1 << 31);
+  if (vec && t.mu_split)
+    return launch_timed("gmm_logits", gmm_logits_split_kernel, g1, dim3(kThreads), s, R, t.M, t.d,
+                        x, ldx, t.mu_split, p.ksplit, part, xsq, gate);
   return launch_timed("gmm_logits", vec ? gmm_logits_kernel<true> : gmm_logits_kernel<false>, g1,
                       dim3(kThreads), s, R, t.M, t.d, x, ldx, t.mu, p.ksplit, part, xsq, gate);
 }
@@ -894,9 +979,10 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
   const bool vec = t.M % KC == 0 && t.d % TILE == 0 && aligned16(x) && aligned16(mq) &&
                    aligned16(sv) && K1 >= 4 &&
                    (int64_t)(TILE + 2) * t.d * 4 < ((int64_t)1 << 31) && t.M < 1 << 22;
-  return launch_timed("gmm_mean_lr", vec ? gmm_mean_lr_kernel<true> : gmm_mean_lr_kernel<false>, g2,
-                      dim3(kThreads), s, R, t.M, t.d, K1, P, t.muT, x, rowc, sv, cstep, t.coef, mq,
-                      lrp, rnd, seed, gate);
+  auto kern = !vec ? gmm_mean_lr_kernel<false, false>
+                    : t.muT_split ? gmm_mean_lr_kernel<true, true> : gmm_mean_lr_kernel<true, false>;
+  return launch_timed("gmm_mean_lr", kern, g2, dim3(kThreads), s, R, t.M, t.d, K1, P, t.muT,
+                      t.muT_split, x, rowc, sv, cstep, t.coef, mq, lrp, rnd, seed, gate);
 }
 
 int lr_tiles(const Target& t) {
