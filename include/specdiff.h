@@ -98,7 +98,10 @@ sd_status sd_schedule_table(const sd_schedule* sched, double* host_out);
  * mean m^q_n(x) = c1_n x + c2_n score (eq. target-distribution).
  * mu [M][d], var [M], log_w [M] are HOST arrays copied at creation.
  * d >= 1, 1 <= n_comp <= 1024.  precision selects the GEMM operand type:
- * SD_FP32 multiplies float32 operands; SD_BF16 stores mu as bf16 (round to
+ * SD_FP32 multiplies float32 operands to float32 accuracy (on the aligned
+ * path as six bf16 products of exact three-term bf16 splits of each operand,
+ * whose dropped terms are below 2^-23 of |a b|, accumulated in float32;
+ * elsewhere with float32 matrix instructions); SD_BF16 stores mu as bf16 (round to
  * nearest even) and rounds x and the softmax weights to bf16 before the two
  * products, accumulating in float32 (||x||^2, ||mu||^2 and the softmax stay
  * float64 from the float32 values; the epilogue is float32).  Only the copies
