@@ -523,6 +523,58 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
   }
 }
 
+// gmm_mean_kernel's contraction on the bf16 matrix cores (gemm_split.hpp):
+// P split in registers, mu^T from its pre-split planes; M a whole number of
+// chunks.
+__global__ __launch_bounds__(kThreads) void gmm_mean_split_kernel(
+    int R, int M, int d, const float* __restrict__ P, const uint16_t* __restrict__ muTs,
+    const float* __restrict__ X, int64_t ldx, const float* __restrict__ rowc,
+    float* __restrict__ mq, int64_t ldq, float* __restrict__ score, int64_t lds,
+    const int* gate) {
+  if (gate && *gate == 0) return;
+  __shared__ TileLds sm;
+  __shared__ float rc[3 * TILE];
+  const int r0 = blockIdx.x * TILE, c0 = blockIdx.y * TILE;
+  for (int e = threadIdx.x; e < 3 * TILE; e += kThreads)
+    rc[e] = r0 + e / 3 < R ? rowc[3 * (int64_t)r0 + e] : 0.f;
+  const size_t plane = (size_t)M * d;
+  const __amdgpu_buffer_rsrc_t va = tile_rows(P, M, R, r0);
+  const __amdgpu_buffer_rsrc_t vb[3] = {split::plane_rows(muTs, M, d, c0),
+                                        split::plane_rows(muTs + plane, M, d, c0),
+                                        split::plane_rows(muTs + 2 * plane, M, d, c0)};
+  split::AChunk sa;
+  split::BChunk sb;
+  split::load_b(vb, M, 0, sb);
+  split::load_a(va, M, 0, sa);
+  // the epilogue's x, whose latency then overlaps the contraction
+  float xv[4][4];
+#pragma unroll
+  for (int b = 0; b < 4; ++b)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int row = r0 + split::out_row(j), col = c0 + split::out_col(b);
+      xv[b][j] = row < R && col < d ? X[(int64_t)row * ldx + col] : 0.f;
+    }
+  split::Acc acc;
+  split::zero(acc);
+  double unused = 0.0;
+  split::tile_run<false>(reinterpret_cast<uint16_t*>(&sm), va, M, vb, M, 0, M, sa, sb, acc, unused);
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const int col = c0 + split::out_col(b);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int lr = split::out_row(j), row = r0 + lr;
+      if (row < R && col < d) {
+        const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
+        const float sc = acc.c[b][j] - rho * xv[b][j];
+        mq[(int64_t)row * ldq + col] = c1 * xv[b][j] + c2 * sc;
+        if (score) score[(int64_t)row * lds + col] = sc;
+      }
+    }
+  }
+}
+
 // The sampler's second GEMM: O = P mu with the EM epilogue, plus the partial
 // log-ratio sums of verification while the tile is on chip.  Rows are
 // (chain b, row j) of a [B][K+1][d] block: x row j is draft yhat_{k+j} (row 0
@@ -946,14 +998,12 @@ hipError_t target_mean_launch(const Target& t, int R, const float* x, int64_t ld
   if (e != hipSuccess) return e;
   dim3 g2((R + TILE - 1) / TILE, (t.d + TILE - 1) / TILE);
   const bool vec = t.M % KC == 0 && t.M < 1 << 22;
-  return timed("gmm_mean", s, [&] {
-    if (vec)
-      gmm_mean_kernel<true><<<g2, kThreads, 0, s>>>(R, t.M, t.d, P, t.muT, x, ldx, rowc, mq, ldq,
-                                                    score, lds, gate);
-    else
-      gmm_mean_kernel<false><<<g2, kThreads, 0, s>>>(R, t.M, t.d, P, t.muT, x, ldx, rowc, mq, ldq,
-                                                     score, lds, gate);
-  });
+  if (vec && t.muT_split)
+    return launch_timed("gmm_mean", gmm_mean_split_kernel, g2, dim3(kThreads), s, R, t.M, t.d, P,
+                        t.muT_split, x, ldx, rowc, mq, ldq, score, lds, gate);
+  return launch_timed("gmm_mean", vec ? gmm_mean_kernel<true> : gmm_mean_kernel<false>, g2,
+                      dim3(kThreads), s, R, t.M, t.d, P, t.muT, x, ldx, rowc, mq, ldq, score, lds,
+                      gate);
 }
 
 hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
