@@ -44,33 +44,24 @@ struct TileLds {
 
 // Load rows r0..r0+63, columns k0..k0+63 (< kend) of a row-major matrix into
 // four float4 registers per thread: thread t covers rows t/16 + 16 h (h < 4)
-// and columns k0 + 4 (t % 16) .. + 3; out-of-range elements read as zero.
-// VEC: the k range is a whole number of chunks and rows are 16-byte aligned,
-// so each piece is one unconditional buffer load from the tile's view (rows
-// past the matrix read zero); otherwise element by element.
-template <bool VEC>
-__device__ __forceinline__ void load_chunk(const float* __restrict__ A, __amdgpu_buffer_rsrc_t view,
-                                           int64_t ld, int nrows, int r0, int k0, int kend,
-                                           float4 (&reg)[4]) {
+// and columns k0 + 4 (t % 16) .. + 3; out-of-range elements read as zero
+// (element by element: the unaligned path).
+__device__ __forceinline__ void load_chunk(const float* __restrict__ A, int64_t ld, int nrows,
+                                           int r0, int k0, int kend, float4 (&reg)[4]) {
   const int t = threadIdx.x;
   const int kc = k0 + 4 * (t & 15);
 #pragma unroll
   for (int h = 0; h < 4; ++h) {
-    const int rr = (t >> 4) + 16 * h;
-    if constexpr (VEC) {
-      reg[h] = buf_ld4(view, (uint32_t)((rr * (int)ld + kc) * 4));
-    } else {
-      const int r = r0 + rr;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (r < nrows) {
-        const float* p = A + (int64_t)r * ld + kc;
-        if (kc < kend) v.x = p[0];
-        if (kc + 1 < kend) v.y = p[1];
-        if (kc + 2 < kend) v.z = p[2];
-        if (kc + 3 < kend) v.w = p[3];
-      }
-      reg[h] = v;
+    const int r = r0 + (t >> 4) + 16 * h;
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (r < nrows) {
+      const float* p = A + (int64_t)r * ld + kc;
+      if (kc < kend) v.x = p[0];
+      if (kc + 1 < kend) v.y = p[1];
+      if (kc + 2 < kend) v.z = p[2];
+      if (kc + 3 < kend) v.w = p[3];
     }
+    reg[h] = v;
   }
 }
 
@@ -116,13 +107,12 @@ __device__ __forceinline__ void mma_chunk(const TileLds& sm, int wr, int wc, f32
 // can issue other loads after the first chunk's: the hardware counts loads in
 // order, and the first wait then does not include them).
 // With SQ it also accumulates the float64 squares of the four A rows this thread loads.
-template <bool SQ, bool VEC>
-__device__ __forceinline__ void nt_tile_run(TileLds& sm, const float* __restrict__ A,
-                                            __amdgpu_buffer_rsrc_t va, int64_t lda, int nra,
-                                            const float* __restrict__ Bm,
-                                            __amdgpu_buffer_rsrc_t vb, int64_t ldb, int nrb,
-                                            int r0, int c0, int kbeg, int kend, float4 (&ra)[4],
-                                            float4 (&rb)[4], f32x16& acc, double (&sq)[4]) {
+template <bool SQ>
+__device__ __forceinline__ void nt_tile_run(TileLds& sm, const float* __restrict__ A, int64_t lda,
+                                            int nra, const float* __restrict__ Bm, int64_t ldb,
+                                            int nrb, int r0, int c0, int kbeg, int kend,
+                                            float4 (&ra)[4], float4 (&rb)[4], f32x16& acc,
+                                            double (&sq)[4]) {
   const int w = threadIdx.x >> 6;
   const int wr = w >> 1, wc = w & 1;
   // one chunk: stage it, fetch the next, multiply.  The first chunk is peeled
@@ -139,8 +129,8 @@ __device__ __forceinline__ void nt_tile_run(TileLds& sm, const float* __restrict
     }
     __syncthreads();
     if (k0 + KC < kend) {
-      load_chunk<VEC>(A, va, lda, nra, r0, k0 + KC, kend, ra);
-      load_chunk<VEC>(Bm, vb, ldb, nrb, c0, k0 + KC, kend, rb);
+      load_chunk(A, lda, nra, r0, k0 + KC, kend, ra);
+      load_chunk(Bm, ldb, nrb, c0, k0 + KC, kend, rb);
     }
     mma_chunk(sm, wr, wc, acc);
   };
@@ -179,7 +169,9 @@ __device__ __forceinline__ int out_col() {
   return (w & 1) * 32 + (lane & 31);
 }
 
-template <bool VEC>
+// The logits GEMM on float32 matrix instructions: the path for rows that are
+// not 16-byte aligned or d that is not a whole number of chunks (the aligned
+// path is gmm_logits_split_kernel).
 __global__ __launch_bounds__(kThreads) void gmm_logits_kernel(
     int R, int M, int d, const float* __restrict__ X, int64_t ldx,
     const float* __restrict__ mu, int ksplit, float* __restrict__ part,
@@ -198,14 +190,13 @@ __global__ __launch_bounds__(kThreads) void gmm_logits_kernel(
   for (int v = 0; v < 16; ++v) acc[v] = 0.f;
   double sq[4] = {0.0, 0.0, 0.0, 0.0};
   const bool want_sq = ct == 0;
-  const __amdgpu_buffer_rsrc_t va = tile_rows(X, ldx, R, r0), vb = tile_rows(mu, d, M, c0);
   float4 ra[4], rb[4];
-  load_chunk<VEC>(X, va, ldx, R, r0, kbeg, kend, ra);
-  load_chunk<VEC>(mu, vb, d, M, c0, kbeg, kend, rb);
+  load_chunk(X, ldx, R, r0, kbeg, kend, ra);
+  load_chunk(mu, d, M, c0, kbeg, kend, rb);
   if (want_sq)
-    nt_tile_run<true, VEC>(sm, X, va, ldx, R, mu, vb, d, M, r0, c0, kbeg, kend, ra, rb, acc, sq);
+    nt_tile_run<true>(sm, X, ldx, R, mu, d, M, r0, c0, kbeg, kend, ra, rb, acc, sq);
   else
-    nt_tile_run<false, VEC>(sm, X, va, ldx, R, mu, vb, d, M, r0, c0, kbeg, kend, ra, rb, acc, sq);
+    nt_tile_run<false>(sm, X, ldx, R, mu, d, M, r0, c0, kbeg, kend, ra, rb, acc, sq);
   float* ps = part + (int64_t)s * R * M;
   const int col = c0 + out_col();
 #pragma unroll
@@ -479,7 +470,9 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_quad_kernel(
   }
 }
 
-template <bool VEC>
+// O = P mu with the EM epilogue on float32 matrix instructions: the path for M
+// that is not a whole number of chunks (the aligned path is
+// gmm_mean_split_kernel).
 __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
     int R, int M, int d, const float* __restrict__ P, const float* __restrict__ muT,
     const float* __restrict__ X, int64_t ldx, const float* __restrict__ rowc,
@@ -494,10 +487,9 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
     rc[e] = r0 + e / 3 < R ? rowc[3 * (int64_t)r0 + e] : 0.f;
   // the contraction's first operand chunk, then the epilogue's inputs, whose
   // latency then overlaps the contraction
-  const __amdgpu_buffer_rsrc_t va = tile_rows(P, M, R, r0), vb = tile_rows(muT, M, d, c0);
   float4 ra[4], rb[4];
-  load_chunk<VEC>(P, va, M, R, r0, 0, M, ra);
-  load_chunk<VEC>(muT, vb, M, d, c0, 0, M, rb);
+  load_chunk(P, M, R, r0, 0, M, ra);
+  load_chunk(muT, M, d, c0, 0, M, rb);
   float xv[16];
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -508,7 +500,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_kernel(
 #pragma unroll
   for (int v = 0; v < 16; ++v) acc[v] = 0.f;
   double unused[4];
-  nt_tile_run<false, VEC>(sm, P, va, M, R, muT, vb, M, d, r0, c0, 0, M, ra, rb, acc, unused);
+  nt_tile_run<false>(sm, P, M, R, muT, M, d, r0, c0, 0, M, ra, rb, acc, unused);
   if (col >= d) return;
 #pragma unroll
   for (int v = 0; v < 16; ++v) {
@@ -596,16 +588,16 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_split_kernel(
 // through a view of the tile's rows (x: 65 rows, the last for the next draft
 // of the tile's last row; SV: the tile's chains; m^q: the tile's rows), so
 // rows past the block read zero and their stores drop.
-// SPLIT (with VEC): the contraction on the bf16 matrix cores from the
-// pre-split planes of mu^T (gemm_split.hpp), P split in registers.
-template <bool VEC, bool SPLIT>
+// VEC also runs the contraction on the bf16 matrix cores from the pre-split
+// planes of mu^T (gemm_split.hpp), P split in registers; otherwise it is on
+// float32 matrix instructions.
+template <bool VEC>
 __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     int R, int M, int d, int K1, const float* __restrict__ P, const float* __restrict__ muT,
     const uint16_t* __restrict__ muTs, const float* __restrict__ X,
     const float* __restrict__ rowc, const float* __restrict__ SV,
     const int32_t* __restrict__ cstep, const float4* __restrict__ coef, float* __restrict__ mq,
     double* __restrict__ lrp, const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
-  static_assert(!SPLIT || VEC, "the split contraction needs the aligned path");
   if (gate && *gate == 0) return;
   __shared__ TileLds sm;
   __shared__ float rc[3 * TILE];
@@ -624,20 +616,20 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
   const int nchain = min((min(r0 + TILE, R) - 1) / K1 - b_first + 1, TILE);
   // the contraction's first operand chunk, then every global load of the
   // epilogue, whose latency then overlaps the contraction
-  const __amdgpu_buffer_rsrc_t va = tile_rows(P, M, R, r0), vb = tile_rows(muT, M, d, c0);
+  const __amdgpu_buffer_rsrc_t va = tile_rows(P, M, R, r0);
   float4 ra[4], rb[4];
   split::AChunk sa;
   split::BChunk sb;
   __amdgpu_buffer_rsrc_t vbs[3];
-  if constexpr (SPLIT) {
+  if constexpr (VEC) {
     const size_t plane = (size_t)M * d;
 #pragma unroll
     for (int p = 0; p < 3; ++p) vbs[p] = split::plane_rows(muTs + p * plane, M, d, c0);
     split::load_b(vbs, M, 0, sb);
     split::load_a(va, M, 0, sa);
   } else {
-    load_chunk<VEC>(P, va, M, R, r0, 0, M, ra);
-    load_chunk<VEC>(muT, vb, M, d, c0, 0, M, rb);
+    load_chunk(P, M, R, r0, 0, M, ra);
+    load_chunk(muT, M, d, c0, 0, M, rb);
   }
   // small per-row and per-chain inputs next (the epilogue's coefficients and
   // the rounds of the residual's G), so that their waits exclude the bulk
@@ -688,7 +680,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
       pv[i] = dr ? ld4(SV + (int64_t)b * d + col, cnt, false) : z4;
     }
   }
-  if constexpr (SPLIT) {
+  if constexpr (VEC) {
     split::Acc acc;
     split::zero(acc);
     double unused = 0.0;
@@ -704,7 +696,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[v] = 0.f;
     double unused[4];
-    nt_tile_run<false, VEC>(sm, P, va, M, R, muT, vb, M, d, r0, c0, 0, M, ra, rb, acc, unused);
+    nt_tile_run<false>(sm, P, M, R, muT, M, d, r0, c0, 0, M, ra, rb, acc, unused);
     __syncthreads();  // every wavefront is done with the operand tiles
     const int cw = out_col();
 #pragma unroll
@@ -925,11 +917,11 @@ hipError_t logits_launch(const Target& t, const Plan& p, int R, const float* x, 
   const bool vec = t.d % KC == 0 && ldx % 4 == 0 && aligned16(x) &&
                    (int64_t)TILE * ldx * 4 < ((int64_t)1 << 31) &&
                    (int64_t)TILE * t.d * 4 < ((int64_t)1 << 31);
-  if (vec && t.mu_split)
+  if (vec)
     return launch_timed("gmm_logits", gmm_logits_split_kernel, g1, dim3(kThreads), s, R, t.M, t.d,
                         x, ldx, t.mu_split, p.ksplit, part, xsq, gate);
-  return launch_timed("gmm_logits", vec ? gmm_logits_kernel<true> : gmm_logits_kernel<false>, g1,
-                      dim3(kThreads), s, R, t.M, t.d, x, ldx, t.mu, p.ksplit, part, xsq, gate);
+  return launch_timed("gmm_logits", gmm_logits_kernel, g1, dim3(kThreads), s, R, t.M, t.d, x, ldx,
+                      t.mu, p.ksplit, part, xsq, gate);
 }
 
 }  // namespace
@@ -998,12 +990,11 @@ hipError_t target_mean_launch(const Target& t, int R, const float* x, int64_t ld
   if (e != hipSuccess) return e;
   dim3 g2((R + TILE - 1) / TILE, (t.d + TILE - 1) / TILE);
   const bool vec = t.M % KC == 0 && t.M < 1 << 22;
-  if (vec && t.muT_split)
+  if (vec)
     return launch_timed("gmm_mean", gmm_mean_split_kernel, g2, dim3(kThreads), s, R, t.M, t.d, P,
                         t.muT_split, x, ldx, rowc, mq, ldq, score, lds, gate);
-  return launch_timed("gmm_mean", vec ? gmm_mean_kernel<true> : gmm_mean_kernel<false>, g2,
-                      dim3(kThreads), s, R, t.M, t.d, P, t.muT, x, ldx, rowc, mq, ldq, score, lds,
-                      gate);
+  return launch_timed("gmm_mean", gmm_mean_kernel, g2, dim3(kThreads), s, R, t.M, t.d, P, t.muT, x,
+                      ldx, rowc, mq, ldq, score, lds, gate);
 }
 
 hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
@@ -1029,9 +1020,8 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
   const bool vec = t.M % KC == 0 && t.d % TILE == 0 && aligned16(x) && aligned16(mq) &&
                    aligned16(sv) && K1 >= 4 &&
                    (int64_t)(TILE + 2) * t.d * 4 < ((int64_t)1 << 31) && t.M < 1 << 22;
-  auto kern = !vec ? gmm_mean_lr_kernel<false, false>
-                    : t.muT_split ? gmm_mean_lr_kernel<true, true> : gmm_mean_lr_kernel<true, false>;
-  return launch_timed("gmm_mean_lr", kern, g2, dim3(kThreads), s, R, t.M, t.d, K1, P, t.muT,
+  return launch_timed("gmm_mean_lr", vec ? gmm_mean_lr_kernel<true> : gmm_mean_lr_kernel<false>, g2,
+                      dim3(kThreads), s, R, t.M, t.d, K1, P, t.muT,
                       t.muT_split, x, rowc, sv, cstep, t.coef, mq, lrp, rnd, seed, gate);
 }
 
