@@ -177,8 +177,9 @@ sd_status sd_verify_block(int32_t B, int32_t K, int32_t d, sd_verify_mode mode,
  * tempered log alpha_{tau-1} (block) or 0 (token), and U is drawn for that
  * alpha_res and the untempered ||Delta_tau||.  log_ratio and delta_norm are
  * the untempered ell_j and ||Delta_j||.  omega = 1 is sd_verify_block; any
- * other value is lossy (the output no longer follows the target).  A
- * non-positive or non-finite omega returns SD_EINVAL. */
+ * other value is lossy (the output no longer follows the target).  An omega
+ * that is not positive and finite, or whose square over- or underflows in
+ * float64, returns SD_EINVAL. */
 sd_status sd_verify_block_tempered(int32_t B, int32_t K, int32_t d, sd_verify_mode mode,
                                    double omega, const float* y_draft, sd_stride ys,
                                    const float* mp, sd_stride mps, const float* mq,
@@ -214,7 +215,9 @@ sd_status sd_sample_residual(int32_t B, int32_t K, int32_t d, const float* y_dra
  * computed as y_draft_{tau-1} - c (mp - mq), c = 1 + 2 (D.W)/(D.D), D = mp -
  * mq, W = y_draft - mp, with the two sums over d in float64.  The full-accept
  * cases (tau = K_b + 1) are those of sd_sample_residual; no U and no RESID
- * noise are used.  Same arguments and layouts as sd_sample_residual. */
+ * noise are used.  A tau that points at a step with mp = mq (no direction
+ * e; a verification never rejects such a step) returns the draft, y =
+ * y_draft_{tau-1}.  Same arguments and layouts as sd_sample_residual. */
 sd_status sd_sample_residual_reflection(int32_t B, int32_t K, int32_t d, const float* y_draft,
                                         sd_stride ys, const float* mp, sd_stride mps,
                                         const float* mq, sd_stride mqs, const double* sigma,

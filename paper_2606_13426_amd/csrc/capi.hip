@@ -322,7 +322,8 @@ static sd_status verify_impl(const char* fn, int32_t B, int32_t K, int32_t d, sd
   SD_CHECK_ARG(K >= 1 && K <= SD_MAX_BLOCK, "%s: K = %d not in [1, %d]", fn, K, SD_MAX_BLOCK);
   SD_CHECK_ARG(mode == SD_BLOCK || mode == SD_TOKEN, "%s: unknown mode", fn);
   SD_CHECK_ARG(usample_mode == SD_USAMPLE_EXACT || usample_mode == SD_USAMPLE_PAPER, "%s: unknown usample mode", fn);
-  SD_CHECK_ARG(omega > 0.0 && isfinite(omega), "%s: omega must be positive and finite", fn);
+  SD_CHECK_ARG(omega > 0.0 && isfinite(omega) && omega * omega > 0.0 && isfinite(omega * omega),
+               "%s: omega must be positive and finite, with omega^2 too", fn);
   SD_CHECK_ARG(y_draft && mp && mq && sigma && kb && round && tau && log_alpha_res && u_res &&
                    delta_norm && log_ratio,
                "%s: NULL pointer argument", fn);
@@ -485,7 +486,9 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
                "sd_run_sampler: the reflection residual needs sample (token) verification");
   SD_CHECK_ARG(opts->drafter == SD_DRAFTER_FREE || opts->drafter == SD_DRAFTER_FROZEN,
                "sd_run_sampler: unknown drafter");
-  SD_CHECK_ARG(opts->omega > 0.0 && isfinite(opts->omega), "sd_run_sampler: omega must be positive and finite");
+  SD_CHECK_ARG(opts->omega > 0.0 && isfinite(opts->omega) && opts->omega * opts->omega > 0.0 &&
+                   isfinite(opts->omega * opts->omega),
+               "sd_run_sampler: omega must be positive and finite, with omega^2 too");
   SD_CHECK_ARG(target, "sd_run_sampler: target is NULL");
   const Target& t = *reinterpret_cast<Target*>(target);
   SD_CHECK_ARG(B >= 1, "sd_run_sampler: B = %d < 1", B);

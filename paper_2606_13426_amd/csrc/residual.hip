@@ -136,7 +136,9 @@ __device__ void reflection_row(int d, const float* yh, const float* p, const flo
   const double t2 = block_sum(a2, red);
   __syncthreads();  // every thread has read red before it is reused
   const double tz = block_sum(az, red);
-  const float cf = (float)(1.0 + 2.0 * tz / t2);  // t2 > 0 for a rejected step
+  // (no direction when D = 0: the draft noise is kept, y = yhat; a verification
+  // never rejects such a step)
+  const float cf = t2 > 0.0 ? (float)(1.0 + 2.0 * tz / t2) : 1.0f;
 #pragma unroll
   for (int i = 0; i < kKeep; ++i) {
     const int g = threadIdx.x + i * nt;

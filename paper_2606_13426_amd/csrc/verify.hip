@@ -349,9 +349,9 @@ __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
   const double st = __shfl(sgl, t <= kb ? t - 1 : kb);
   const double s2t = __shfl(s2, t <= kb ? t - 1 : 0), szt = __shfl(sz, t <= kb ? t - 1 : 0);
   if (t <= kb && reflect) {
-    // D.D > 0: a rejection never lands on a zero offset
+    // D.D > 0: a rejection never lands on a zero offset (kept as a guard)
     rm = 4;
-    cf = (float)(1.0 + 2.0 * szt / s2t);
+    cf = s2t > 0.0 ? (float)(1.0 + 2.0 * szt / s2t) : 1.0f;
   } else if (t <= kb) {
     const double v = __shfl(vn, t - 1);
     const double eG = __shfl(sgd, t - 1) / (st * v);

@@ -88,7 +88,7 @@ def test_invalid_arguments_rejected_without_gpu(lib):
     _expect_einval(st, "B >= 1")
     st = lib.sd_run_sampler(null, 4, 8, 0, 0, 0, null, null, 0, null, null, 0, null)
     _expect_einval(st, "target is NULL")
-    for omega in (0.0, -1.0, float("inf"), float("nan")):
+    for omega in (0.0, -1.0, float("inf"), float("nan"), 1e-200, 1e200):
         st = lib.sd_verify_block_tempered(4, 8, 8, 0, omega, null, s0, null, s0, null, s0, null, null,
                                           null, 0, 0, null, null, null, null, null, null, null)
         _expect_einval(st, "omega")

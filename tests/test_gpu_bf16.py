@@ -164,3 +164,28 @@ def test_bf16_sampler_deterministic_and_close_to_fp32_efficiency():
     be16 = s1["steps"] / s1["chain_rounds"]
     be32 = s32["steps"] / s32["chain_rounds"]
     assert abs(be16 - be32) <= 0.1 * be32, (be16, be32)
+
+
+def test_bf16_sampler_variants_deterministic_and_close_to_fp32():
+    """The variants on a bf16 target: deterministic, every chain reaches N, the
+    Frozen Drafter accepts its first draft every round, and the block
+    efficiency stays within 10 % of the float32 target's."""
+    d, M, N, B, K, seed = 512, 32, 60, 64, 6, 8
+    p = make_gmm(d, M, mu_std=1.0, var=(0.01, 0.2), dirichlet=1.0, seed=4)
+    sched = _lib.schedule(N)
+    t16 = _lib.Target(sched, p["mu"], p["var"], p["log_w"], precision=_lib.SD_BF16)
+    t32 = _lib.Target(sched, p["mu"], p["var"], p["log_w"])
+    for kw in (dict(drafter=_lib.SD_DRAFTER_FROZEN),
+               dict(mode=_lib.SD_TOKEN, residual=_lib.SD_RESIDUAL_REFLECTION),
+               dict(omega=2.0)):
+        y1, s1, tr = _lib.sd_run_sampler_ex(t16, B, K, seed, trace_rounds=N, **kw)
+        y2, s2, _ = _lib.sd_run_sampler_ex(t16, B, K, seed, **kw)
+        assert torch.equal(y1, y2) and s1["rounds"] == s2["rounds"], kw
+        assert torch.isfinite(y1).all() and s1["steps"] == B * N, kw
+        if kw.get("drafter") == _lib.SD_DRAFTER_FROZEN:
+            t = tr.cpu().numpy()
+            assert np.all(t[t > 0] >= 2)
+        _, s32, _ = _lib.sd_run_sampler_ex(t32, B, K, seed, **kw)
+        be16 = s1["steps"] / s1["chain_rounds"]
+        be32 = s32["steps"] / s32["chain_rounds"]
+        assert abs(be16 - be32) <= 0.1 * be32, (kw, be16, be32)

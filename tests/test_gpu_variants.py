@@ -275,3 +275,18 @@ def test_pixel3072_full_size_sampled_chains(mode, residual, drafter):
             assert_rows_close(y[b][None], ref["y"][0][None], rtol=1e-3, what=f"Y_N chain {b}")
             full += 1
     assert full >= 2
+
+
+def test_reflection_without_direction_keeps_the_draft():
+    # a tau forced onto a step with m^p = m^q (no direction e): the draft is kept
+    B, K, d, N, seed = 6, 4, 70, 100, 5
+    inp = _inputs(B, K, d, N, seed)
+    inp["kb"][:] = K
+    inp["steps_left"][:] = N
+    inp["mq"][:, 1] = inp["mp"][:, 1]
+    tau = torch.full((B,), 2, dtype=torch.int32, device=DEV)
+    y = torch.empty(B, d, device=DEV)
+    _lib.sd_sample_residual_reflection(inp["y_draft"], inp["mp"], inp["mq"], inp["sigma"], inp["kb"],
+                                       inp["steps_left"], tau, inp["round"], seed, y)
+    torch.cuda.synchronize()
+    assert torch.equal(y, inp["y_draft"][:, 1])
