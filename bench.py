@@ -33,20 +33,22 @@ METRIC = "verified chain-steps/sec + mean accepted steps per block; % MFMA / HBM
 
 # HBM bytes per launch of a workload's dominant kernel from two rocprofv3 passes
 # (FETCH_SIZE x 2.000 and WRITE_SIZE x 1.000, the factors a 1 GiB device copy
-# gives; profiles/sampler_pixel3072_hbm_traffic.md), valid for the library
-# sources whose digest (source_digest()) was recorded with them.
+# gives; profiles/sampler_pixel3072_hbm_traffic.md), valid while the kernel's
+# sources (its translation unit, every library header and the C header) have
+# the digest (source_digest(unit)) recorded with them.
 MEASURED_TRAFFIC = {
-    ("pixel3072", "gmm_mean_lr"): dict(bytes=(141.7 + 122.0) * 1e6,
-                                       sources="a14e39a8da0863f20c40ae66490685b87700705f"),
+    ("pixel3072", "gmm_mean_lr"): dict(bytes=(141.4 + 122.0) * 1e6, unit="gmm.hip",
+                                       sources="2603983f5da0a1e3c1be07789fdd73a1e1ac70bb"),
 }
 
 
-def source_digest():
-    """sha1 over the library's HIP sources, headers and C header (names and contents)."""
+def source_digest(unit):
+    """sha1 over a kernel's translation unit csrc/<unit>, the library headers
+    and the C header (names and contents)."""
     import glob
     import hashlib
     h = hashlib.sha1()
-    files = sorted(glob.glob(os.path.join(ROOT, "paper_2606_13426_amd", "csrc", "*.hip")) +
+    files = sorted([os.path.join(ROOT, "paper_2606_13426_amd", "csrc", unit)] +
                    glob.glob(os.path.join(ROOT, "paper_2606_13426_amd", "csrc", "*.hpp")) +
                    [os.path.join(ROOT, "include", "specdiff.h")])
     for f in files:
@@ -541,7 +543,7 @@ def main():
     res = run_sampler_bench(lib, args.workload, lib.SD_BLOCK, args.steps, args.warmup, profile=True)
     roof, table = roofline_of(res, args.steps)
     meas = MEASURED_TRAFFIC.get((args.workload, roof["kernel"])) if roof else None
-    if roof and meas and meas["sources"] == source_digest():
+    if roof and meas and meas["sources"] == source_digest(meas["unit"]):
         roof["traffic"] = meas["bytes"]
     line = dict(metric=METRIC, value=res["B"] * res["N"] / res["sec"], unit="chain-steps/s", n_gpus=1,
                 steps=args.steps, warmup=args.warmup, ms_per_step=1e3 * res["sec"], higher_is_better=True,
