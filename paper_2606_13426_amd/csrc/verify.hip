@@ -14,8 +14,8 @@
 // coin, and a ballot gives tau.  U is found by inverting Psi_alpha: the
 // doubling of Alg. 7 is done for all 64 candidate lower ends at once (lane i
 // tests u* - 2^i), and the bisection becomes a 64-way multisection that
-// shrinks the bracket 65-fold per step until it is 1e-13 (relative) wide or
-// has collapsed in float64.
+// shrinks the bracket 65-fold per step until it is 1e-8 (relative) wide, then
+// a linear interpolation of log Psi inside it (see usample_exact).
 //
 // Both scans take the temperature as w2 = omega^2 (the tempered
 // verifications of the appendix divide every ell_j by omega^2), and the
@@ -111,30 +111,48 @@ __device__ __forceinline__ double log_cdf(double x, double la, double v, double 
   return log_excess(x, la, v) - Lstar;
 }
 
-// Exact inverse of Psi_alpha at u, with all 64 lanes of the wavefront.
+// Inverse of Psi_alpha at u, with all 64 lanes of the wavefront: the doubling
+// of Alg. 7 for all 64 candidate lower ends at once (lane i tests u* - 2^i),
+// then a 64-way multisection (lane i evaluates log Psi at the i+1-th of 65
+// points) until the bracket is 1e-8 (relative) wide, then a linear
+// interpolation of log Psi between the bracket's ends, whose values the lanes
+// already hold: inside so narrow a bracket its error is far below the
+// bracket width except next to u*, where the density vanishes (there it is
+// at most the width).
 __device__ double usample_exact(double u, double la, double v, int lane) {
   const double us = la / v + 0.5 * v;
   const double Lstar = log_excess(us, la, v);
   const double logu = log(u);
-  // doubling of the bracket width: lane i tests the lower end u* - 2^i
   const double cand = us - ldexp(1.0, lane);
-  const uint64_t above = __ballot(log_cdf(cand, la, v, us, Lstar) > logu);
+  const double fc = log_cdf(cand, la, v, us, Lstar);
+  const uint64_t above = __ballot(fc > logu);
   const int p = (~above == 0ull) ? 63 : (__ffsll((unsigned long long)~above) - 1);
-  double lo = us - ldexp(1.0, p);
-  double hi = p == 0 ? us : us - ldexp(1.0, p - 1);
-  if (~above == 0ull) hi = us - ldexp(1.0, 62);
+  double lo = us - ldexp(1.0, p), flo = __shfl(fc, p);
+  double hi = p == 0 ? us : us - ldexp(1.0, p - 1), fhi = p == 0 ? 0.0 : __shfl(fc, p > 0 ? p - 1 : 0);
+  if (~above == 0ull) {
+    hi = us - ldexp(1.0, 62);
+    fhi = __shfl(fc, 62);
+  }
   for (int it = 0; it < 64; ++it) {
     const double mid = 0.5 * (lo + hi);
-    if (!(mid > lo && mid < hi) || hi - lo <= 1e-13 * fmax(1.0, fabs(lo))) break;
+    if (!(mid > lo && mid < hi) || hi - lo <= 1e-8 * fmax(1.0, fabs(lo))) break;
     const double x = lo + (hi - lo) * ((double)(lane + 1) / 65.0);
-    const uint64_t below = __ballot(log_cdf(x, la, v, us, Lstar) < logu);
+    const double fx = log_cdf(x, la, v, us, Lstar);
+    const uint64_t below = __ballot(fx < logu);
     const int cnt = __popcll(below);
-    const double nlo = __shfl(x, cnt > 0 ? cnt - 1 : 0);
-    const double nhi = __shfl(x, cnt < 64 ? cnt : 63);
-    lo = cnt > 0 ? nlo : lo;
-    hi = cnt < 64 ? nhi : hi;
+    const double nlo = __shfl(x, cnt > 0 ? cnt - 1 : 0), nflo = __shfl(fx, cnt > 0 ? cnt - 1 : 0);
+    const double nhi = __shfl(x, cnt < 64 ? cnt : 63), nfhi = __shfl(fx, cnt < 64 ? cnt : 63);
+    if (cnt > 0) {
+      lo = nlo;
+      flo = nflo;
+    }
+    if (cnt < 64) {
+      hi = nhi;
+      fhi = nfhi;
+    }
   }
-  return 0.5 * (lo + hi);
+  const double t = fhi > flo ? (logu - flo) / (fhi - flo) : 0.5;
+  return lo + (hi - lo) * fmin(fmax(t, 0.0), 1.0);
 }
 
 // The capped doubling/bisection of the paper's experiments (3 + 4 steps).
