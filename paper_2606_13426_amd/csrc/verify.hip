@@ -121,18 +121,16 @@ __device__ __forceinline__ double log_cdf(double x, double la, double v, double 
 // at most the width).
 __device__ double usample_exact(double u, double la, double v, int lane) {
   const double us = la / v + 0.5 * v;
-  const double Lstar = log_excess(us, la, v);
   const double logu = log(u);
-  const double cand = us - ldexp(1.0, lane);
-  const double fc = log_cdf(cand, la, v, us, Lstar);
-  const uint64_t above = __ballot(fc > logu);
+  // one pass: lanes 0..62 the doubling candidates u* - 2^i, lane 63 the
+  // normaliser log(alpha Phi(u*) - Phi(u* - v))
+  const double le = log_excess(lane < 63 ? us - ldexp(1.0, lane) : us, la, v);
+  const double Lstar = __shfl(le, 63);
+  const double fc = le - Lstar;
+  const uint64_t above = __ballot(lane < 63 && fc > logu) | (1ull << 63);
   const int p = (~above == 0ull) ? 63 : (__ffsll((unsigned long long)~above) - 1);
-  double lo = us - ldexp(1.0, p), flo = __shfl(fc, p);
+  double lo = us - ldexp(1.0, p), flo = p < 63 ? __shfl(fc, p < 63 ? p : 0) : -INFINITY;
   double hi = p == 0 ? us : us - ldexp(1.0, p - 1), fhi = p == 0 ? 0.0 : __shfl(fc, p > 0 ? p - 1 : 0);
-  if (~above == 0ull) {
-    hi = us - ldexp(1.0, 62);
-    fhi = __shfl(fc, 62);
-  }
   for (int it = 0; it < 64; ++it) {
     const double mid = 0.5 * (lo + hi);
     if (!(mid > lo && mid < hi) || hi - lo <= 1e-8 * fmax(1.0, fabs(lo))) break;
