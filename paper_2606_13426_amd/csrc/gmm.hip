@@ -10,11 +10,14 @@
 //   gmm_softmax: sums the split partials in a fixed order and forms P, rho (float64 logits);
 //   gmm_mean:    O = P mu     (rows x M by M x d) with the EM epilogue fused.
 // Both GEMMs are "A times B-transposed" over row-major operands whose
-// contraction index is contiguous (mu^T is stored at target creation), so one
-// tile core serves both: a 64x64 output tile per workgroup, four wavefronts of
-// 32x32, k staged through LDS in chunks of 64 and fed to
-// v_mfma_f32_32x32x2f32.  Within a chunk, lane half h supplies k = 32h + s to
-// MFMA s, so each lane reads its 32 k-values as eight 16-byte LDS reads.
+// contraction index is contiguous (mu^T is stored at target creation), on 64x64
+// output tiles per workgroup of four wavefronts.  The aligned path (rows
+// 16-byte aligned, whole chunks of k) runs them on the bf16 matrix cores
+// through exact three-term operand splits (gemm_split.hpp: float32-accurate
+// products, mu and mu^T pre-split at target creation).  The unaligned path
+// stages k through LDS in chunks of 64 for v_mfma_f32_32x32x2f32 (wavefronts
+// of 32x32; lane half h supplies k = 32h + s to MFMA s, eight 16-byte LDS
+// reads per lane per chunk).
 #include <vector>
 
 #include <type_traits>
