@@ -11,16 +11,17 @@
 // the result is float32-accurate at 6/16 of the float32 instruction's
 // matrix-core time.
 //
-// Tile: 64 rows of A x 64 rows of B (the output's columns) per workgroup of
-// four wavefronts; wavefront w owns rows 16 w .. 16 w + 15 and all four
-// 16-column blocks.  A (float32) goes from memory straight into its
-// wavefront's registers, lane l holding row 16 w + l % 16 and k = 8 (l / 16)
-// .. + 7 of each 32-wide step, and is split there.  B comes pre-split (three
+// Tile: 64 RB rows of A x 64 rows of B (the output's columns) per workgroup
+// of four wavefronts; wavefront w owns RB blocks of 16 rows (rows 16 (RB w +
+// r) .. + 15, r < RB) and all four 16-column blocks, so each B fragment read
+// from LDS feeds RB row blocks.  A (float32) goes from memory straight into
+// its wavefront's registers, lane l holding row 16 (RB w + r) + l % 16 and
+// k = 8 (l / 16) .. + 7 of each 32-wide step, and is split there.  B comes pre-split (three
 // bf16 planes in memory, row-major with the same leading dimension) and is
 // staged through LDS, 64 k per chunk, three planes of 64 x 72 (row stride 144
 // bytes: the 16 rows of one 16-lane read pass fall in distinct banks).
-// Output block c of wavefront w: lane l holds rows 16 w + 4 (l / 16) + j
-// (j < 4) of column 16 c + l % 16.
+// Output block c of row block r of wavefront w: lane l holds rows
+// 16 (RB w + r) + 4 (l / 16) + j (j < 4) of column 16 c + l % 16.
 //
 // The aligned path only: every row 16-byte aligned, k ranges whole chunks,
 // rows past a matrix read as zero from the tile's buffer views.
@@ -97,16 +98,20 @@ struct AChunk {
   float4 v[2][2];
 };
 
-// view: the (at most 64) rows of A of the tile; lane row 16 w + l % 16.
-__device__ __forceinline__ void load_a(__amdgpu_buffer_rsrc_t view, int64_t lda, int k0, AChunk& a) {
+// view: the (at most 64 RB) rows of A of the tile; lane rows 16 (RB w + r) + l % 16.
+template <int RB>
+__device__ __forceinline__ void load_a(__amdgpu_buffer_rsrc_t view, int64_t lda, int k0, AChunk (&a)[RB]) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const uint32_t base = (uint32_t)(((16 * w + (lane & 15)) * (int)lda + 8 * (lane >> 4)) * 4);
   const int so = __builtin_amdgcn_readfirstlane(k0 * 4);
 #pragma unroll
-  for (int s = 0; s < 2; ++s)
+  for (int r = 0; r < RB; ++r) {
+    const uint32_t base = (uint32_t)(((16 * (RB * w + r) + (lane & 15)) * (int)lda + 8 * (lane >> 4)) * 4);
 #pragma unroll
-    for (int q = 0; q < 2; ++q)
-      a.v[s][q] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(view, base + (uint32_t)((32 * s + 4 * q) * 4), so, 0));
+    for (int s = 0; s < 2; ++s)
+#pragma unroll
+      for (int q = 0; q < 2; ++q)
+        a[r].v[s][q] = __builtin_bit_cast(float4, __builtin_amdgcn_raw_buffer_load_b128(view, base + (uint32_t)((32 * s + 4 * q) * 4), so, 0));
+  }
 }
 
 // float64 sum of squares of the lane's A values of a chunk.
@@ -126,25 +131,30 @@ __device__ __forceinline__ bf16x8 frag(const uint16_t* p) {
   return __builtin_bit_cast(bf16x8, *reinterpret_cast<const uint4*>(p));
 }
 
-// The chunk's 2 steps x 4 column blocks x 6 terms.
-__device__ __forceinline__ void mma_chunk(const uint16_t* lds, const AChunk& a, Acc& acc) {
+// The chunk's 2 steps x 4 column blocks x RB row blocks x 6 terms.
+template <int RB>
+__device__ __forceinline__ void mma_chunk(const uint16_t* lds, const AChunk (&a)[RB], Acc (&acc)[RB]) {
   const int lane = threadIdx.x & 63;
   const uint16_t* pb = lds + (lane & 15) * LDH + 8 * (lane >> 4);
 #pragma unroll
   for (int s = 0; s < 2; ++s) {
-    bf16x8 ah, am, al;
-    split8(a.v[s][0], a.v[s][1], ah, am, al);
+    bf16x8 ah[RB], am[RB], al[RB];
+#pragma unroll
+    for (int r = 0; r < RB; ++r) split8(a[r].v[s][0], a[r].v[s][1], ah[r], am[r], al[r]);
 #pragma unroll
     for (int b = 0; b < 4; ++b) {
       const uint16_t* q = pb + 16 * b * LDH + 32 * s;
       const bf16x8 bh = frag(q), bm = frag(q + kPlaneElems), bl = frag(q + 2 * kPlaneElems);
-      f32x4 c = acc.c[b];
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al, bh, c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bl, c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, bm, c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am, bh, c, 0, 0, 0);
-      c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bm, c, 0, 0, 0);
-      acc.c[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah, bh, c, 0, 0, 0);
+#pragma unroll
+      for (int r = 0; r < RB; ++r) {
+        f32x4 c = acc[r].c[b];
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(al[r], bh, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[r], bl, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am[r], bm, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(am[r], bh, c, 0, 0, 0);
+        c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[r], bm, c, 0, 0, 0);
+        acc[r].c[b] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ah[r], bh, c, 0, 0, 0);
+      }
     }
   }
 }
@@ -157,24 +167,30 @@ __device__ __forceinline__ void mma_chunk(const uint16_t* lds, const AChunk& a, 
 // not a chunk ahead: a prefetch register set would cost the occupancy that
 // hides those loads behind the other workgroups' matrix work.  The caller's
 // first use of lds afterwards must follow a barrier.
-template <bool SQ>
+template <bool SQ, int RB>
 __device__ __forceinline__ void tile_run(uint16_t* lds, __amdgpu_buffer_rsrc_t va, int64_t lda,
                                          const __amdgpu_buffer_rsrc_t (&vb)[3], int64_t ldb,
-                                         int kbeg, int kend, AChunk& ra, BChunk& rb, Acc& acc,
-                                         double& sq) {
+                                         int kbeg, int kend, AChunk (&ra)[RB], BChunk& rb,
+                                         Acc (&acc)[RB], double (&sq)[RB]) {
   const int n = (kend - kbeg) / KC;
   store_b(lds, rb);
   __syncthreads();
-  if constexpr (SQ) sq += squares(ra);
-  mma_chunk(lds, ra, acc);
+  if constexpr (SQ) {
+#pragma unroll
+    for (int r = 0; r < RB; ++r) sq[r] += squares(ra[r]);
+  }
+  mma_chunk<RB>(lds, ra, acc);
   for (int c = 1; c < n; ++c) {
     load_b(vb, ldb, kbeg + c * KC, rb);
-    load_a(va, lda, kbeg + c * KC, ra);
+    load_a<RB>(va, lda, kbeg + c * KC, ra);
     __syncthreads();  // every wavefront is done with the previous chunk
     store_b(lds, rb);
     __syncthreads();
-    if constexpr (SQ) sq += squares(ra);
-    mma_chunk(lds, ra, acc);
+    if constexpr (SQ) {
+#pragma unroll
+      for (int r = 0; r < RB; ++r) sq[r] += squares(ra[r]);
+    }
+    mma_chunk<RB>(lds, ra, acc);
   }
 }
 
@@ -184,10 +200,12 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t plane_rows(const uint16_t* P, 
   return buf_view(P + (int64_t)r0 * ld, (int64_t)max(0, min(nrows - r0, TILE)) * ld * 2);
 }
 
-// Row (inside the tile) of accumulator element j and column of block b.
-__device__ __forceinline__ int out_row(int j) {
+// Row (inside the tile) of accumulator element j of row block r, and column
+// of block b.
+template <int RB>
+__device__ __forceinline__ int out_row(int r, int j) {
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  return 16 * w + 4 * (lane >> 4) + j;
+  return 16 * (RB * w + r) + 4 * (lane >> 4) + j;
 }
 __device__ __forceinline__ int out_col(int b) { return 16 * b + (threadIdx.x & 15); }
 

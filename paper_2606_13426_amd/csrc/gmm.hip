@@ -224,11 +224,15 @@ __global__ __launch_bounds__(kThreads) void gmm_logits_kernel(
 
 // The logits GEMM of the aligned float32 path on the bf16 matrix cores
 // (gemm_split.hpp): X rows split in registers, mu from its pre-split planes;
-// the same tile order, outputs and float64 ||x||^2 as gmm_logits_kernel.
+// the same outputs and float64 ||x||^2 as gmm_logits_kernel.  The tile is
+// kSplitRows = 128 rows of X (two 16-row blocks per wavefront, each B
+// fragment read from LDS serving both) by 64 components: half the LDS
+// traffic and B loads per output of a 64-row tile, at two wavefronts per
+// SIMD (the 32 accumulators and 32 A values per lane need the registers).
 static_assert(split::kLdsBytes <= (int)sizeof(TileLds), "the split planes reuse the float32 tile's LDS");
+constexpr int kSplitRB = 2, kSplitRows = 64 * kSplitRB;
 
-// (four wavefronts per SIMD: 128 registers, the accumulators in VGPRs)
-__global__ __launch_bounds__(kThreads, 4) void gmm_logits_split_kernel(
+__global__ __launch_bounds__(kThreads, 2) void gmm_logits_split_kernel(
     int R, int M, int d, const float* __restrict__ X, int64_t ldx,
     const uint16_t* __restrict__ musplit, int ksplit, float* __restrict__ part,
     double* __restrict__ xsq, const int* gate) {
@@ -237,43 +241,55 @@ __global__ __launch_bounds__(kThreads, 4) void gmm_logits_split_kernel(
   const int nsplit = gridDim.x, nrt = gridDim.y;
   const int lin = xcd_tile(nsplit * nrt * gridDim.z);
   const int s = lin % nsplit, rt = (lin / nsplit) % nrt, ct = lin / (nsplit * nrt);
-  const int r0 = rt * TILE, c0 = ct * TILE;
+  const int r0 = rt * kSplitRows, c0 = ct * TILE;
   const int kbeg = s * ksplit, kend = min(d, kbeg + ksplit);
   const size_t plane = (size_t)M * d;
-  const __amdgpu_buffer_rsrc_t va = tile_rows(X, ldx, R, r0);
+  // rows past R read as zero from the view
+  const __amdgpu_buffer_rsrc_t va =
+      buf_view(X + (int64_t)r0 * ldx, (int64_t)max(0, min(R - r0, kSplitRows)) * ldx * 4);
   const __amdgpu_buffer_rsrc_t vb[3] = {split::plane_rows(musplit, d, M, c0),
                                         split::plane_rows(musplit + plane, d, M, c0),
                                         split::plane_rows(musplit + 2 * plane, d, M, c0)};
-  split::Acc acc;
-  split::zero(acc);
-  double sq = 0.0;
-  split::AChunk ra;
+  split::Acc acc[kSplitRB];
+  double sq[kSplitRB];
+#pragma unroll
+  for (int r = 0; r < kSplitRB; ++r) {
+    split::zero(acc[r]);
+    sq[r] = 0.0;
+  }
+  split::AChunk ra[kSplitRB];
   split::BChunk rb;
   split::load_b(vb, d, kbeg, rb);
-  split::load_a(va, ldx, kbeg, ra);
+  split::load_a<kSplitRB>(va, ldx, kbeg, ra);
   uint16_t* lds = reinterpret_cast<uint16_t*>(&sm);
   const bool want_sq = ct == 0;
   if (want_sq)
-    split::tile_run<true>(lds, va, ldx, vb, d, kbeg, kend, ra, rb, acc, sq);
+    split::tile_run<true, kSplitRB>(lds, va, ldx, vb, d, kbeg, kend, ra, rb, acc, sq);
   else
-    split::tile_run<false>(lds, va, ldx, vb, d, kbeg, kend, ra, rb, acc, sq);
+    split::tile_run<false, kSplitRB>(lds, va, ldx, vb, d, kbeg, kend, ra, rb, acc, sq);
   float* ps = part + (int64_t)s * R * M;
 #pragma unroll
-  for (int b = 0; b < 4; ++b) {
-    const int col = c0 + split::out_col(b);
+  for (int r = 0; r < kSplitRB; ++r)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int row = r0 + split::out_row(j);
-      if (row < R && col < M) ps[(int64_t)row * M + col] = acc.c[b][j];
+    for (int b = 0; b < 4; ++b) {
+      const int col = c0 + split::out_col(b);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int row = r0 + split::out_row<kSplitRB>(r, j);
+        if (row < R && col < M) ps[(int64_t)row * M + col] = acc[r].c[b][j];
+      }
     }
-  }
   if (want_sq) {
     // the four lanes of a row are l % 16 + 16 q
-    sq += __shfl_xor(sq, 16);
-    sq += __shfl_xor(sq, 32);
-    const int lane = threadIdx.x & 63;
-    const int row = r0 + 16 * (threadIdx.x >> 6) + lane;
-    if (lane < 16 && row < R) xsq[(int64_t)s * R + row] = sq;
+    const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+#pragma unroll
+    for (int r = 0; r < kSplitRB; ++r) {
+      double t = sq[r];
+      t += __shfl_xor(t, 16);
+      t += __shfl_xor(t, 32);
+      const int row = r0 + 16 * (kSplitRB * w + r) + lane;
+      if (lane < 16 && row < R) xsq[(int64_t)s * R + row] = t;
+    }
   }
 }
 
@@ -537,32 +553,32 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_split_kernel(
   const __amdgpu_buffer_rsrc_t vb[3] = {split::plane_rows(muTs, M, d, c0),
                                         split::plane_rows(muTs + plane, M, d, c0),
                                         split::plane_rows(muTs + 2 * plane, M, d, c0)};
-  split::AChunk sa;
+  split::AChunk sa[1];
   split::BChunk sb;
   split::load_b(vb, M, 0, sb);
-  split::load_a(va, M, 0, sa);
+  split::load_a<1>(va, M, 0, sa);
   // the epilogue's x, whose latency then overlaps the contraction
   float xv[4][4];
 #pragma unroll
   for (int b = 0; b < 4; ++b)
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int row = r0 + split::out_row(j), col = c0 + split::out_col(b);
+      const int row = r0 + split::out_row<1>(0, j), col = c0 + split::out_col(b);
       xv[b][j] = row < R && col < d ? X[(int64_t)row * ldx + col] : 0.f;
     }
-  split::Acc acc;
-  split::zero(acc);
-  double unused = 0.0;
-  split::tile_run<false>(reinterpret_cast<uint16_t*>(&sm), va, M, vb, M, 0, M, sa, sb, acc, unused);
+  split::Acc acc[1];
+  split::zero(acc[0]);
+  double unused[1] = {0.0};
+  split::tile_run<false, 1>(reinterpret_cast<uint16_t*>(&sm), va, M, vb, M, 0, M, sa, sb, acc, unused);
 #pragma unroll
   for (int b = 0; b < 4; ++b) {
     const int col = c0 + split::out_col(b);
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
-      const int lr = split::out_row(j), row = r0 + lr;
+      const int lr = split::out_row<1>(0, j), row = r0 + lr;
       if (row < R && col < d) {
         const float c1 = rc[3 * lr], c2 = rc[3 * lr + 1], rho = rc[3 * lr + 2];
-        const float sc = acc.c[b][j] - rho * xv[b][j];
+        const float sc = acc[0].c[b][j] - rho * xv[b][j];
         mq[(int64_t)row * ldq + col] = c1 * xv[b][j] + c2 * sc;
         if (score) score[(int64_t)row * lds + col] = sc;
       }
@@ -621,7 +637,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
   // epilogue, whose latency then overlaps the contraction
   const __amdgpu_buffer_rsrc_t va = tile_rows(P, M, R, r0);
   float4 ra[4], rb[4];
-  split::AChunk sa;
+  split::AChunk sa[1];
   split::BChunk sb;
   __amdgpu_buffer_rsrc_t vbs[3];
   if constexpr (VEC) {
@@ -629,7 +645,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
 #pragma unroll
     for (int p = 0; p < 3; ++p) vbs[p] = split::plane_rows(muTs + p * plane, M, d, c0);
     split::load_b(vbs, M, 0, sb);
-    split::load_a(va, M, 0, sa);
+    split::load_a<1>(va, M, 0, sa);
   } else {
     load_chunk(P, M, R, r0, 0, M, ra);
     load_chunk(muT, M, d, c0, 0, M, rb);
@@ -684,16 +700,17 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     }
   }
   if constexpr (VEC) {
-    split::Acc acc;
-    split::zero(acc);
-    double unused = 0.0;
-    split::tile_run<false>(reinterpret_cast<uint16_t*>(&sm), va, M, vbs, M, 0, M, sa, sb, acc,
-                           unused);
+    split::Acc acc[1];
+    split::zero(acc[0]);
+    double unused[1] = {0.0};
+    split::tile_run<false, 1>(reinterpret_cast<uint16_t*>(&sm), va, M, vbs, M, 0, M, sa, sb, acc,
+                              unused);
     __syncthreads();  // every wavefront is done with the operand planes
 #pragma unroll
     for (int b = 0; b < 4; ++b)
 #pragma unroll
-      for (int j = 0; j < 4; ++j) sm.a[split::out_row(j) * LDW + split::out_col(b)] = acc.c[b][j];
+      for (int j = 0; j < 4; ++j)
+        sm.a[split::out_row<1>(0, j) * LDW + split::out_col(b)] = acc[0].c[b][j];
   } else {
     f32x16 acc;
 #pragma unroll
@@ -916,15 +933,16 @@ Plan make_plan(const Target& t, int R) {
 // aligned and a tile's rows fit 32-bit offsets).
 hipError_t logits_launch(const Target& t, const Plan& p, int R, const float* x, int64_t ldx,
                          float* part, double* xsq, hipStream_t s, const int* gate) {
-  dim3 g1(p.S, (R + TILE - 1) / TILE, (t.M + TILE - 1) / TILE);
   const bool vec = t.d % KC == 0 && ldx % 4 == 0 && aligned16(x) &&
-                   (int64_t)TILE * ldx * 4 < ((int64_t)1 << 31) &&
-                   (int64_t)TILE * t.d * 4 < ((int64_t)1 << 31);
+                   (int64_t)kSplitRows * ldx * 4 < ((int64_t)1 << 31) &&
+                   (int64_t)TILE * t.d * 2 < ((int64_t)1 << 31);
   if (vec)
-    return launch_timed("gmm_logits", gmm_logits_split_kernel, g1, dim3(kThreads), s, R, t.M, t.d,
-                        x, ldx, t.mu_split, p.ksplit, part, xsq, gate);
-  return launch_timed("gmm_logits", gmm_logits_kernel, g1, dim3(kThreads), s, R, t.M, t.d, x, ldx,
-                      t.mu, p.ksplit, part, xsq, gate);
+    return launch_timed("gmm_logits", gmm_logits_split_kernel,
+                        dim3(p.S, (R + kSplitRows - 1) / kSplitRows, (t.M + TILE - 1) / TILE),
+                        dim3(kThreads), s, R, t.M, t.d, x, ldx, t.mu_split, p.ksplit, part, xsq, gate);
+  return launch_timed("gmm_logits", gmm_logits_kernel,
+                      dim3(p.S, (R + TILE - 1) / TILE, (t.M + TILE - 1) / TILE), dim3(kThreads), s,
+                      R, t.M, t.d, x, ldx, t.mu, p.ksplit, part, xsq, gate);
 }
 
 }  // namespace
