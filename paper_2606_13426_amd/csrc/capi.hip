@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <chrono>
 #include <map>
 #include <mutex>
 #include <string>
@@ -555,7 +556,7 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
   // hold the next round's first kernel back by several microseconds.
   int32_t* host_act = nullptr;
   int32_t* host_act_dev = nullptr;
-  constexpr int kLag = 3, kSlots = kLag + 1;
+  constexpr int kLag = 3, kSlots = kLag + 1, kQuietMs = 20;
   SD_HIP(hipHostMalloc(reinterpret_cast<void**>(&host_act), sizeof(int32_t) * kSlots, hipHostMallocDefault));
   if (hipHostGetDevicePointer(reinterpret_cast<void**>(&host_act_dev), host_act, 0) != hipSuccess) {
     (void)hipHostFree(host_act);
@@ -605,11 +606,16 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
     const int back = r - kLag;
     if (back >= 0) {
       // round back + 1's scan (enqueued) publishes round back's flag; the wait
-      // ends on the tag, or on an error or a drained stream reported by the runtime
+      // ends on the tag, or on an error or a drained stream reported by the
+      // runtime.  The runtime is asked only after kQuietMs without the tag: a
+      // stream query queues a marker whose system-scope release holds the
+      // next kernel back by several microseconds.
       volatile int32_t* slot = pub + back % kSlots;
       int32_t v;
+      auto next_query = std::chrono::steady_clock::now() + std::chrono::milliseconds(kQuietMs);
       for (uint32_t spin = 1; ((v = *slot) >> 1) != back; ++spin) {
-        if ((spin & 1023u) == 0) {
+        if ((spin & 1023u) == 0 && std::chrono::steady_clock::now() >= next_query) {
+          next_query = std::chrono::steady_clock::now() + std::chrono::milliseconds(kQuietMs);
           const hipError_t q = hipStreamQuery(s);
           // not-ready is a status, not a failure: keep it out of the launch checks
           if (q == hipErrorNotReady) {

@@ -221,13 +221,16 @@ inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
 #ifdef __HIPCC__
 // Workgroups are dispatched round-robin over the eight XCDs, each with its own
-// L2.  Remap the linear workgroup id so that XCD x works on the contiguous
-// x-th eighth of the tile space (tiles that share operand rows stay on one
-// L2); the innermost tile index is the fastest-varying one.
+// L2.  Remap the linear workgroup id so that XCD x works on a contiguous
+// range of the tile space (tiles that share operand rows stay on one L2); the
+// innermost tile index is the fastest-varying one.  Workgroup L runs on XCD
+// x = L % 8 as its (L / 8)-th; with total = 8 q + r, XCDs x < r receive q + 1
+// workgroups and the others q, so XCD x takes the range starting at
+// x q + min(x, r) (a bijection of [0, total)).
 __device__ __forceinline__ int xcd_tile(int total) {
   const int L = blockIdx.x + gridDim.x * (blockIdx.y + gridDim.y * blockIdx.z);
-  if (total % 8 != 0) return L;
-  return (L % 8) * (total / 8) + L / 8;
+  const int x = L % 8, q = total / 8, r = total % 8;
+  return x * q + min(x, r) + L / 8;
 }
 #endif
 
