@@ -88,7 +88,7 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_logits_bf16_kernel(
 // the aligned case: d a whole number of chunks, rows of X 16-byte aligned.
 // Grid and tile order as gmm_logits_bf16_kernel; the ||x||^2 partials come
 // from the column tile 0 workgroups.
-__global__ __launch_bounds__(bf16w::kThreads, 1) void gmm_logits_bf16_wide_kernel(
+__global__ __launch_bounds__(bf16w::kThreads, 2) void gmm_logits_bf16_wide_kernel(
     int R, int M, int d, const float* __restrict__ X, int64_t ldx,
     const uint16_t* __restrict__ mu, int ksplit, float* __restrict__ part,
     double* __restrict__ xsq, const int* gate) {
@@ -100,11 +100,11 @@ __global__ __launch_bounds__(bf16w::kThreads, 1) void gmm_logits_bf16_wide_kerne
   const int ct = lin % nct, rt = (lin / nct) % nrt, s = lin / (nct * nrt);
   const int r0 = rt * WT, c0 = ct * WT;
   const int kbeg = s * ksplit, kend = min(d, kbeg + ksplit);
-  bf16w::f32x16 acc[4][4];
+  bf16w::f32x16 acc[4][2];
   bf16w::zero(acc);
-  double sq[16];
+  double sq[8];
 #pragma unroll
-  for (int h = 0; h < 16; ++h) sq[h] = 0.0;
+  for (int h = 0; h < 8; ++h) sq[h] = 0.0;
   const __amdgpu_buffer_rsrc_t va = bf16w::tile_view(X, ldx, R, r0);
   const __amdgpu_buffer_rsrc_t vb = bf16w::tile_view(mu, (int64_t)d, M, c0);
   const bool want_sq = ct == 0;
@@ -114,7 +114,7 @@ __global__ __launch_bounds__(bf16w::kThreads, 1) void gmm_logits_bf16_wide_kerne
     bf16w::tile<false, float>(sm, va, ldx, vb, d, kbeg, kend, acc, sq);
   float* ps = part + (int64_t)s * R * M;
 #pragma unroll
-  for (int qb = 0; qb < 4; ++qb) {
+  for (int qb = 0; qb < 2; ++qb) {
     const int col = c0 + bf16w::out_col(qb);
     if (col >= M) continue;
 #pragma unroll
@@ -128,13 +128,13 @@ __global__ __launch_bounds__(bf16w::kThreads, 1) void gmm_logits_bf16_wide_kerne
   if (want_sq) {
     // the 16 threads that loaded a row are 16 consecutive lanes
 #pragma unroll
-    for (int h = 0; h < 16; ++h) {
+    for (int h = 0; h < 8; ++h) {
       double t = sq[h];
       t += __shfl_xor(t, 1);
       t += __shfl_xor(t, 2);
       t += __shfl_xor(t, 4);
       t += __shfl_xor(t, 8);
-      const int row = r0 + (threadIdx.x >> 4) + 16 * h;
+      const int row = r0 + (threadIdx.x >> 4) + 32 * h;
       if ((threadIdx.x & 15) == 0 && row < R) xsq[(int64_t)s * R + row] = t;
     }
   }
