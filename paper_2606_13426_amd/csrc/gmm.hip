@@ -424,6 +424,7 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_quad_kernel(
   const int mc = has ? m0 : 0;  // loads of lanes past M read component 0 (unused)
   // the partials first (independent of the step), then the step's tables
   double dot[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 8
   for (int sp = 0; sp < S; ++sp) {
     const float4 v = *reinterpret_cast<const float4*>(part + ((int64_t)sp * R + rr) * M + mc);
     dot[0] += (double)v.x;
@@ -432,6 +433,7 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_quad_kernel(
     dot[3] += (double)v.w;
   }
   double xs = 0.0;
+#pragma unroll 8
   for (int sp = 0; sp < S; ++sp) xs += xsq[(int64_t)sp * R + rr];
   const int n = step[rr];
   const double a = sched_signal(sc, n), a2 = a * a, hd = 0.5 * (double)d;
@@ -827,10 +829,12 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_small_kernel(
   const int n = step[rr];
   const double a = sched_signal(sc, n), a2 = a * a, hd = 0.5 * (double)d;
   double xs = 0.0;
+#pragma unroll 8
   for (int sp = 0; sp < S; ++sp) xs += xsq[(int64_t)sp * R + rr];
   const int m0 = 4 * q;
   const bool has = m0 < M;
   double dot[4] = {0.0, 0.0, 0.0, 0.0};
+#pragma unroll 8
   for (int sp = 0; sp < S; ++sp) {
     if (has) {
       const float4 v = *reinterpret_cast<const float4*>(part + ((int64_t)sp * R + rr) * M + m0);
@@ -897,18 +901,21 @@ struct Plan {
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Split of the logits GEMM over d: the number of k-chunks per split and the
-// number of splits minimise (workgroups per CU, rounded up) x (chunks per
-// workgroup), i.e. the critical path over 256 compute units, preferring fewer
-// splits on ties.
+// number of splits minimise (rounds of workgroups over 512 slots, two per
+// compute unit) x (chunks per workgroup), i.e. the critical path, preferring
+// fewer splits on ties.
 Plan make_plan(const Target& t, int R) {
   Plan p{};
-  const int tiles = ((R + TILE - 1) / TILE) * ((t.M + TILE - 1) / TILE);
+  // the aligned path's tiles (kSplitRows rows, two workgroups per compute
+  // unit); the unaligned kernel takes the same splits
+  const int tiles = ((R + kSplitRows - 1) / kSplitRows) * ((t.M + TILE - 1) / TILE);
   const int nchunks = (t.d + KC - 1) / KC;
+  constexpr int kSlots = 512, kMaxSplits = 32;
   int best_cost = 1 << 30, best_per = nchunks;
-  for (int S = 1; S <= 8 && S <= nchunks; ++S) {
+  for (int S = 1; S <= kMaxSplits && S <= nchunks; ++S) {
     const int per = (nchunks + S - 1) / S;
     const int splits = (nchunks + per - 1) / per;
-    const int cost = ((tiles * splits + 255) / 256) * per;
+    const int cost = ((tiles * splits + kSlots - 1) / kSlots) * per;
     if (cost < best_cost) {
       best_cost = cost;
       best_per = per;
