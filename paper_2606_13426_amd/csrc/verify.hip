@@ -112,13 +112,18 @@ __device__ __forceinline__ double log_cdf(double x, double la, double v, double 
 }
 
 // Inverse of Psi_alpha at u, with all 64 lanes of the wavefront: the doubling
-// of Alg. 7 for all 64 candidate lower ends at once (lane i tests u* - 2^i),
-// then a 64-way multisection (lane i evaluates log Psi at the i+1-th of 65
-// points) until the bracket is 1e-8 (relative) wide, then a linear
-// interpolation of log Psi between the bracket's ends, whose values the lanes
-// already hold: inside so narrow a bracket its error is far below the
-// bracket width except next to u*, where the density vanishes (there it is
-// at most the width).
+// of Alg. 7 for 63 candidate lower ends at once (lane i tests u* - 2^i), then
+// a 64-way multisection (lane i evaluates log Psi at the i+1-th of 65
+// points).  After the second and later multisection passes the four points
+// around the crossing (the pass's points and the bracket's ends) give the
+// cubic inverse interpolant of log Psi at log u; it is taken when it lies in
+// the new bracket and agrees with both quadratic interpolants to 1e-13
+// (relative), i.e. where log Psi is smooth on the scale of the points --
+// typically after the second or third pass.  Otherwise the multisection goes
+// on until the bracket is 1e-8 (relative) wide and a linear interpolation of
+// log Psi between its ends, whose values the lanes already hold, closes it:
+// its error is far below the bracket width except next to u*, where the
+// density vanishes (there it is at most the width).
 __device__ double usample_exact(double u, double la, double v, int lane) {
   const double us = la / v + 0.5 * v;
   const double logu = log(u);
@@ -140,6 +145,35 @@ __device__ double usample_exact(double u, double la, double v, int lane) {
     const int cnt = __popcll(below);
     const double nlo = __shfl(x, cnt > 0 ? cnt - 1 : 0), nflo = __shfl(fx, cnt > 0 ? cnt - 1 : 0);
     const double nhi = __shfl(x, cnt < 64 ? cnt : 63), nfhi = __shfl(fx, cnt < 64 ? cnt : 63);
+    // the points in order: e = 0 the bracket's low end, e = i + 1 lane i's
+    // point, e = 65 its high end; the crossing lies between e = cnt and cnt + 1
+    const int e0 = min(max(cnt - 1, 0), 62);
+    double px[4], pf[4];  // points and their log Psi, increasing
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = e0 + q;
+      const int src = min(max(e - 1, 0), 63);
+      const double sx = __shfl(x, src), sf = __shfl(fx, src);
+      px[q] = e == 0 ? lo : e == 65 ? hi : sx;
+      pf[q] = e == 0 ? flo : e == 65 ? fhi : sf;
+    }
+    // (after the first pass the points are still too far apart to pass the test)
+    if (it > 0 && isfinite(pf[0]) && isfinite(pf[3]) && pf[0] < pf[1] && pf[1] < pf[2] &&
+        pf[2] < pf[3]) {
+      // Lagrange weights in log Psi at log u, from the six reciprocal differences
+      const double r01 = 1.0 / (pf[0] - pf[1]), r02 = 1.0 / (pf[0] - pf[2]), r03 = 1.0 / (pf[0] - pf[3]);
+      const double r12 = 1.0 / (pf[1] - pf[2]), r13 = 1.0 / (pf[1] - pf[3]), r23 = 1.0 / (pf[2] - pf[3]);
+      const double d0 = logu - pf[0], d1 = logu - pf[1], d2 = logu - pf[2], d3 = logu - pf[3];
+      const double x3 = px[0] * (d1 * d2 * d3) * (r01 * r02 * r03) - px[1] * (d0 * d2 * d3) * (r01 * r12 * r13) +
+                        px[2] * (d0 * d1 * d3) * (r02 * r12 * r23) - px[3] * (d0 * d1 * d2) * (r03 * r13 * r23);
+      const double q0 = px[0] * (d1 * d2) * (r01 * r02) - px[1] * (d0 * d2) * (r01 * r12) +
+                        px[2] * (d0 * d1) * (r02 * r12);
+      const double q1 = px[1] * (d2 * d3) * (r12 * r13) - px[2] * (d1 * d3) * (r12 * r23) +
+                        px[3] * (d1 * d2) * (r13 * r23);
+      const double blo = cnt > 0 ? nlo : lo, bhi = cnt < 64 ? nhi : hi;
+      if (fmax(fabs(x3 - q0), fabs(x3 - q1)) <= 1e-13 * fmax(1.0, fabs(x3)) && x3 >= blo && x3 <= bhi)
+        return x3;
+    }
     if (cnt > 0) {
       lo = nlo;
       flo = nflo;
