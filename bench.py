@@ -36,6 +36,8 @@ METRIC = "verified chain-steps/sec + mean accepted steps per block; % MFMA / HBM
 # gives; profiles/sampler_pixel3072_hbm_traffic.md), valid while the kernel's
 # sources (its translation unit, every library header and the C header) have
 # the digest (source_digest(unit)) recorded with them.
+PROFILE_EVERY = 4  # the timed runs' event sample of the dominant kernel's launches
+
 MEASURED_TRAFFIC = {
     ("pixel3072", "gmm_mean_lr"): dict(bytes=(141.5 + 122.0) * 1e6, unit="gmm.hip",
                                        sources="ca76030a8313b4e60002925056a1e3a410dbe14d"),
@@ -155,7 +157,11 @@ def run_sampler_bench(lib, name, mode, steps, warmup, profile):
             only = max(breakdown, key=lambda n: breakdown[n][1])
     torch.cuda.synchronize()
     if profile:
+        # the timed runs bracket every PROFILE_EVERY-th launch of the dominant
+        # kernel: a systematic sample over the timed region whose events cost
+        # the stream a quarter of what timing every launch does
         lib.sd_profile_only(only)
+        lib.sd_profile_every(PROFILE_EVERY)
         lib.sd_profile_enable(True)
     stats = []
     t0 = time.perf_counter()
@@ -168,14 +174,16 @@ def run_sampler_bench(lib, name, mode, steps, warmup, profile):
     torch.cuda.synchronize()
     t1 = time.perf_counter()
     prof = lib.sd_profile_read() if profile else {}
+    seen = lib.sd_profile_seen(only) if profile else 0
     if profile:
         lib.sd_profile_enable(False)
         lib.sd_profile_only(None)
+        lib.sd_profile_every(1)
     sec = (t1 - t0) / steps
     st = stats[0]
     be = st["steps"] / st["chain_rounds"]
     act, rows_v, rows_t = _counts_from_trace(trace0, N, K)
-    return dict(B=B, K=K, N=N, d=d, M=M, sec=sec, be=be, rounds=st["rounds"], prof=prof,
+    return dict(B=B, K=K, N=N, d=d, M=M, sec=sec, be=be, rounds=st["rounds"], prof=prof, seen=seen,
                 breakdown=breakdown,
                 act=act, rows_verified=rows_v, rows_target=rows_t, tau_hist=st["tau_hist"][: K + 2],
                 steps=steps)
@@ -190,10 +198,17 @@ def roofline_of(res, steps):
     name = max(prof, key=lambda n: prof[n][1])
     table = {}
     sources = dict(res["breakdown"])
-    sources[name] = prof[name]
+    # the timed runs timed a systematic sample of the dominant kernel's
+    # launches: its total time over all of them is the sample's mean duration
+    # times the launches seen
+    timed, ms_timed = prof[name]
+    seen = max(res.get("seen", 0), timed)
+    sources[name] = (seen, ms_timed * seen / max(timed, 1))
     for kname, (launches, ms) in sources.items():
         runs = steps if kname == name else 1
         entry = dict(launches=launches, avg_us=1e3 * ms / max(launches, 1), total_ms=ms)
+        if kname == name:
+            entry.update(timed_launches=timed)
         w = algorithmic_work(kname, res["B"], res["K"], res["d"], res["M"], res["act"],
                              res["rows_verified"], runs)
         if w is not None:
@@ -214,7 +229,7 @@ def roofline_of(res, steps):
                 unit=e.get("unit"), frac=e.get("frac"), traffic=None,
                 algorithmic_per_launch=per(e.get("algorithmic_bytes") if e.get("bound") == "hbm"
                                            else e.get("algorithmic_flops")),
-                avg_launch_us=e["avg_us"], launches=e["launches"])
+                avg_launch_us=e["avg_us"], launches=e["launches"], timed_launches=timed)
     return roof, table
 
 

@@ -291,7 +291,8 @@ sd_status sd_run_plain_em(sd_target target, int32_t B, uint64_t seed, float* y_o
  * Per-kernel timing with HIP events recorded around every launch on the
  * launch's own stream.  sd_profile_enable(1) clears and starts collection,
  * (0) stops it.  sd_profile_read waits for the recorded events and returns up
- * to `capacity` entries (host out), *count = number of kernels seen. */
+ * to `capacity` entries (host out), *count = number of kernels seen; its
+ * `launches` counts the timed launches. */
 typedef struct {
   char name[48];
   int64_t launches;
@@ -302,6 +303,13 @@ sd_status sd_profile_enable(int32_t on);
 /* Restrict collection to launches of the kernel named `name` (host string,
  * copied); NULL times every kernel again. */
 sd_status sd_profile_only(const char* name);
+/* Time only every n-th launch of each profiled kernel (n >= 1, default 1;
+ * counted per kernel name from the last sd_profile_enable(1)): a systematic
+ * sample that keeps the events' cost off most launches.  SD_EINVAL for n < 1. */
+sd_status sd_profile_every(int32_t n);
+/* Launches of the kernel `name` (host string) seen while collecting, timed or
+ * not (host out *count; 0 for a kernel not profiled). */
+sd_status sd_profile_seen(const char* name, int64_t* count);
 sd_status sd_profile_read(sd_kernel_stat* out, int32_t capacity, int32_t* count);
 
 /* ----------------------------------------------------------- test hooks --

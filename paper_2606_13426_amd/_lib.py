@@ -85,6 +85,8 @@ SIGNATURES = [
     ("sd_run_plain_em", c_int32, [P, c_int32, c_uint64, P, P, c_size_t, P]),
     ("sd_profile_enable", c_int32, [c_int32]),
     ("sd_profile_only", c_int32, [c_char_p]),
+    ("sd_profile_every", c_int32, [c_int32]),
+    ("sd_profile_seen", c_int32, [c_char_p, ctypes.POINTER(c_int64)]),
     ("sd_profile_read", c_int32, [ctypes.POINTER(sd_kernel_stat), c_int32, ctypes.POINTER(c_int32)]),
     ("sd_philox_words", c_int32, [c_uint64, c_int32, P, P, P]),
     ("sd_philox_normals", c_int32, [c_uint64, c_uint32, c_uint32, c_uint32, c_uint32, c_int32, P, P]),
@@ -328,6 +330,16 @@ def sd_profile_enable(on=True):
 
 def sd_profile_only(name=None):
     _check(load().sd_profile_only(None if name is None else name.encode()), "sd_profile_only")
+
+
+def sd_profile_every(n):
+    _check(load().sd_profile_every(int(n)), "sd_profile_every")
+
+
+def sd_profile_seen(name):
+    n = c_int64()
+    _check(load().sd_profile_seen(name.encode(), ctypes.byref(n)), "sd_profile_seen")
+    return n.value
 
 
 def sd_profile_read():

@@ -58,10 +58,14 @@ void drain_locked() {
 }  // namespace
 
 std::string g_prof_only;
+int64_t g_prof_every = 1;
+std::map<std::string, int64_t> g_prof_seen;  // launches of each profiled kernel so far
 
 bool prof_on(const char* name) {
   if (!g_prof) return false;
-  return g_prof_only.empty() || g_prof_only == name;
+  if (!(g_prof_only.empty() || g_prof_only == name)) return false;
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  return g_prof_seen[name]++ % g_prof_every == 0;
 }
 
 void prof_events(hipEvent_t* a, hipEvent_t* b) {
@@ -733,6 +737,7 @@ sd_status sd_profile_enable(int32_t on) {
   if (on) {
     drain_locked();
     g_stats.clear();
+    g_prof_seen.clear();
   }
   g_prof = on != 0;
   return SD_OK;
@@ -741,6 +746,22 @@ sd_status sd_profile_enable(int32_t on) {
 sd_status sd_profile_only(const char* name) {
   std::lock_guard<std::mutex> lk(g_prof_mu);
   g_prof_only = name ? name : "";
+  return SD_OK;
+}
+
+sd_status sd_profile_every(int32_t n) {
+  SD_CHECK_ARG(n >= 1, "sd_profile_every: n < 1");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  g_prof_every = n;
+  g_prof_seen.clear();
+  return SD_OK;
+}
+
+sd_status sd_profile_seen(const char* name, int64_t* count) {
+  SD_CHECK_ARG(name && count, "sd_profile_seen: NULL pointer argument");
+  std::lock_guard<std::mutex> lk(g_prof_mu);
+  const auto it = g_prof_seen.find(name);
+  *count = it == g_prof_seen.end() ? 0 : it->second;
   return SD_OK;
 }
 

@@ -118,6 +118,17 @@ def test_invalid_arguments_rejected_without_gpu(lib):
     assert lib.sd_target_mean_workspace(null, 4) == 0
 
 
+def test_profile_controls_without_gpu(lib):
+    # the profiling switches are host state: no HIP call, no device needed
+    _expect_einval(lib.sd_profile_every(0), "n < 1")
+    _expect_einval(lib.sd_profile_seen(None, None), "NULL")
+    assert lib.sd_profile_every(4) == _lib.SD_OK
+    assert lib.sd_profile_enable(1) == _lib.SD_OK
+    assert _lib.sd_profile_seen("gmm_mean_lr") == 0
+    assert lib.sd_profile_enable(0) == _lib.SD_OK
+    assert lib.sd_profile_every(1) == _lib.SD_OK
+
+
 def test_strides_validated(lib):
     good = _lib.schedule(10)
     p = ctypes.c_void_p(256)  # never dereferenced: validation fails first
