@@ -6,7 +6,8 @@
 //   residual  y_i = m^q_i + sigma G_i + rcoef (m^p_i - m^q_i)     (Alg. 5 with e.G known)
 //             or y_i = yhat_tau,i - rcoef (m^p_i - m^q_i)          (Alg. 4, reflection)
 //             or the full-accept target draw, or the last draft at step N (Alg. 8);
-//   commit    k <- min(k + tau, N), round <- round + 1 (one thread per chain);
+//   commit    k <- min(k + tau, N), round <- round + 1 (one thread per chain),
+//             the new state into x row 0 (and into y once the chain is done);
 //   draft     the next round's Free-Drafter block from y_i, whose cached score
 //             is that of row min(tau, K_b) of this round (Sec. 3.3), recovered
 //             from the same round's (x, m^q) rows.
@@ -126,7 +127,10 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
   } else {
     load4(xb + (int64_t)kb * d, cnt, vec, yv);
   }
-  store4(y + (int64_t)b * d + e0, cnt, vec, yv);
+  // y holds the state only where something reads it before the next round's
+  // advance: the Frozen Drafter's draft (from y) and the run's output once the
+  // chain has reached step N; otherwise x row 0 carries it
+  if (frozen || knew >= N) store4(y + (int64_t)b * d + e0, cnt, vec, yv);
   if (knew >= N) return;
   if (frozen) {
     store4(xb, cnt, vec, yv);
