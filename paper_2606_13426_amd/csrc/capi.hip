@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <atomic>
 #include <chrono>
 #include <map>
 #include <mutex>
@@ -37,7 +38,7 @@ struct Stat {
   double ms = 0.0;
 };
 std::mutex g_prof_mu;
-bool g_prof = false;
+std::atomic<bool> g_prof{false};  // read without the lock on every launch
 std::vector<PendingEv> g_pending;
 std::vector<hipEvent_t> g_pool;
 std::map<std::string, Stat> g_stats;
@@ -62,9 +63,9 @@ int64_t g_prof_every = 1;
 std::map<std::string, int64_t> g_prof_seen;  // launches of each profiled kernel so far
 
 bool prof_on(const char* name) {
-  if (!g_prof) return false;
-  if (!(g_prof_only.empty() || g_prof_only == name)) return false;
+  if (!g_prof.load(std::memory_order_relaxed)) return false;
   std::lock_guard<std::mutex> lk(g_prof_mu);
+  if (!g_prof || !(g_prof_only.empty() || g_prof_only == name)) return false;
   return g_prof_seen[name]++ % g_prof_every == 0;
 }
 
