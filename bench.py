@@ -39,9 +39,20 @@ METRIC = "verified chain-steps/sec + mean accepted steps per block; % MFMA / HBM
 PROFILE_EVERY = 4  # the timed runs' event sample of the dominant kernel's launches
 
 MEASURED_TRAFFIC = {
+    ("verify12288", "logratio_reduce"): dict(bytes=(19344.1 + 8.5) * 1e6, unit="verify.hip",
+                                             sources="def2d1763c10052cf6d824bc66a2e783ed214580"),
     ("pixel3072", "gmm_mean_lr"): dict(bytes=(141.8 + 122.0) * 1e6, unit="gmm.hip",
                                        sources="50e3aa3216c7c400ab4cb6782b75779b51406317"),
 }
+
+
+def measured_traffic(workload, kernel):
+    """HBM bytes per launch from the committed counters, while the kernel's
+    sources are those the counters were taken from; else None."""
+    meas = MEASURED_TRAFFIC.get((workload, kernel))
+    if meas and meas["sources"] == source_digest(meas["unit"]):
+        return meas["bytes"]
+    return None
 
 
 def source_digest(unit):
@@ -413,7 +424,8 @@ def verify_bench(lib, steps, warmup):
                 logratio=dict(bound="hbm", achieved=algo / (lr_ms / lr_launches * 1e-3) / 1e9,
                               peak=HBM_PEAK_GBS, unit="GB/s",
                               frac=algo / (lr_ms / lr_launches * 1e-3) / 1e9 / HBM_PEAK_GBS,
-                              avg_launch_us=1e3 * lr_ms / lr_launches),
+                              traffic=measured_traffic("verify12288", "logratio_reduce"),
+                              algorithmic_per_launch=algo, avg_launch_us=1e3 * lr_ms / lr_launches),
                 pass_GBps=(algo + res_bytes) / sec / 1e9,
                 kernels={k: dict(launches=v[0], avg_us=1e3 * v[1] / max(v[0], 1)) for k, v in prof.items()})
 
@@ -506,12 +518,22 @@ def main():
     ap.add_argument("--library-gemms", action="store_true",
                     help="only time the workloads' denoiser GEMM shapes through the vendor library "
                          "(torch.mm) and exit")
+    ap.add_argument("--verify-only", action="store_true",
+                    help="only run the verification-only workload (verify12288: sd_verify_block + "
+                         "sd_sample_residual) and exit")
     ap.add_argument("--variants", action="store_true",
                     help="only run the variants (reflection / decomposition / block at three "
                          "temperatures, the Frozen Drafter, the plain EM chain) on --workload and exit")
     args = ap.parse_args()
     if args.library_gemms:
         print(json.dumps(dict(library_gemms=library_gemms())))
+        return
+    if args.verify_only:
+        import torch
+        from paper_2606_13426_amd import _lib as lib
+        lib.load()
+        assert torch.cuda.is_available(), "bench.py needs a GPU"
+        print(json.dumps(dict(verify_only=verify_bench(lib, args.steps, args.warmup))))
         return
     if args.variants:
         import torch
@@ -557,9 +579,8 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     res = run_sampler_bench(lib, args.workload, lib.SD_BLOCK, args.steps, args.warmup, profile=True)
     roof, table = roofline_of(res, args.steps)
-    meas = MEASURED_TRAFFIC.get((args.workload, roof["kernel"])) if roof else None
-    if roof and meas and meas["sources"] == source_digest(meas["unit"]):
-        roof["traffic"] = meas["bytes"]
+    if roof:
+        roof["traffic"] = measured_traffic(args.workload, roof["kernel"])
     line = dict(metric=METRIC, value=res["B"] * res["N"] / res["sec"], unit="chain-steps/s", n_gpus=1,
                 steps=args.steps, warmup=args.warmup, ms_per_step=1e3 * res["sec"], higher_is_better=True,
                 scaling="weak", vs_baseline=None, dtype=_dtype(args.workload), data="synthetic",
