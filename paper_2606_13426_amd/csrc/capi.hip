@@ -77,7 +77,10 @@ void prof_events(hipEvent_t* a, hipEvent_t* b) {
       *e = g_pool.back();
       g_pool.pop_back();
     } else {
-      (void)hipEventCreate(e);
+      // timing only: no system-scope fence (cache writeback and invalidation)
+      // when the event is recorded, so the timed launch and the work after it
+      // run as they would untimed
+      (void)hipEventCreateWithFlags(e, hipEventDisableSystemFence);
     }
   }
 }
