@@ -106,12 +106,18 @@ __device__ __forceinline__ void store(uint16_t* lds, const Chunk<uint16_t>& c) {
     *reinterpret_cast<uint4*>(&lds[((t >> 3) + 64 * h) * LDH + 8 * (t & 7)]) = c.v[h];
 }
 
-// float64 sum of squares of the float32 values of a chunk, per loaded row.
-__device__ __forceinline__ void add_squares(const Chunk<float>& c, double (&sq)[8]) {
+// Sum of squares of the float32 values of a chunk for the loaded rows h
+// whose bit is set in mask (wavefront-uniform): the four values of a row
+// summed in float32, the chunk partial added in float64.  The float32 partial
+// is within a few ulp (about 2e-7 relative) of the exact one, far inside the
+// bf16 rounding of the same values in the contraction.
+__device__ __forceinline__ void add_squares(const Chunk<float>& c, double (&sq)[8], uint32_t mask) {
 #pragma unroll
-  for (int h = 0; h < 8; ++h)
-    sq[h] += (double)c.v[h].x * c.v[h].x + (double)c.v[h].y * c.v[h].y +
-             (double)c.v[h].z * c.v[h].z + (double)c.v[h].w * c.v[h].w;
+  for (int h = 0; h < 8; ++h) {
+    if (!(mask >> h & 1u)) continue;
+    const float4 v = c.v[h];
+    sq[h] += (double)(v.x * v.x + v.y * v.y + v.z * v.z + v.w * v.w);
+  }
 }
 
 __device__ __forceinline__ bf16x8 frag(const uint16_t* p) {
@@ -153,12 +159,14 @@ __device__ __forceinline__ void zero(f32x16 (&acc)[4][2]) {
 
 // Accumulate the tile of the views va (A rows) and vb (B rows) over the
 // chunks of k in [kbeg, kend) (a whole number of chunks).  With SQ (float32 A
-// only) also the float64 squares of this thread's eight A rows.  The
-// caller's first use of sm after this returns must follow a barrier.
+// only) also the squares of this thread's A rows h selected by sqmask (a
+// runtime mask rather than a second instantiation: one copy of the loop keeps
+// the register allocation and schedule of the plain tile).  The caller's
+// first use of sm after this returns must follow a barrier.
 template <bool SQ, class TA>
 __device__ __forceinline__ void tile(OperandLds (&sm)[2], __amdgpu_buffer_rsrc_t va, int64_t lda,
                                      __amdgpu_buffer_rsrc_t vb, int64_t ldb, int kbeg, int kend,
-                                     f32x16 (&acc)[4][2], double (&sq)[8]) {
+                                     f32x16 (&acc)[4][2], double (&sq)[8], uint32_t sqmask) {
   const int n = (kend - kbeg) / KC;
   if (n <= 0) return;
   Chunk<TA> ra;
@@ -170,7 +178,7 @@ __device__ __forceinline__ void tile(OperandLds (&sm)[2], __amdgpu_buffer_rsrc_t
   auto st = [&](OperandLds& buf) {
     store(buf.a, ra);
     store(buf.b, rb);
-    if constexpr (SQ) add_squares(ra, sq);
+    if constexpr (SQ) add_squares(ra, sq, sqmask);
   };
   ld(0);
   st(sm[0]);

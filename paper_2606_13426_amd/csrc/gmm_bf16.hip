@@ -86,8 +86,10 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_logits_bf16_kernel(
 
 // The logits GEMM on 256 x 256 tiles (one workgroup per compute unit), for
 // the aligned case: d a whole number of chunks, rows of X 16-byte aligned.
-// Grid and tile order as gmm_logits_bf16_kernel; the ||x||^2 partials come
-// from the column tile 0 workgroups.
+// Grid and tile order as gmm_logits_bf16_kernel.  The ||x||^2 partials of a
+// row are taken by one of the column tiles: a thread's loaded rows h (< 8)
+// go to column tile h % nct, so the column tiles (that run side by side)
+// share the work instead of column tile 0 doing all of it.
 __global__ __launch_bounds__(bf16w::kThreads, 2) void gmm_logits_bf16_wide_kernel(
     int R, int M, int d, const float* __restrict__ X, int64_t ldx,
     const uint16_t* __restrict__ mu, int ksplit, float* __restrict__ part,
@@ -107,11 +109,10 @@ __global__ __launch_bounds__(bf16w::kThreads, 2) void gmm_logits_bf16_wide_kerne
   for (int h = 0; h < 8; ++h) sq[h] = 0.0;
   const __amdgpu_buffer_rsrc_t va = bf16w::tile_view(X, ldx, R, r0);
   const __amdgpu_buffer_rsrc_t vb = bf16w::tile_view(mu, (int64_t)d, M, c0);
-  const bool want_sq = ct == 0;
-  if (want_sq)
-    bf16w::tile<true, float>(sm, va, ldx, vb, d, kbeg, kend, acc, sq);
-  else
-    bf16w::tile<false, float>(sm, va, ldx, vb, d, kbeg, kend, acc, sq);
+  uint32_t sqmask = 0;
+#pragma unroll
+  for (int h = 0; h < 8; ++h) sqmask |= (h % nct == ct ? 1u : 0u) << h;
+  bf16w::tile<true, float>(sm, va, ldx, vb, d, kbeg, kend, acc, sq, sqmask);
   float* ps = part + (int64_t)s * R * M;
 #pragma unroll
   for (int qb = 0; qb < 2; ++qb) {
@@ -125,18 +126,17 @@ __global__ __launch_bounds__(bf16w::kThreads, 2) void gmm_logits_bf16_wide_kerne
         if (row < R) ps[(int64_t)row * M + col] = acc[qa][qb][v];
       }
   }
-  if (want_sq) {
-    // the 16 threads that loaded a row are 16 consecutive lanes
+  // the 16 threads that loaded a row are 16 consecutive lanes
 #pragma unroll
-    for (int h = 0; h < 8; ++h) {
-      double t = sq[h];
-      t += __shfl_xor(t, 1);
-      t += __shfl_xor(t, 2);
-      t += __shfl_xor(t, 4);
-      t += __shfl_xor(t, 8);
-      const int row = r0 + (threadIdx.x >> 4) + 32 * h;
-      if ((threadIdx.x & 15) == 0 && row < R) xsq[(int64_t)s * R + row] = t;
-    }
+  for (int h = 0; h < 8; ++h) {
+    if (!(sqmask >> h & 1u)) continue;
+    double t = sq[h];
+    t += __shfl_xor(t, 1);
+    t += __shfl_xor(t, 2);
+    t += __shfl_xor(t, 4);
+    t += __shfl_xor(t, 8);
+    const int row = r0 + (threadIdx.x >> 4) + 32 * h;
+    if ((threadIdx.x & 15) == 0 && row < R) xsq[(int64_t)s * R + row] = t;
   }
 }
 
