@@ -41,7 +41,7 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
     const float* __restrict__ MQ, float* __restrict__ y, int32_t* __restrict__ step,
     double* __restrict__ sigma, int32_t* __restrict__ hist, int64_t* __restrict__ steps,
     int* act_next, int32_t* __restrict__ trace, int r_round, int trace_rounds, bool vec_ok,
-    bool frozen, const int* gate) {
+    bool frozen, bool stream, const int* gate) {
   if (gate && *gate == 0) return;
   const int N = sc.N, K1 = K + 1;
   const int b = blockIdx.y;
@@ -133,7 +133,7 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
   if (frozen || knew >= N) store4(y + (int64_t)b * d + e0, cnt, vec, yv);
   if (knew >= N) return;
   if (frozen) {
-    store4(xb, cnt, vec, yv);
+    store4(xb, cnt, vec, yv, stream);
     return;
   }
   float xcv[4], qcv[4], sv[4];
@@ -143,9 +143,9 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
 #pragma unroll
   for (int c = 0; c < 4; ++c) sv[c] = qcv[c] - cc.x * xcv[c];  // c2_c S_c
   store4(sb, cnt, vec, sv);
-  store4(xb, cnt, vec, yv);
+  store4(xb, cnt, vec, yv, stream);
   draft_rows(sc, coef, K, knew, min(K, N - knew), (uint32_t)b, r + 1u, seed, g, yv, sv, cc.w, xb,
-             d, nullptr, d, cnt, vec);
+             d, nullptr, d, cnt, vec, stream);
 }
 
 }  // namespace
@@ -162,10 +162,11 @@ hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int
   const int ng = (d + 3) / 4;
   dim3 grid((ng + kThreads - 1) / kThreads, B);
   const bool vec = (d % 4 == 0) && aligned16(x) && aligned16(sv) && aligned16(mq) && aligned16(y);
+  const bool stream = stream_rows((int64_t)B * (K + 1) * d * 4);
   return launch_timed("advance", advance_kernel, grid, dim3(kThreads), s, sc, coef, B, K, d, seed,
                       kcur, rcur, crow_cur, cstep_cur, knext, rnext, crow_next, cstep_next, tau, rmode,
                       rcoef, rsig, x, sv, mq, y, step, sigma, hist, steps, act_next, trace, r,
-                      trace_rounds, vec, frozen, gate);
+                      trace_rounds, vec, frozen, stream, gate);
 }
 
 }  // namespace sd

@@ -37,4 +37,12 @@ __device__ __forceinline__ void buf_st4(__amdgpu_buffer_rsrc_t v, uint32_t off, 
   __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, x), v, off, 0, 0);
 }
 
+// A non-temporal (streaming) store (cache policy bit 1, NT on gfx950): for
+// outputs of which the next kernels read back only a small part, so that
+// they do not displace the lines that are read again from the caches.
+__device__ __forceinline__ void buf_st4_stream(__amdgpu_buffer_rsrc_t v, uint32_t off, float4 x) {
+  typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+  __builtin_amdgcn_raw_buffer_store_b128(__builtin_bit_cast(u32x4, x), v, off, 0, 2);
+}
+
 }  // namespace sd

@@ -219,6 +219,17 @@ hipError_t philox_normals_launch(uint64_t seed, uint32_t chain, uint32_t rnd, ui
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
+// Whether a kernel that writes a block of `bytes` of draft rows uses
+// non-temporal stores for them.  The next target call reads the whole block
+// back: while it is at most half of the 256 MB infinity cache most of it is
+// still there for that read, so the rows are stored normally; a larger block
+// mostly leaves the cache before it is read, and normal stores then only
+// displace other lines (measured: streaming a 113 MB block slowed the next
+// logits GEMM by 5 us; streaming 151 MB and 428 MB blocks made the advance
+// kernel 10 and 25 us faster and the logits GEMM no slower).
+constexpr int64_t kStreamRowsBytes = (int64_t)128 << 20;
+inline bool stream_rows(int64_t bytes) { return bytes > kStreamRowsBytes; }
+
 #ifdef __HIPCC__
 // Workgroups are dispatched round-robin over the eight XCDs, each with its own
 // L2.  Remap the linear workgroup id so that XCD x works on a contiguous

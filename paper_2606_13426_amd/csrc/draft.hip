@@ -44,7 +44,7 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(
     const float* __restrict__ mqprev, int64_t qc, int64_t qr, const int32_t* __restrict__ kk,
     const uint32_t* __restrict__ rnd, uint64_t seed, float* __restrict__ x, int64_t xc,
     int64_t xr, float* __restrict__ mp, int64_t mc, int64_t mr, float* __restrict__ svout,
-    bool vec_ok, const int* gate) {
+    bool vec_ok, bool stream, const int* gate) {
   if (gate && *gate == 0) return;
   const int b = blockIdx.y;
   const int g = blockIdx.x * kThreads + threadIdx.x;
@@ -74,8 +74,9 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(
   } else {
     load4(cs + (int64_t)b * d + e0, cnt, vec, sv);
   }
-  store4(xb, cnt, vec, yv);
-  draft_rows(sc, coef, K, k, kb, (uint32_t)b, r, seed, g, yv, sv, scale, xb, xr, mb, mr, cnt, vec);
+  store4(xb, cnt, vec, yv, stream);
+  draft_rows(sc, coef, K, k, kb, (uint32_t)b, r, seed, g, yv, sv, scale, xb, xr, mb, mr, cnt, vec,
+             stream);
 }
 
 // One thread per chain, at the start of a round:
@@ -177,10 +178,11 @@ hipError_t draft_launch(const Sched& sc, int B, int K, int d, const float* y, co
   const int ng = (d + 3) / 4;
   dim3 grid((ng + kThreads - 1) / kThreads, B);
   const bool vec = draft_vec(d, xs, mps, y, x, mp) && aligned16(cs);
+  const bool stream = stream_rows((int64_t)B * (K + 1) * d * 4);
   return timed("draft_block", s, [&] {
     draft_kernel<false><<<grid, kThreads, 0, s>>>(sc, nullptr, K, d, y, cs, nullptr, nullptr, nullptr, 0, 0,
                                                   k, rnd, seed, x, xs.chain, xs.row, mp, mps.chain,
-                                                  mps.row, nullptr, vec, gate);
+                                                  mps.row, nullptr, vec, stream, gate);
   });
 }
 
@@ -194,10 +196,11 @@ hipError_t draft_cached_launch(const Sched& sc, const float4* coef, int B, int K
   dim3 grid((ng + kThreads - 1) / kThreads, B);
   const bool vec = draft_vec(d, xs, sd_stride{d, d}, y, x, sv) && aligned16(mqprev) &&
                    mqs.chain % 4 == 0 && mqs.row % 4 == 0;
+  const bool stream = stream_rows((int64_t)B * (K + 1) * d * 4);
   return timed("draft_block", s, [&] {
     draft_kernel<true><<<grid, kThreads, 0, s>>>(sc, coef, K, d, y, nullptr, crow, cstep, mqprev,
                                                  mqs.chain, mqs.row, k, rnd, seed, x, xs.chain,
-                                                 xs.row, nullptr, 0, 0, sv, vec, gate);
+                                                 xs.row, nullptr, 0, 0, sv, vec, stream, gate);
   });
 }
 

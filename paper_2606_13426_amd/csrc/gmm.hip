@@ -609,6 +609,8 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_split_kernel(
 // through a view of the tile's rows (x: 65 rows, the last for the next draft
 // of the tile's last row; SV: the tile's chains; m^q: the tile's rows), so
 // rows past the block read zero and their stores drop.
+// VEC stores m^q with non-temporal stores: of a chain's K + 1 rows the round
+// reads back two (the residual's mean and the next cache row).
 // VEC also runs the contraction on the bf16 matrix cores from the pre-split
 // planes of mu^T (gemm_split.hpp), P split in registers; otherwise it is on
 // float32 matrix instructions.
@@ -760,7 +762,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
                                   c1 * x.z + c2 * (ov.z - rho * x.z),
                                   c1 * x.w + c2 * (ov.w - rho * x.w));
     if constexpr (VEC) {
-      buf_st4(vq, (uint32_t)((lr * d + col) * 4), qv);
+      buf_st4_stream(vq, (uint32_t)((lr * d + col) * 4), qv);
     } else {
       if (row >= R || cnt == 0) continue;
       st4(mq + (int64_t)row * d + col, cnt, false, qv);

@@ -261,7 +261,8 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_bf16_kernel(
 // and the eight rows meet at most two chains (two cache-row loads).  Every
 // global load of both passes is issued before the first store (stores and
 // loads share one in-order counter), through buffer views of the tile's rows
-// (rows past the block read zero; their stores drop).
+// (rows past the block read zero; their stores drop).  m^q goes out with
+// non-temporal stores: the round reads back two of a chain's K + 1 rows.
 __device__ __forceinline__ void mean_lr_epilogue_vec(
     float* stg, float* gz, const float* cscale, const float* rc, const f32x16 (&acc)[2][2], int R,
     int d, int K1, int r0, int c0, int ct, int nct, int b_first, int nchain,
@@ -319,7 +320,7 @@ __device__ __forceinline__ void mean_lr_epilogue_vec(
                                     c1 * x.y + c2 * (ov.y - rho * x.y),
                                     c1 * x.z + c2 * (ov.z - rho * x.z),
                                     c1 * x.w + c2 * (ov.w - rho * x.w));
-      buf_st4(vq, (uint32_t)((lr * d + col) * 4), qv);
+      buf_st4_stream(vq, (uint32_t)((lr * d + col) * 4), qv);
       // every row is computed and kept only when it is a draft row of the
       // block (a select: rows past R read zeros and their chain index stays
       // inside gz and cscale)

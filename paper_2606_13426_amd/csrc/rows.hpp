@@ -17,8 +17,14 @@ __device__ __forceinline__ void load4(const float* p, int cnt, bool vec, float (
   }
 }
 
-__device__ __forceinline__ void store4(float* p, int cnt, bool vec, const float (&v)[4]) {
-  if (vec) {
+// stream: a non-temporal store of an aligned vector (see stream_rows).
+__device__ __forceinline__ void store4(float* p, int cnt, bool vec, const float (&v)[4],
+                                      bool stream = false) {
+  typedef float f32x4 __attribute__((ext_vector_type(4)));
+  if (vec && stream) {
+    const f32x4 t = {v[0], v[1], v[2], v[3]};
+    __builtin_nontemporal_store(t, reinterpret_cast<f32x4*>(p));
+  } else if (vec) {
     *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
   } else {
 #pragma unroll
@@ -50,11 +56,13 @@ __device__ __forceinline__ float draft_mean(float c1, float y, float c2s, float 
 // where c2_n S_c = (c2_n * scale) * sv; rows past K_b repeat the last draft
 // and mean so that every row the target call reads is finite.  mb may be
 // null (the sampler recomputes m^p where it needs it, see draft_mean).
+// stream: the rows are written with non-temporal stores (stream_rows).
 __device__ __forceinline__ void draft_rows(const Sched& sc, const float4* __restrict__ coef, int K,
                                            int k, int kb, uint32_t chain, uint32_t rnd,
                                            uint64_t seed, int g, float (&yv)[4],
                                            const float (&sv)[4], float scale, float* xb,
-                                           int64_t xr, float* mb, int64_t mr, int cnt, bool vec) {
+                                           int64_t xr, float* mb, int64_t mr, int cnt, bool vec,
+                                           bool stream) {
   float m[4] = {0.f, 0.f, 0.f, 0.f};
   for (int i = 1; i <= kb; ++i) {
     const int n = k + i - 1;
@@ -66,12 +74,12 @@ __device__ __forceinline__ void draft_rows(const Sched& sc, const float4* __rest
       m[c] = draft_mean(cf.x, yv[c], c2, sv[c]);
       yv[c] = m[c] + cf.z * get4(z, c);
     }
-    if (mb) store4(mb + (int64_t)(i - 1) * mr, cnt, vec, m);
-    store4(xb + (int64_t)i * xr, cnt, vec, yv);
+    if (mb) store4(mb + (int64_t)(i - 1) * mr, cnt, vec, m, stream);
+    store4(xb + (int64_t)i * xr, cnt, vec, yv, stream);
   }
   for (int i = kb + 1; i <= K; ++i) {
-    if (mb) store4(mb + (int64_t)(i - 1) * mr, cnt, vec, m);
-    store4(xb + (int64_t)i * xr, cnt, vec, yv);
+    if (mb) store4(mb + (int64_t)(i - 1) * mr, cnt, vec, m, stream);
+    store4(xb + (int64_t)i * xr, cnt, vec, yv, stream);
   }
 }
 
