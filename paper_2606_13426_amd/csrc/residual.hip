@@ -21,7 +21,7 @@ namespace sd {
 namespace {
 
 constexpr int kMaxThreads = 512;
-constexpr int kKeep = 4;  // float4 groups per thread kept in registers (d <= 8192)
+constexpr int kKeep = 6;  // float4 groups per thread kept in registers (d <= 12288)
 
 // Sum over the workgroup (blockDim.x a multiple of 64, at most 512).
 __device__ __forceinline__ double block_sum(double v, double* red) {
@@ -40,17 +40,42 @@ __device__ __forceinline__ void ld4(const float* p, int cnt, float (&v)[4]) {
   for (int c = 0; c < 4; ++c) v[c] = c < cnt ? p[c] : 0.0f;
 }
 
+// VEC: every row is 16-byte aligned and d % 4 == 0 (cnt is then always 4), so
+// a group is one 16-byte access.
+template <bool VEC>
+__device__ __forceinline__ void ldg(const float* p, int cnt, float (&v)[4]) {
+  if constexpr (VEC) {
+    const float4 t = *reinterpret_cast<const float4*>(p);
+    v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+  } else {
+    ld4(p, cnt, v);
+  }
+}
+template <bool VEC>
+__device__ __forceinline__ void stg(float* p, int cnt, const float (&v)[4]) {
+  if constexpr (VEC) {
+    *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+  } else {
+#pragma unroll
+    for (int c = 0; c < 4; ++c)
+      if (c < cnt) p[c] = v[c];
+  }
+}
+
 // The rejection case: one pass reads m^q, m^p and draws G for this thread's
-// groups (kept in registers), reduces e.G, and the second pass writes
-// y = m^q + sigma G + c (m^p - m^q) from the registers.  Groups beyond
-// kKeep * blockDim.x (d > 8192) are re-read and redrawn in the second pass.
-__device__ void decomposition_row(int b, int d, uint32_t r, uint64_t seed, const float* p,
+// groups (m^q and m^p - m^q kept in registers), reduces e.G, and the second
+// pass writes y = m^q + sigma G + c (m^p - m^q), drawing G again (the same
+// counter-based normals) rather than holding it: fewer registers, more
+// workgroups in flight.  Groups beyond kKeep * blockDim.x (d > 12288) are
+// re-read and redrawn in the second pass.
+template <bool VEC>
+__device__ __forceinline__ void decomposition_row(int b, int d, uint32_t r, uint64_t seed, const float* p,
                                   const float* q, double s, double v, double U, float* out,
                                   double* red) {
   const int ng = (d + 3) / 4;
   const int nt = blockDim.x;
   const uint32_t c3 = TAG_RESID << 24;
-  float gq[kKeep][4], gd[kKeep][4], gz[kKeep][4];
+  float gq[kKeep][4], gd[kKeep][4];
   double acc = 0.0;
 #pragma unroll
   for (int i = 0; i < kKeep; ++i) {
@@ -59,13 +84,12 @@ __device__ void decomposition_row(int b, int d, uint32_t r, uint64_t seed, const
       const int e0 = 4 * g, cnt = min(4, d - e0);
       const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, c3, seed));
       float pv[4];
-      ld4(p + e0, cnt, pv);
-      ld4(q + e0, cnt, gq[i]);
+      ldg<VEC>(p + e0, cnt, pv);
+      ldg<VEC>(q + e0, cnt, gq[i]);
 #pragma unroll
       for (int c = 0; c < 4; ++c) {
-        gz[i][c] = get4(z, c);
         gd[i][c] = pv[c] - gq[i][c];
-        if (c < cnt) acc += ((double)pv[c] - (double)gq[i][c]) * (double)gz[i][c];
+        if (c < cnt) acc += ((double)pv[c] - (double)gq[i][c]) * (double)get4(z, c);
       }
     }
   }
@@ -82,9 +106,11 @@ __device__ void decomposition_row(int b, int d, uint32_t r, uint64_t seed, const
     const int g = threadIdx.x + i * nt;
     if (g < ng) {
       const int e0 = 4 * g, cnt = min(4, d - e0);
+      const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, c3, seed));
+      float o[4];
 #pragma unroll
-      for (int c = 0; c < 4; ++c)
-        if (c < cnt) out[e0 + c] = gq[i][c] + sf * gz[i][c] + coef * gd[i][c];
+      for (int c = 0; c < 4; ++c) o[c] = gq[i][c] + sf * get4(z, c) + coef * gd[i][c];
+      stg<VEC>(out + e0, cnt, o);
     }
   }
   for (int g = threadIdx.x + kKeep * nt; g < ng; g += nt) {
@@ -100,7 +126,7 @@ __device__ void decomposition_row(int b, int d, uint32_t r, uint64_t seed, const
 // The reflection residual of one rejected chain: sums D.D and D.W over the
 // row in float64 (the thread's groups kept in registers up to kKeep), then
 // y = yhat - c D.
-__device__ void reflection_row(int d, const float* yh, const float* p, const float* q,
+__device__ __forceinline__ void reflection_row(int d, const float* yh, const float* p, const float* q,
                                float* out, double* red) {
   const int ng = (d + 3) / 4;
   const int nt = blockDim.x;
@@ -159,8 +185,11 @@ __device__ void reflection_row(int d, const float* yh, const float* p, const flo
 // k <- min(k + tau, N), round <- round + 1, and records where the Free Drafter
 // finds its cached score next round (row min(tau, K_b) of this round's target
 // means, at step k + min(tau, K_b)) and how many steps the chain advanced.
-template <bool COMMIT>
-__global__ __launch_bounds__(kMaxThreads) void residual_kernel(
+// Four wavefronts per SIMD (two 512-thread workgroups per compute unit): the
+// register budget of 128 keeps a second chain's loads in flight while one
+// workgroup reduces.
+template <bool COMMIT, bool VEC>
+__global__ __launch_bounds__(kMaxThreads, 4) void residual_kernel(
     int B, int K, int d, int N, const float* __restrict__ yd, int64_t yc, int64_t yr,
     const float* __restrict__ mp, int64_t pc, int64_t pr, const float* __restrict__ mq,
     int64_t qc, int64_t qr, const double* __restrict__ sigma, const int32_t* __restrict__ kbv,
@@ -186,7 +215,7 @@ __global__ __launch_bounds__(kMaxThreads) void residual_kernel(
                    mp + (int64_t)b * pc + (int64_t)(t - 1) * pr,
                    mq + (int64_t)b * qc + (int64_t)(t - 1) * qr, out, red);
   } else if (t <= kb) {
-    decomposition_row(b, d, r, seed, mp + (int64_t)b * pc + (int64_t)(t - 1) * pr,
+    decomposition_row<VEC>(b, d, r, seed, mp + (int64_t)b * pc + (int64_t)(t - 1) * pr,
                       mq + (int64_t)b * qc + (int64_t)(t - 1) * qr,
                       sigma[(int64_t)b * (K + 1) + (t - 1)], dn[(int64_t)b * K + (t - 1)], ures[b],
                       out, red);
@@ -229,13 +258,21 @@ inline int residual_threads(int d) {
 
 }  // namespace
 
+// Rows of the m^p and m^q views and of y all 16-byte aligned, d % 4 == 0.
+inline bool residual_vec(int d, sd_stride mps, sd_stride mqs, const float* mp, const float* mq,
+                         const float* y) {
+  return d % 4 == 0 && mps.chain % 4 == 0 && mps.row % 4 == 0 && mqs.chain % 4 == 0 &&
+         mqs.row % 4 == 0 && aligned16(mp) && aligned16(mq) && aligned16(y);
+}
+
 hipError_t residual_launch(int B, int K, int d, const float* yd, sd_stride ys, const float* mp,
                            sd_stride mps, const float* mq, sd_stride mqs, const double* sigma,
                            const int32_t* kb, const int32_t* left, const int32_t* tau,
                            const double* ures, const double* dn, const uint32_t* rnd,
                            uint64_t seed, float* y, hipStream_t s) {
+  const bool vec = residual_vec(d, mps, mqs, mp, mq, y);
   return timed("residual_draw", s, [&] {
-    residual_kernel<false><<<B, residual_threads(d), 0, s>>>(
+    (vec ? residual_kernel<false, true> : residual_kernel<false, false>)<<<B, residual_threads(d), 0, s>>>(
         B, K, d, 0, yd, ys.chain, ys.row, mp, mps.chain, mps.row, mq, mqs.chain, mqs.row, sigma,
         kb, left, tau, ures, dn, const_cast<uint32_t*>(rnd), seed, y, nullptr, nullptr, nullptr,
         nullptr, nullptr, 0, 0, false, nullptr);
@@ -247,7 +284,7 @@ hipError_t reflection_launch(int B, int K, int d, const float* yd, sd_stride ys,
                              const int32_t* kb, const int32_t* left, const int32_t* tau,
                              const uint32_t* rnd, uint64_t seed, float* y, hipStream_t s) {
   return timed("residual_reflect", s, [&] {
-    residual_kernel<false><<<B, residual_threads(d), 0, s>>>(
+    residual_kernel<false, false><<<B, residual_threads(d), 0, s>>>(
         B, K, d, 0, yd, ys.chain, ys.row, mp, mps.chain, mps.row, mq, mqs.chain, mqs.row, sigma,
         kb, left, tau, nullptr, nullptr, const_cast<uint32_t*>(rnd), seed, y, nullptr, nullptr,
         nullptr, nullptr, nullptr, 0, 0, true, nullptr);
@@ -261,8 +298,9 @@ hipError_t residual_commit_launch(int B, int K, int d, int N, const float* yd, s
                                   uint32_t* rnd, uint64_t seed, float* y, int32_t* k,
                                   int32_t* crow, int32_t* cstep, int32_t* adv, int32_t* trace,
                                   int r, int trace_rounds, hipStream_t s, const int* gate) {
+  const bool vec = residual_vec(d, mps, mqs, mp, mq, y);
   return timed("residual_commit", s, [&] {
-    residual_kernel<true><<<B, residual_threads(d), 0, s>>>(
+    (vec ? residual_kernel<true, true> : residual_kernel<true, false>)<<<B, residual_threads(d), 0, s>>>(
         B, K, d, N, yd, ys.chain, ys.row, mp, mps.chain, mps.row, mq, mqs.chain, mqs.row, sigma,
         kb, left, tau, ures, dn, rnd, seed, y, k, crow, cstep, adv, trace, r, trace_rounds, false,
         gate);
