@@ -40,9 +40,9 @@ PROFILE_EVERY = 4  # the timed runs' event sample of the dominant kernel's launc
 
 MEASURED_TRAFFIC = {
     ("verify12288", "logratio_reduce"): dict(bytes=(19344.1 + 8.5) * 1e6, unit="verify.hip",
-                                             sources="b433caaeb199b4dc26650a05dfc0ed27953f90d1"),
+                                             sources="f836d93df582b1a3e80a36bc35a70cc54c617707"),
     ("pixel3072", "gmm_mean_lr"): dict(bytes=(136.1 + 122.0) * 1e6, unit="gmm.hip",
-                                       sources="15cd72ad9f3e678b6040b368fa7c20a84f890f41"),
+                                       sources="0099a411fb3bc5708d0675116594a868814a4032"),
 }
 
 

@@ -104,7 +104,9 @@ sd_status sd_schedule_table(const sd_schedule* sched, double* host_out);
  * elsewhere with float32 matrix instructions); SD_BF16 stores mu as bf16 (round to
  * nearest even) and rounds x and the softmax weights to bf16 before the two
  * products, accumulating in float32 (||x||^2, ||mu||^2 and the softmax stay
- * float64 from the float32 values; the epilogue is float32).  Only the copies
+ * float64 from the float32 values, ||x||^2 on the widest logits tiles as a
+ * float64 sum of float32 partials of four squares; the epilogue is float32).
+ * Only the copies
  * of the chosen precision are allocated. */
 sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp,
                            const float* mu, const float* var, const float* log_w,

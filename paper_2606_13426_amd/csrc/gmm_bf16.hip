@@ -3,7 +3,8 @@
 // float32 path (logits GEMM split over d, float64 softmax, mean GEMM with the
 // EM epilogue) on tiles of v_mfma_f32_32x32x16_bf16.
 //   gmm_logits_bf16: S = X mu^T, X float32 rounded to bf16 on staging, mu bf16;
-//                    ||x||^2 in float64 from the unrounded float32 values;
+//                    ||x||^2 from the unrounded float32 values (float64
+//                    sums; on 256 x 256 tiles of float32 partials of four);
 //                    256 x 256 tiles (gemm_bf16_wide.hpp) when d is a whole
 //                    number of chunks and rows are aligned, else 128 x 128;
 //   softmax:         the float32 path's kernels, writing P in bf16;
