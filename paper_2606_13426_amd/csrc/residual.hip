@@ -69,9 +69,9 @@ __device__ __forceinline__ void stg(float* p, int cnt, const float (&v)[4]) {
 // workgroups in flight.  Groups beyond kKeep * blockDim.x (d > 12288) are
 // re-read and redrawn in the second pass.
 template <bool VEC>
-__device__ __forceinline__ void decomposition_row(int b, int d, uint32_t r, uint64_t seed, const float* p,
-                                  const float* q, double s, double v, double U, float* out,
-                                  double* red) {
+__device__ __forceinline__ void decomposition_row(int b, int d, uint32_t r, uint64_t seed,
+                                                  const float* p, const float* q, double s,
+                                                  double v, double U, float* out, double* red) {
   const int ng = (d + 3) / 4;
   const int nt = blockDim.x;
   const uint32_t c3 = TAG_RESID << 24;
@@ -126,8 +126,8 @@ __device__ __forceinline__ void decomposition_row(int b, int d, uint32_t r, uint
 // The reflection residual of one rejected chain: sums D.D and D.W over the
 // row in float64 (the thread's groups kept in registers up to kKeep), then
 // y = yhat - c D.
-__device__ __forceinline__ void reflection_row(int d, const float* yh, const float* p, const float* q,
-                               float* out, double* red) {
+__device__ __forceinline__ void reflection_row(int d, const float* yh, const float* p,
+                                               const float* q, float* out, double* red) {
   const int ng = (d + 3) / 4;
   const int nt = blockDim.x;
   float gy[kKeep][4], gd[kKeep][4];
