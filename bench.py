@@ -471,6 +471,28 @@ LIBRARY_GEMMS = {
 }
 
 
+def mfma_calibration(lib, blocks=1024, iters=512, reps=5):
+    """The bf16 matrix-core rate this GPU sustains: the library's register-only
+    loop of v_mfma_f32_32x32x16_bf16 (sd_mfma_loop; four wavefronts per SIMD,
+    four independent accumulators each), timed with events after a warm-up,
+    against the published dense peak."""
+    import torch
+    out = torch.empty(blocks * 4, dtype=torch.float32, device="cuda")
+    for _ in range(2):
+        lib.sd_mfma_loop(blocks, iters, out)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(reps):
+        lib.sd_mfma_loop(blocks, iters, out)
+    ev[1].record()
+    torch.cuda.synchronize()
+    s = ev[0].elapsed_time(ev[1]) / reps / 1e3
+    tflops = blocks * 16 * iters * 32768 / s / 1e12
+    return dict(kernel="mfma_loop", instruction="v_mfma_f32_32x32x16_bf16", blocks=blocks, iters=iters,
+                us=s * 1e6, tflops=tflops, peak=2500.0, frac=tflops / 2500.0)
+
+
 def library_gemms(reps=20):
     """The same products as plain library GEMMs (row-major, contiguous
     operands, output written), timed with events: what the vendor library
@@ -512,6 +534,9 @@ def main():
     ap.add_argument("--no-extra", action="store_true", help="skip the token and verification-only runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--calibrate-mfma", action="store_true",
+                    help="only time the library's register-only bf16 matrix-instruction loop (the sustained "
+                         "matrix-core rate beside the published peak) and exit")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run a plain device copy of 1 GiB five times (the reference "
                          "kernel of known size for scaling the HBM byte counters) and exit")
@@ -542,6 +567,13 @@ def main():
         # torch initialises the device before the library's first HIP call
         assert torch.cuda.is_available(), "bench.py needs a GPU"
         print(json.dumps(dict(workload=args.workload, variants=variants_bench(lib, args.workload, args.steps))))
+        return
+    if args.calibrate_mfma:
+        import torch
+        from paper_2606_13426_amd import _lib as lib
+        lib.load()
+        assert torch.cuda.is_available(), "bench.py needs a GPU"
+        print(json.dumps(dict(mfma_calibration=mfma_calibration(lib))))
         return
     if args.calibrate_copy:
         # also the achievable streaming rates of this machine: a read-plus-write
@@ -610,6 +642,7 @@ def main():
                                        for k, v in table2.items() if "avg_us" in v})
         line["other_workloads"] = others
         line["library_gemms"] = library_gemms()
+        line["mfma_calibration"] = mfma_calibration(lib)
         line["variants"] = variants_bench(lib, args.workload, args.steps)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_budget)

@@ -323,6 +323,16 @@ sd_status sd_philox_words(uint64_t seed, int32_t n, const uint32_t* counters, ui
 sd_status sd_philox_normals(uint64_t seed, uint32_t chain, uint32_t round, uint32_t tag,
                             uint32_t slot, int32_t d, float* out, sd_stream stream);
 
+/* Calibration of the matrix cores (not part of the sampler): `blocks`
+ * workgroups of four wavefronts, each issuing iters x 4
+ * v_mfma_f32_32x32x16_bf16 (32768 flops each) on register operands with no
+ * memory traffic, so blocks x 16 x iters x 32768 flops in all; one float per
+ * wavefront is written to out (device, [blocks][4], caller-owned) so the loop
+ * is kept.  Timing it gives the bf16 matrix rate this GPU sustains, the
+ * practical ceiling beside the published dense peak.  SD_EINVAL unless
+ * blocks >= 1, iters >= 1 and out is non-null. */
+sd_status sd_mfma_loop(int32_t blocks, int32_t iters, float* out, sd_stream stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -90,6 +90,7 @@ SIGNATURES = [
     ("sd_profile_read", c_int32, [ctypes.POINTER(sd_kernel_stat), c_int32, ctypes.POINTER(c_int32)]),
     ("sd_philox_words", c_int32, [c_uint64, c_int32, P, P, P]),
     ("sd_philox_normals", c_int32, [c_uint64, c_uint32, c_uint32, c_uint32, c_uint32, c_int32, P, P]),
+    ("sd_mfma_loop", c_int32, [c_int32, c_int32, P, P]),
 ]
 
 _lib = None
@@ -358,3 +359,8 @@ def sd_philox_words(seed, counters, out):
 def sd_philox_normals(seed, chain, rnd, tag, slot, out):
     _check(load().sd_philox_normals(seed, chain, rnd, tag, slot, out.numel(), _p(out), _stream()),
            "sd_philox_normals")
+
+
+def sd_mfma_loop(blocks, iters, out):
+    """Matrix-core calibration loop: blocks x 16 x iters x 32768 bf16 flops; out [blocks][4] float32."""
+    _check(load().sd_mfma_loop(blocks, iters, _p(out), _stream()), "sd_mfma_loop")

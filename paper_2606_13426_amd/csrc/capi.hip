@@ -805,4 +805,11 @@ sd_status sd_philox_normals(uint64_t seed, uint32_t chain, uint32_t round, uint3
   return SD_OK;
 }
 
+sd_status sd_mfma_loop(int32_t blocks, int32_t iters, float* out, sd_stream stream) {
+  SD_CHECK_ARG(blocks >= 1 && iters >= 1, "sd_mfma_loop: need blocks >= 1 and iters >= 1");
+  SD_CHECK_ARG(out, "sd_mfma_loop: NULL out");
+  SD_HIP(mfma_loop_launch(blocks, iters, out, (hipStream_t)stream));
+  return SD_OK;
+}
+
 }  // extern "C"

@@ -216,6 +216,9 @@ hipError_t philox_words_launch(uint64_t seed, int n, const uint32_t* ctr, uint32
                                hipStream_t s);
 hipError_t philox_normals_launch(uint64_t seed, uint32_t chain, uint32_t rnd, uint32_t tag,
                                  uint32_t slot, int d, float* out, hipStream_t s);
+// blocks workgroups of four wavefronts, each issuing iters x 4 bf16 matrix
+// instructions on registers; one float per wavefront to out ([blocks][4]).
+hipError_t mfma_loop_launch(int blocks, int iters, float* out, hipStream_t s);
 
 inline bool aligned16(const void* p) { return ((uintptr_t)p & 15u) == 0; }
 
