@@ -40,9 +40,9 @@ PROFILE_EVERY = 4  # the timed runs' event sample of the dominant kernel's launc
 
 MEASURED_TRAFFIC = {
     ("verify12288", "logratio_reduce"): dict(bytes=(19344.1 + 8.5) * 1e6, unit="verify.hip",
-                                             sources="f836d93df582b1a3e80a36bc35a70cc54c617707"),
+                                             sources="ea7ba0139a0bc5b69f3731957c94da1a81dfb8b2"),
     ("pixel3072", "gmm_mean_lr"): dict(bytes=(136.1 + 122.0) * 1e6, unit="gmm.hip",
-                                       sources="0099a411fb3bc5708d0675116594a868814a4032"),
+                                       sources="f3e06c62cf09a8fbf8101f1fe1e515fc20c93769"),
 }
 
 
