@@ -29,7 +29,9 @@ Y = m^q + sigma (I - 2 e e^T) Z with Z the rejected step's draft noise.
 
 Parity: pinned by trapezoid integration of the unnormalised density (the
 paper's own numerical method for its residual plots), KS tests of sampled
-U against Psi, and exactness of the sampled residual in d = 1, 2, 8.
+U against Psi, exactness of the sampled residual in d = 1, 2, 8, and, for the
+paper mode, the dyadic midpoint that the exact inverse determines (the caps
+and the tolerance stop included).
 """
 import math
 

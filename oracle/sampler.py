@@ -37,7 +37,8 @@ whose law the speculative sampler must reproduce exactly (Sec. 2/3.2).
 Parity: the exact numeric trajectories are fixed only by this oracle and the
 shared Philox contract ("parity unpinned" for single trajectories); their law
 is pinned by the distribution tests against the plain EM chain and the
-degenerate drafter = target case.  The variants are pinned the same way
+degenerate drafter = target case, and the Free Drafter's cache row by finite
+differences of log q at the rejected (or last) draft and its time.  The variants are pinned the same way
 (tests/test_oracle_variants.py): the reflection and Frozen-Drafter samplers
 against the plain EM law, the Frozen Drafter with K = 1 path by path against
 an EM chain with the round's noises, temperature by the closed-form tempered

@@ -3,8 +3,9 @@
 * Psi_alpha equals the trapezoid-normalised CDF of max(0, alpha N(u) - N(u - v))
   (the paper's own numerical method for its residual plots, App. D);
 * sampled U follows that CDF (KS), down to alpha = e^-500;
-* the paper-mode sampler (3 doublings, 4 bisections) stays inside the bracket and
-  close to the exact inverse;
+* the paper-mode sampler (3 doublings, 4 bisections, tolerance 1e-6) equals the
+  dyadic midpoint that the exact inverse of Psi fixes, including a binding
+  doubling cap and early stops after 0..3 bisections;
 * the Decomposition residual has density ∝ max(0, alpha q - p) in y-space (d = 1),
   and in d = 2, 8 its e-component follows psi_alpha while the orthogonal part is
   an independent N(0, I - e e^T).
@@ -109,3 +110,86 @@ def test_decomposition_orthogonal_structure(d):
     for i in range(d - 1):
         assert stats.kstest(perp[:, i], "norm").pvalue > 1e-4
         assert abs(np.corrcoef(perp[:, i], proj)[0, 1]) < 4.5 / np.sqrt(n)
+
+
+PAPER_TOL = 1e-6   # the reading of the paper-mode tolerance (its value is not given)
+
+
+def _paper_mode_from_exact(u, log_alpha, v):
+    """The paper-mode draw (<= 3 doublings, <= 4 bisections, |Psi(mid) - u| <= tol)
+    derived from the exact inverse of Psi alone.
+
+    Psi is increasing on its support, so Psi(x) > u <=> x > Psi^-1(u) and
+    |Psi(x) - u| <= tol <=> Psi^-1(u - tol) <= x <= Psi^-1(u + tol).  Doubling
+    from [u* - 1, u*] stops at the first n in 0..3 with u* - 2^n <= Psi^-1(u),
+    so the bracket is [u* - 2^n, u*] of width W = 2^n; after i bisections the
+    midpoint is the centre of the dyadic cell holding t = (Psi^-1(u) - lo)/W
+    (t clamped to [0, 1]: when the cap binds every midpoint lies above the
+    quantile), lo + W (floor(2^i t) + 1/2) / 2^i.  The draw is the first of
+    these midpoints (i = 0..3) inside the tolerance window, else the one after
+    the fourth bisection.  Returns (draw, doublings, bisections)."""
+    us = upper_end(log_alpha, v)
+
+    def inv(q):
+        return usample(q, log_alpha, v, USAMPLE_EXACT)
+
+    ue = inv(u)
+    n = next((n for n in range(4) if us - 2.0 ** n <= ue), 3)
+    lo, width = us - 2.0 ** n, 2.0 ** n
+    t = min(max((ue - lo) / width, 0.0), 1.0)
+    wl = inv(u - PAPER_TOL) if u - PAPER_TOL > 0.0 else -math.inf
+    wh = inv(u + PAPER_TOL) if u + PAPER_TOL < 1.0 else math.inf
+    for i in range(5):
+        j = min(math.floor(2 ** i * t), 2 ** i - 1)
+        mid = lo + width * (j + 0.5) / 2 ** i
+        if i == 4 or wl <= mid <= wh:
+            return mid, n, i
+
+
+def _u_with_exact_inverse_at(x, log_alpha, v):
+    """The u in (0, 1) whose exact inverse is x (bisection on u; Psi^-1 is increasing)."""
+    a, b = 0.0, 1.0
+    for _ in range(80):
+        m = 0.5 * (a + b)
+        if usample(m, log_alpha, v, USAMPLE_EXACT) < x:
+            a = m
+        else:
+            b = m
+    return 0.5 * (a + b)
+
+
+@pytest.mark.parametrize("log_alpha,v", [(0.0, 1.0), (math.log(0.5), 1.0), (math.log(1e-3), 0.3),
+                                         (-500.0, 30.0), (0.0, 0.05)])
+def test_usample_paper_mode_equals_dyadic_closed_form(log_alpha, v):
+    # App. "Experimental details" / Alg. 7: the capped doubling and bisection.
+    # Random u (no early stop in practice), a u so small that the three
+    # doublings do not reach the quantile (the cap binds), and u placed just
+    # inside (and, as a control, just outside) the tolerance window of the
+    # midpoint after i bisections (i = 0..3).
+    us = upper_end(log_alpha, v)
+    tol = 1e-12 * max(1.0, abs(us))   # the candidates are >= 1/32 apart
+    rng = np.random.default_rng(17)
+    cases = [(float(q), None) for q in rng.uniform(size=60)] + [(1e-300, "cap")]
+    lo0 = us - 1.0
+    for i in range(4):
+        # the midpoint after i bisections of [u* - 1, u*] when the quantile is
+        # in its lowest dyadic cell: u* - 1 + 2^-(i+1)
+        target = lo0 + 2.0 ** -(i + 1)
+        q = _u_with_exact_inverse_at(target, log_alpha, v)
+        if 10 * PAPER_TOL < q < 1.0 - 10 * PAPER_TOL:
+            cases.append((q + 0.4 * PAPER_TOL, i))
+            cases.append((q + 3.0 * PAPER_TOL, -1 - i))
+    stops = set()
+    for u, kind in cases:
+        want, n, i = _paper_mode_from_exact(u, log_alpha, v)
+        got = usample(u, log_alpha, v, USAMPLE_PAPER)
+        assert abs(got - want) <= tol, (u, kind, got, want, n, i)
+        if kind == "cap":
+            assert n == 3 and usample(u, log_alpha, v, USAMPLE_EXACT) < us - 8.0
+        elif kind is not None and kind >= 0:
+            assert i <= kind, (u, kind, i)
+            stops.add(i)
+        elif kind is not None:
+            # just outside the window: the draw is not that midpoint
+            assert abs(got - (lo0 + 2.0 ** kind)) > tol, (u, kind, got)
+    assert stops, "no early stop was constructed"

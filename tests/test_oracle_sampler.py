@@ -5,7 +5,9 @@
 * block verification advances at least as many steps per round as token;
 * in the first round the Free Drafter's first draft mean equals the target
   mean, so Delta_1 = 0 and the first draft is always accepted;
-* every chain ends exactly at step N; same seed, same result.
+* every chain ends exactly at step N; same seed, same result;
+* the Free Drafter's cached score is the target score at the rejected draft
+  (or at the last draft after a full accept), at that draft's time.
 """
 import numpy as np
 import pytest
@@ -68,3 +70,50 @@ def test_deterministic():
     assert np.array_equal(a["y"], b["y"])
     c = S.run_sampler(g, sch, 8, 3, seed=10)
     assert not np.array_equal(a["y"], c["y"])
+
+
+def _fd_score(g, x, a, h=1e-5):
+    """Central differences of log q_s at one point: the score without the oracle's score code."""
+    d = x.shape[0]
+    out = np.empty(d)
+    for i in range(d):
+        e = np.zeros(d)
+        e[i] = h
+        out[i] = (g.log_density((x + e)[None], a)[0] - g.log_density((x - e)[None], a)[0]) / (2 * h)
+    return out
+
+
+def test_free_drafter_cache_is_score_at_rejected_or_last_draft():
+    """Sec. 3.3: the next round drafts with the target score the round already
+    computed at the rejected draft yhat_{k+tau}, time t_{k+tau} (tau <= K_b), or
+    after a full accept at the last draft yhat_{k+K_b}, time t_{k+K_b}.
+
+    The score the next round actually used is read back from its first draft
+    mean, S_c = (m^p_0 - c1_k' Y_k') / c2_k', and compared with finite
+    differences of log q at the expected row and time; the neighbouring rows
+    and the neighbouring time do not match it."""
+    g = _gmm(2, 7)
+    sch = Schedule(40)
+    K = 4
+    res = S.run_sampler(g, sch, 60, K, seed=13, keep_trace=True)
+    rej = full = distinct = compared = 0
+    for rec in res["trace"]:
+        for cur, nxt in zip(rec[:-1], rec[1:]):
+            k1 = nxt["k"]
+            used = (nxt["mp"][0] - sch.c1(k1) * nxt["yh"][0]) / sch.c2(k1)
+            c = min(cur["tau"], cur["kb"])
+            n = cur["k"] + c
+            assert k1 == min(cur["k"] + cur["tau"], sch.n_steps)
+            want = _fd_score(g, cur["yh"][c], sch.signal(n))
+            assert np.allclose(used, want, rtol=1e-6, atol=1e-6), (cur["k"], cur["tau"], used, want)
+            alts = [_fd_score(g, cur["yh"][c], sch.signal(n - 1))]
+            alts += [_fd_score(g, cur["yh"][j], sch.signal(cur["k"] + j))
+                     for j in (c - 1, c + 1) if 0 <= j <= cur["kb"]]
+            compared += 1
+            distinct += all(np.max(np.abs(alt - used)) > 1e-4 for alt in alts)
+            if cur["tau"] <= cur["kb"]:
+                rej += 1
+            else:
+                full += 1
+    assert rej >= 20 and full >= 20, (rej, full)
+    assert distinct >= 0.95 * compared, (distinct, compared)

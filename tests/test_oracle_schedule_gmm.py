@@ -5,7 +5,9 @@
 * the mixture score is the gradient of the mixture log-density (finite differences);
 * the marginal q_s matches samples of the forward process (KS, d = 1);
 * the Euler-Maruyama chain m^q_n(y) + sigma_n xi, started from N(0, I), ends at
-  the data law for two churn values (this pins sigma_n, c1_n, c2_n together).
+  the data law for two churn values (this pins sigma_n, c1_n, c2_n together);
+* above d = 64 the squared distances by the norm expansion equal the direct
+  differences, and so do the scores built on them.
 """
 import numpy as np
 import pytest
@@ -102,3 +104,25 @@ def test_em_chain_reaches_data_law(churn):
         y = mq + sch.sigma(n) * rng.standard_normal(y.shape)
     assert y.mean() == pytest.approx(mu0, abs=0.03)
     assert y.var() == pytest.approx(v0, rel=0.05)
+
+
+@pytest.mark.parametrize("d,M,a", [(3072, 64, 0.02), (3072, 64, 0.9), (16384, 24, 0.5), (65, 7, 0.99)])
+def test_expanded_distances_match_direct(d, M, a):
+    # above d = 64 the oracle forms ||x - a mu||^2 by the float64 norm
+    # expansion (one matrix product); the direct differences on a subset of
+    # rows fix it: rows near a component, far from all of them, and at the
+    # data end (a close to 1, small s2) where the logits are sharpest
+    rng = np.random.default_rng(d + M)
+    mu = rng.standard_normal((M, d))
+    var = rng.uniform(0.01, 0.2, M)
+    g = GMM(mu, var, np.log(rng.dirichlet(np.ones(M))))
+    x = np.concatenate([a * mu[:3] + 0.1 * rng.standard_normal((3, d)),
+                        rng.standard_normal((2, d)) * 3.0])
+    av = np.full(len(x), a)
+    direct = g.sq_dist(x, av, direct=True)
+    expd = g.sq_dist(x, av, direct=False)
+    assert np.allclose(expd, direct, rtol=1e-12, atol=0.0)
+    sd = g.score(x, a, direct=True)
+    se = g.score(x, a, direct=False)
+    err = np.linalg.norm(se - sd, axis=1) / np.linalg.norm(sd, axis=1)
+    assert err.max() <= 1e-9, err
