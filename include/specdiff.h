@@ -16,8 +16,9 @@
  *  - The caller owns all memory.  The library allocates device memory only in
  *    sd_target_create (freed by sd_target_destroy); everything else lives in
  *    caller buffers, including a caller workspace sized by the *_workspace query.
- *    sd_run_sampler also holds, for the duration of the call, 16 bytes of
- *    mapped pinned host memory.
+ *    sd_target_create also allocates 1 KB of mapped pinned host memory: the
+ *    words through which a running sampler call learns, round by round,
+ *    whether any chain is still active (up to 64 calls at once per target).
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
  *    null stream).  Only sd_run_sampler reads results back: a per-round "any
  *    chain active" flag that its kernels store into the mapped host memory,
@@ -44,7 +45,7 @@
 extern "C" {
 #endif
 
-#define SD_ABI_VERSION 2
+#define SD_ABI_VERSION 3
 #define SD_MAX_BLOCK 64
 
 typedef enum {
@@ -232,15 +233,25 @@ sd_status sd_sample_residual_reflection(int32_t B, int32_t K, int32_t d, const f
  * one explicit target call at Y_0 to seed the cached score, then rounds of
  * draft -> target means on all min(K_b+1, N-k) rows -> verify -> residual ->
  * commit until every chain has reached step N.  Chains run in lockstep rounds,
- * each with its own step k and round counter.  Returns Y_N in y_out [B][d].
+ * each with its own step k and round counter.  Returns Y_N in y_out [B][d]
+ * (written only by a call that ends with every chain at step N).
  * tau_trace (nullable): [trace_rounds][B] int32, tau of each chain per round
- * (0 once a chain has finished).  stats (host, nullable): rounds, chain-rounds,
- * steps and the tau histogram.  ws: >= sd_sampler_workspace bytes.
- * Returns SD_ENUMERIC if a non-finite log-ratio was met. */
+ * (0 once a chain has finished).  stats (host, nullable): see sd_stats.
+ * ws: >= sd_sampler_workspace bytes; it holds the whole sampler state between
+ * rounds, so a run may be split over calls (sd_sampler_options).
+ * Returns SD_ENUMERIC if a non-finite log-ratio was met, SD_EHIP also when no
+ * round finishes within 120 s (the kernels are then left running and the call
+ * returns without waiting for them).
+ * Statistics are counted from the start of the run (Y_0), over every call. */
 typedef struct {
-  int64_t rounds;       /* lockstep rounds launched until all chains finished */
+  int64_t rounds;       /* rounds run so far: until all chains finished, or the
+                           rounds a partial call has left in the workspace     */
   int64_t chain_rounds; /* sum over chains of rounds in which the chain was active */
-  int64_t steps;        /* sum over chains of steps advanced (= B * N)          */
+  int64_t steps;        /* sum over chains of steps advanced (B * N when done) */
+  int64_t ties;         /* coins with |eta_j - h_j| <= 1e-6 (alpha_j for token):
+                           decisions another rounding may flip               */
+  double mean_tau;      /* sum of tau over chain-rounds / chain_rounds        */
+  int32_t finished;     /* 1 when every chain has reached step N              */
   int64_t tau_hist[SD_MAX_BLOCK + 2]; /* tau_hist[t] = number of chain-rounds with tau = t */
 } sd_stats;
 
@@ -250,7 +261,8 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
                          int32_t* tau_trace, int32_t trace_rounds, sd_stats* stats, void* ws,
                          size_t ws_bytes, sd_stream stream);
 
-/* The sampler's variants (host struct, read during the call only):
+/* The sampler's variants and how much of the run one call does (host struct,
+ * read during the call only):
  *  mode, usample_mode   as in sd_run_sampler;
  *  residual             DECOMPOSITION (Alg. 5) or REFLECTION (Alg. 4; needs
  *                       mode == SD_TOKEN, else SD_EINVAL);
@@ -260,22 +272,83 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
  *                       on B rows is made per round;
  *  omega                temperature > 0 of the verification (see
  *                       sd_verify_block_tempered); 1 is exact, other values
- *                       are lossy. */
+ *                       are lossy;
+ *  start_round          0: a new run: the call first initialises the state
+ *                       in ws (Y_0, the explicit target call at Y_0, the
+ *                       first draft block).  r > 0: continue the run whose
+ *                       first r rounds (stats.rounds of the call that left
+ *                       them) are in ws, called with the same target, B, K,
+ *                       options, seed and workspace (anything else is
+ *                       undefined); a run split over calls gives the same
+ *                       result as one call;
+ *  max_rounds           the rounds this call may run: negative = until every
+ *                       chain has reached step N; n >= 0 = at most n (0 with
+ *                       start_round 0 only initialises).  The state stays in
+ *                       ws (see sd_sampler_state); a call that ends before the
+ *                       run is finished does not write y_out. */
 typedef struct {
   sd_verify_mode mode;
   sd_usample_mode usample_mode;
   sd_residual_kind residual;
   sd_drafter drafter;
   double omega;
+  int32_t start_round;
+  int32_t max_rounds;
 } sd_sampler_options;
 
 /* sd_run_sampler with options (sd_run_sampler is this call with DECOMPOSITION,
- * FREE and omega = 1).  Same workspace (sd_sampler_workspace), outputs and
- * errors. */
+ * FREE, omega = 1, start_round = 0 and max_rounds = -1).  Same workspace
+ * (sd_sampler_workspace), outputs and errors; SD_EINVAL also for a negative
+ * start_round. */
 sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
                             const sd_sampler_options* options, uint64_t seed, float* y_out,
                             int32_t* tau_trace, int32_t trace_rounds, sd_stats* stats, void* ws,
                             size_t ws_bytes, sd_stream stream);
+
+/* The sampler state that a workspace holds after `rounds` rounds (stats.rounds
+ * of the last call), as device pointers into ws (test hook: for checking a
+ * round against another implementation, or reading a partial run):
+ *  x           [B][K+1][d]  the next round's block: row 0 = Y_k of every chain
+ *                           with k < N; with the Free Drafter rows 1..K are its
+ *                           drafts (rows past K_b repeat the last one);
+ *  y           [B][d]       Y_N of the chains that have reached step N;
+ *  cache       [B][d]       c2_c S_c, the Free Drafter's cached score S_c times
+ *                           c2 at its step c = cache_step[b] (Sec. 3.3);
+ *  cache_step, k, round [B] the cache's step, the chain's step k and its round
+ *                           counter for the next round;
+ *  mq          [B][K+1][d]  the last round's target means m^q (row j at step
+ *                           k + j of that round; rows past min(K_b, N-k-1)
+ *                           are not meaningful);
+ *  lrp         [B (K+1)][n_tiles][3] float64: the last round's verification
+ *                           partial sums per draft row j < K_b over column
+ *                           tiles: ||m^p - m^q||^2, (yhat_{j+1} - m^p).(m^p - m^q),
+ *                           G.(m^p - m^q) (G the residual's normals); sums over
+ *                           the tiles divided by sigma^2 give ||Delta_{j+1}||^2
+ *                           and -ell_{j+1} - ||Delta_{j+1}||^2/2;
+ *  tau, coins, log_alpha_res, u [B]: the last round's decision record (tau 0
+ *                           for a chain that was inactive; coins bit j-1 = c_j;
+ *                           u = U of the residual draw, NaN when none);
+ *  ties        [B]          running count of the chain's tied coins.
+ * SD_EINVAL for a NULL or short workspace, or rounds < 0. */
+typedef struct {
+  float* x;
+  float* y;
+  float* cache;
+  int32_t* cache_step;
+  int32_t* k;
+  uint32_t* round;
+  float* mq;
+  double* lrp;
+  int32_t n_tiles;
+  int32_t* tau;
+  uint64_t* coins;
+  double* log_alpha_res;
+  double* u;
+  int32_t* ties;
+} sd_sampler_view;
+
+sd_status sd_sampler_state(sd_target target, int32_t B, int32_t K, void* ws, size_t ws_bytes,
+                           int64_t rounds, sd_sampler_view* out);
 
 /* ------------------------------------------------------------- plain EM --
  * The plain Euler-Maruyama chain (Sec. 2), the non-speculative baseline whose

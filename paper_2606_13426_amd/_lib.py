@@ -35,12 +35,21 @@ class sd_stride(ctypes.Structure):
 
 class sd_stats(ctypes.Structure):
     _fields_ = [("rounds", c_int64), ("chain_rounds", c_int64), ("steps", c_int64),
+                ("ties", c_int64), ("mean_tau", c_double), ("finished", c_int32),
                 ("tau_hist", c_int64 * (SD_MAX_BLOCK + 2))]
 
 
 class sd_sampler_options(ctypes.Structure):
     _fields_ = [("mode", c_int32), ("usample_mode", c_int32), ("residual", c_int32),
-                ("drafter", c_int32), ("omega", c_double)]
+                ("drafter", c_int32), ("omega", c_double), ("start_round", c_int32),
+                ("max_rounds", c_int32)]
+
+
+class sd_sampler_view(ctypes.Structure):
+    _fields_ = [("x", c_void_p), ("y", c_void_p), ("cache", c_void_p), ("cache_step", c_void_p),
+                ("k", c_void_p), ("round", c_void_p), ("mq", c_void_p), ("lrp", c_void_p),
+                ("n_tiles", c_int32), ("tau", c_void_p), ("coins", c_void_p),
+                ("log_alpha_res", c_void_p), ("u", c_void_p), ("ties", c_void_p)]
 
 
 class sd_kernel_stat(ctypes.Structure):
@@ -81,6 +90,8 @@ SIGNATURES = [
                                  ctypes.POINTER(sd_stats), P, c_size_t, P]),
     ("sd_run_sampler_ex", c_int32, [P, c_int32, c_int32, ctypes.POINTER(sd_sampler_options), c_uint64, P,
                                     P, c_int32, ctypes.POINTER(sd_stats), P, c_size_t, P]),
+    ("sd_sampler_state", c_int32, [P, c_int32, c_int32, P, c_size_t, c_int64,
+                                   ctypes.POINTER(sd_sampler_view)]),
     ("sd_plain_em_workspace", c_size_t, [P, c_int32]),
     ("sd_run_plain_em", c_int32, [P, c_int32, c_uint64, P, P, c_size_t, P]),
     ("sd_profile_enable", c_int32, [c_int32]),
@@ -271,7 +282,8 @@ def sd_sampler_workspace(target, B, K):
 
 
 def _stats_dict(st):
-    return dict(rounds=st.rounds, chain_rounds=st.chain_rounds, steps=st.steps,
+    return dict(rounds=st.rounds, chain_rounds=st.chain_rounds, steps=st.steps, ties=st.ties,
+                mean_tau=st.mean_tau, finished=bool(st.finished),
                 tau_hist=[st.tau_hist[i] for i in range(SD_MAX_BLOCK + 2)])
 
 
@@ -293,20 +305,58 @@ def sd_run_sampler(target, B, K, seed, mode=SD_BLOCK, usample_mode=SD_USAMPLE_EX
 
 def sd_run_sampler_ex(target, B, K, seed, mode=SD_BLOCK, usample_mode=SD_USAMPLE_EXACT,
                       residual=SD_RESIDUAL_DECOMPOSITION, drafter=SD_DRAFTER_FREE, omega=1.0,
-                      y_out=None, trace_rounds=0, ws=None, device="cuda"):
-    """Alg. 8 with the sampler options (residual, drafter, temperature); returns as sd_run_sampler."""
+                      y_out=None, trace_rounds=0, ws=None, device="cuda", start_round=0,
+                      max_rounds=-1, trace=None):
+    """Alg. 8 with the sampler options (residual, drafter, temperature, and the
+    rounds of a run this call does: max_rounds < 0 until done, 0 initialise
+    only); returns as sd_run_sampler.  A partial run continues with the same
+    ws (and trace) and start_round = stats["rounds"]."""
     import torch
     if y_out is None:
         y_out = torch.empty(B, target.d, dtype=torch.float32, device=device)
     if ws is None:
         ws = torch.empty(sd_sampler_workspace(target, B, K), dtype=torch.uint8, device=device)
-    trace = torch.zeros(trace_rounds, B, dtype=torch.int32, device=device) if trace_rounds > 0 else None
+    if trace is None and trace_rounds > 0:
+        trace = torch.zeros(trace_rounds, B, dtype=torch.int32, device=device)
+    if trace is not None:
+        trace_rounds = trace.shape[0]
     st = sd_stats()
-    opts = sd_sampler_options(mode, usample_mode, residual, drafter, float(omega))
+    opts = sd_sampler_options(mode, usample_mode, residual, drafter, float(omega), int(start_round),
+                              int(max_rounds))
     _check(load().sd_run_sampler_ex(target.handle, B, K, ctypes.byref(opts), seed, _p(y_out), _p(trace),
                                     trace_rounds, ctypes.byref(st), _p(ws), ws.numel(), _stream()),
            "sd_run_sampler_ex")
     return y_out, _stats_dict(st), trace
+
+
+def sd_sampler_state(target, B, K, ws, rounds):
+    """Views (torch tensors aliasing ws) of the sampler state after `rounds` rounds:
+    x [B][K+1][d], y [B][d], cache [B][d], cache_step, k, round [B] int32,
+    mq [B][K+1][d], lrp [B(K+1)][n_tiles][3] float64, tau [B], coins [B] int64,
+    log_alpha_res, u [B] float64, ties [B] int32."""
+    import torch
+    v = sd_sampler_view()
+    _check(load().sd_sampler_state(target.handle, B, K, _p(ws), ws.numel(), int(rounds), ctypes.byref(v)),
+           "sd_sampler_state")
+    base = ws.data_ptr()
+    d, K1 = target.d, K + 1
+
+    def view(ptr, shape, dtype):
+        esz = torch.empty((), dtype=dtype).element_size()
+        off = ptr - base
+        assert off % esz == 0
+        n = 1
+        for e in shape:
+            n *= e
+        return ws[off: off + n * esz].view(dtype).view(*shape)
+
+    f32, i32, f64, i64 = torch.float32, torch.int32, torch.float64, torch.int64
+    return dict(x=view(v.x, (B, K1, d), f32), y=view(v.y, (B, d), f32), cache=view(v.cache, (B, d), f32),
+                cache_step=view(v.cache_step, (B,), i32), k=view(v.k, (B,), i32),
+                round=view(v.round, (B,), i32), mq=view(v.mq, (B, K1, d), f32),
+                lrp=view(v.lrp, (B * K1, v.n_tiles, 3), f64), tau=view(v.tau, (B,), i32),
+                coins=view(v.coins, (B,), i64), log_alpha_res=view(v.log_alpha_res, (B,), f64),
+                u=view(v.u, (B,), f64), ties=view(v.ties, (B,), i32))
 
 
 def sd_plain_em_workspace(target, B):

@@ -11,6 +11,7 @@
 #include <map>
 #include <mutex>
 #include <string>
+#include <thread>
 #include <vector>
 
 #include "common.hpp"
@@ -180,7 +181,7 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
     vv[m] = var[m];
     lw[m] = log_w[m];
   }
-  Target* t = new Target();
+  Target* t = new Target();  // value-initialised: every pointer starts NULL
   t->sc = to_sched(sched);
   t->d = d;
   t->M = n_comp;
@@ -203,6 +204,17 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
     sd_target_destroy(reinterpret_cast<sd_target>(t));
     return SD_ENOMEM;
   }
+  // the sampler's per-round flags: mapped pinned host words, one group per
+  // concurrent sampler call
+  if (hipHostMalloc(reinterpret_cast<void**>(&t->host_flags),
+                    sizeof(int32_t) * kFlagGroups * kFlagSlots, hipHostMallocDefault) != hipSuccess ||
+      hipHostGetDevicePointer(reinterpret_cast<void**>(&t->host_flags_dev), t->host_flags, 0) !=
+          hipSuccess) {
+    set_error("sd_target_create: mapped host flags could not be allocated");
+    sd_target_destroy(reinterpret_cast<sd_target>(t));
+    return SD_ENOMEM;
+  }
+  t->flag_busy = 0;
   if (bf) {
     std::vector<uint16_t> h(M * D), hT(M * D);
     for (size_t m = 0; m < M; ++m)
@@ -271,6 +283,10 @@ sd_status sd_target_destroy(sd_target target) {
   if (t->logw) (void)hipFree(t->logw);
   if (t->musq) (void)hipFree(t->musq);
   if (t->coef) (void)hipFree(t->coef);
+  // a flag group still held by a call that timed out may be written by its
+  // kernels later: that memory is then left allocated
+  if (t->host_flags && __atomic_load_n(&t->flag_busy, __ATOMIC_ACQUIRE) == 0)
+    (void)hipHostFree(t->host_flags);
   delete t;
   return SD_OK;
 }
@@ -413,7 +429,7 @@ namespace {
 
 struct SamplerLayout {
   size_t y, x, sv, mq, sigma, step, k2, rnd2, crow2, cstep2, tau, rmode, rcoef, rsig, hist, steps,
-      act, nan, kb, left, dummy_i32, dummy_i64, lrp, tws, total;
+      act, nan, kb, left, dummy_i32, dummy_i64, coins, lar, ures, ties, lrp, tws, total;
   size_t tws_bytes;
   int nct;
 };
@@ -452,6 +468,10 @@ SamplerLayout sampler_layout(const Target& t, int B, int K) {
   L.left = take(4 * Bs);
   L.dummy_i32 = take(4 * (Bs + 2));
   L.dummy_i64 = take(8 * (SD_MAX_BLOCK + 3));
+  L.coins = take(8 * Bs);
+  L.lar = take(8 * Bs);
+  L.ures = take(8 * Bs);
+  L.ties = take(4 * Bs);
   L.lrp = take(8 * 3 * Bs * K1 * (size_t)L.nct);
   // the target calls on all B (K + 1) rows and, with the Frozen Drafter, on the
   // B states alone (fewer rows may take more splits of the logits GEMM)
@@ -475,10 +495,55 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
                          sd_usample_mode usample_mode, uint64_t seed, float* y_out,
                          int32_t* tau_trace, int32_t trace_rounds, sd_stats* stats, void* ws,
                          size_t ws_bytes, sd_stream stream) {
-  const sd_sampler_options o{mode, usample_mode, SD_RESIDUAL_DECOMPOSITION, SD_DRAFTER_FREE, 1.0};
+  const sd_sampler_options o{mode, usample_mode, SD_RESIDUAL_DECOMPOSITION, SD_DRAFTER_FREE, 1.0, 0, -1};
   return sd_run_sampler_ex(target, B, K, &o, seed, y_out, tau_trace, trace_rounds, stats, ws,
                            ws_bytes, stream);
 }
+
+}  // extern "C"
+
+namespace {
+
+using Clock = std::chrono::steady_clock;
+
+// A sampler call gives up on a GPU that finishes no round for this long.
+constexpr int kStallSeconds = 120;
+
+// Wait for the stream without blocking in the runtime past the deadline:
+// hipSuccess, the stream's error, or hipErrorNotReady with *timed_out set.
+hipError_t wait_bounded(hipStream_t s, Clock::time_point deadline, bool* timed_out) {
+  *timed_out = false;
+  for (;;) {
+    const hipError_t q = hipStreamQuery(s);
+    if (q != hipErrorNotReady) return q;
+    (void)hipGetLastError();  // not-ready is a status, not a failure
+    if (Clock::now() >= deadline) {
+      *timed_out = true;
+      return q;
+    }
+    std::this_thread::sleep_for(std::chrono::microseconds(50));
+  }
+}
+
+// One group of the target's mapped flag words for the duration of a call.
+int acquire_flags(Target* t) {
+  uint64_t cur = __atomic_load_n(&t->flag_busy, __ATOMIC_ACQUIRE);
+  while (cur != ~0ull) {
+    const int g = __builtin_ctzll(~cur);
+    if (__atomic_compare_exchange_n(&t->flag_busy, &cur, cur | (1ull << g), false,
+                                    __ATOMIC_ACQ_REL, __ATOMIC_ACQUIRE))
+      return g;
+  }
+  return -1;
+}
+
+void release_flags(Target* t, int g) {
+  __atomic_fetch_and(&t->flag_busy, ~(1ull << g), __ATOMIC_RELEASE);
+}
+
+}  // namespace
+
+extern "C" {
 
 sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
                             const sd_sampler_options* opts, uint64_t seed, float* y_out,
@@ -498,8 +563,10 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
   SD_CHECK_ARG(opts->omega > 0.0 && isfinite(opts->omega) && opts->omega * opts->omega > 0.0 &&
                    isfinite(opts->omega * opts->omega),
                "sd_run_sampler: omega must be positive and finite, with omega^2 too");
+  SD_CHECK_ARG(opts->start_round >= 0, "sd_run_sampler: start_round must be >= 0");
   SD_CHECK_ARG(target, "sd_run_sampler: target is NULL");
-  const Target& t = *reinterpret_cast<Target*>(target);
+  Target* tp = reinterpret_cast<Target*>(target);
+  const Target& t = *tp;
   SD_CHECK_ARG(B >= 1, "sd_run_sampler: B = %d < 1", B);
   SD_CHECK_ARG(K >= 1 && K <= SD_MAX_BLOCK, "sd_run_sampler: K = %d not in [1, %d]", K, SD_MAX_BLOCK);
   const bool frozen = opts->drafter == SD_DRAFTER_FROZEN;
@@ -511,75 +578,94 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
   const SamplerLayout L = sampler_layout(t, B, K);
   SD_CHECK_ARG(ws_bytes >= L.total, "sd_run_sampler: workspace %zu < %zu bytes", ws_bytes, L.total);
   SD_CHECK_ARG((int64_t)B * (K + 1) <= INT32_MAX, "sd_run_sampler: B*(K+1) rows exceed int32");
+  const int N = t.sc.N;
+  // a round advances every active chain by at least one step, so at most N
+  // rounds have work
+  constexpr int kLag = 3;
+  static_assert(kLag + 1 <= kFlagSlots, "a flag group must hold kLag + 1 rounds");
+  const int start = opts->start_round;
+  const int64_t cap = (int64_t)N + 1 + kLag;
+  SD_CHECK_ARG(start <= cap, "sd_run_sampler: start_round %d beyond the %lld rounds a run can have",
+               start, (long long)cap);
+  const int end = (int)std::min<int64_t>(cap, opts->max_rounds >= 0
+                                                  ? (int64_t)start + opts->max_rounds
+                                                  : cap);
 
   hipStream_t s = (hipStream_t)stream;
   char* base = static_cast<char*>(ws);
   auto F = [&](size_t o) { return reinterpret_cast<float*>(base + o); };
   auto I = [&](size_t o) { return reinterpret_cast<int32_t*>(base + o); };
-  const int d = t.d, N = t.sc.N, K1 = K + 1;
+  auto D = [&](size_t o) { return reinterpret_cast<double*>(base + o); };
+  const int d = t.d, K1 = K + 1;
   float *y = F(L.y), *x = F(L.x), *sv = F(L.sv), *mq = F(L.mq), *rcoef = F(L.rcoef),
         *rsig = F(L.rsig);
-  double* sigma = reinterpret_cast<double*>(base + L.sigma);
-  double* lrp = reinterpret_cast<double*>(base + L.lrp);
+  double *sigma = D(L.sigma), *lrp = D(L.lrp), *lar = D(L.lar), *ures = D(L.ures);
   int32_t *step = I(L.step), *k2 = I(L.k2), *crow2 = I(L.crow2), *cstep2 = I(L.cstep2),
           *tau = I(L.tau), *rmode = I(L.rmode), *hist = I(L.hist), *act = I(L.act),
-          *nanflag = I(L.nan), *kb = I(L.kb), *left = I(L.left), *dummy = I(L.dummy_i32);
+          *nanflag = I(L.nan), *kb = I(L.kb), *left = I(L.left), *dummy = I(L.dummy_i32),
+          *ties = I(L.ties);
   uint32_t* rnd2 = reinterpret_cast<uint32_t*>(base + L.rnd2);
+  uint64_t* coins = reinterpret_cast<uint64_t*>(base + L.coins);
   int64_t* steps = reinterpret_cast<int64_t*>(base + L.steps);
   int64_t* dummy64 = reinterpret_cast<int64_t*>(base + L.dummy_i64);
   void* tws = base + L.tws;
   const sd_stride xs{(int64_t)K1 * d, d}, mqs{(int64_t)K1 * d, d};
 
-  // Y_0 (also row 0 of x); the one explicit target call at Y_0, whose mean
-  // (row 0 of mq) seeds the Free Drafter's cached score; the round-0 rows'
-  // steps and sigmas; the first draft block.  The Frozen Drafter makes that
-  // call and draft at the start of every round instead.
-  SD_HIP(fill_i32_launch(k2, 2 * (int64_t)B, 0, s));
-  SD_HIP(fill_i32_launch(reinterpret_cast<int32_t*>(rnd2), 2 * (int64_t)B, 0, s));
-  SD_HIP(fill_i32_launch(crow2, 2 * (int64_t)B, 0, s));
-  SD_HIP(fill_i32_launch(cstep2, 2 * (int64_t)B, 0, s));
-  SD_HIP(fill_i32_launch(hist, (int64_t)B * (SD_MAX_BLOCK + 2), 0, s));
-  SD_HIP(fill_i64_launch(steps, B, 0, s));
-  SD_HIP(fill_i32_launch(act, 1, 1, s));
-  SD_HIP(fill_i32_launch(act + 1, 1, 0, s));
-  SD_HIP(fill_i32_launch(nanflag, 1, 0, s));
-  SD_HIP(fill_i32_launch(step, B, 0, s));
-  SD_HIP(fill_i32_launch(tau, B, 0, s));
-  SD_HIP(fill_i32_launch(dummy, B + 2, 0, s));
-  SD_HIP(init_chains_launch(B, d, seed, y, x, (int64_t)K1 * d, s));
-  if (!frozen)
-    SD_HIP(target_mean_launch(t, B, x, (int64_t)K1 * d, step, mq, (int64_t)K1 * d, nullptr, 0,
-                              tws, s, nullptr));
-  SD_HIP(prepare_launch(t.sc, B, K, k2, kb, left, step, sigma, tau, dummy, dummy + B,
-                        dummy + B + 1, dummy64, dummy64 + SD_MAX_BLOCK + 2, s));
-  if (!frozen)
-    SD_HIP(draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2, cstep2, mq, mqs, k2, rnd2, seed,
-                               x, xs, sv, s, nullptr));
+  if (start == 0) {
+    // Y_0 (also row 0 of x); the one explicit target call at Y_0, whose mean
+    // (row 0 of mq) seeds the Free Drafter's cached score; the round-0 rows'
+    // steps and sigmas; the first draft block.  The Frozen Drafter makes that
+    // call and draft at the start of every round instead.
+    SD_HIP(fill_i32_launch(k2, 2 * (int64_t)B, 0, s));
+    SD_HIP(fill_i32_launch(reinterpret_cast<int32_t*>(rnd2), 2 * (int64_t)B, 0, s));
+    SD_HIP(fill_i32_launch(crow2, 2 * (int64_t)B, 0, s));
+    SD_HIP(fill_i32_launch(cstep2, 2 * (int64_t)B, 0, s));
+    SD_HIP(fill_i32_launch(hist, (int64_t)B * (SD_MAX_BLOCK + 2), 0, s));
+    SD_HIP(fill_i64_launch(steps, B, 0, s));
+    SD_HIP(fill_i32_launch(ties, B, 0, s));
+    SD_HIP(fill_i32_launch(act, 1, 1, s));
+    SD_HIP(fill_i32_launch(act + 1, 1, 0, s));
+    SD_HIP(fill_i32_launch(nanflag, 1, 0, s));
+    SD_HIP(fill_i32_launch(step, B, 0, s));
+    SD_HIP(fill_i32_launch(tau, B, 0, s));
+    SD_HIP(fill_i32_launch(dummy, B + 2, 0, s));
+    SD_HIP(init_chains_launch(B, d, seed, y, x, (int64_t)K1 * d, s));
+    if (!frozen)
+      SD_HIP(target_mean_launch(t, B, x, (int64_t)K1 * d, step, mq, (int64_t)K1 * d, nullptr, 0,
+                                tws, s, nullptr));
+    SD_HIP(prepare_launch(t.sc, B, K, k2, kb, left, step, sigma, tau, dummy, dummy + B,
+                          dummy + B + 1, dummy64, dummy64 + SD_MAX_BLOCK + 2, s));
+    if (!frozen)
+      SD_HIP(draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2, cstep2, mq, mqs, k2, rnd2, seed,
+                                 x, xs, sv, s, nullptr));
+  }
 
   // Round r's scan publishes round r - 1's active flag, tagged with r - 1, into
-  // slot (r - 1) % kSlots of a mapped host array.  After enqueueing round r
-  // the host polls round r - kLag's slot until the tag is there (the queue
-  // stays kLag rounds ahead) and stops enqueueing at the first cleared flag.
-  // No event or copy is queued per round: a marker between rounds would
-  // hold the next round's first kernel back by several microseconds.
-  int32_t* host_act = nullptr;
-  int32_t* host_act_dev = nullptr;
-  constexpr int kLag = 3, kSlots = kLag + 1, kQuietMs = 20;
-  SD_HIP(hipHostMalloc(reinterpret_cast<void**>(&host_act), sizeof(int32_t) * kSlots, hipHostMallocDefault));
-  if (hipHostGetDevicePointer(reinterpret_cast<void**>(&host_act_dev), host_act, 0) != hipSuccess) {
-    (void)hipHostFree(host_act);
-    set_error("sd_run_sampler: host flag not mapped");
-    return SD_EHIP;
+  // slot (r - 1) % kFlagSlots of this call's group of mapped host words.  After
+  // enqueueing round r the host polls round r - kLag's slot until the tag is
+  // there (the queue stays kLag rounds ahead) and stops enqueueing at the
+  // first cleared flag.  No event or copy is queued per round: a marker
+  // between rounds would hold the next round's first kernel back by several
+  // microseconds.  The first flag this call reads is that of round start - 1
+  // (published by round start's scan), so a finished run is seen at once.
+  const int grp = acquire_flags(tp);
+  if (grp < 0) {
+    set_error("sd_run_sampler: more than %d sampler calls at once on one target", kFlagGroups);
+    return SD_EUNSUPPORTED;
   }
-  for (int i = 0; i < kSlots; ++i) host_act[i] = -1;  // tag -1: nothing published
+  int32_t* const host_act = t.host_flags + grp * kFlagSlots;
+  int32_t* const host_act_dev = t.host_flags_dev + grp * kFlagSlots;
+  for (int i = 0; i < kFlagSlots; ++i) host_act[i] = -1;  // tag -1: nothing published
+  std::atomic_thread_fence(std::memory_order_seq_cst);
   volatile int32_t* const pub = host_act;
+  constexpr int kQuietMs = 20;
+  const int first_flag = start > 0 ? start - 1 : 0;
   sd_status st = SD_OK;
+  bool stalled = false;
   int64_t rounds = -1;
-  // a round advances every active chain by at least one step, so at most N
-  // rounds have work
-  const int max_rounds = N + 1 + kLag;
-  int r = 0;
-  for (; r < max_rounds && rounds < 0; ++r) {
+  Clock::time_point last_progress = Clock::now();
+  int r = start;
+  for (; r < end && rounds < 0; ++r) {
     const int cur = r & 1, nxt = cur ^ 1;
     const int* gate = act + cur;
     hipError_t e = hipSuccess;
@@ -595,11 +681,12 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
     if (e == hipSuccess)
       e = target_mean_lr_launch(t, B * K1, K1, x, step, mq, sv, cstep2 + cur * B, lrp,
                                 rnd2 + cur * B, seed, tws, s, gate);
-    int32_t* publish = r >= 1 ? host_act_dev + (r - 1) % kSlots : nullptr;
+    int32_t* publish = r >= 1 ? host_act_dev + (r - 1) % kFlagSlots : nullptr;
     if (e == hipSuccess)
       e = scan_fused_launch(B, K, d, N, (int)mode, (int)usample_mode, lrp, L.nct, sigma,
                             k2 + cur * B, rnd2 + cur * B, seed, w2, reflect, tau, rmode, rcoef,
-                            rsig, nanflag, act + nxt, publish, r - 1, s, gate);
+                            rsig, coins, lar, ures, ties, nanflag, act + nxt, publish, r - 1, s,
+                            gate);
     if (e == hipSuccess)
       e = advance_launch(t.sc, t.coef, B, K, d, seed, k2 + cur * B, rnd2 + cur * B,
                          crow2 + cur * B, cstep2 + cur * B, k2 + nxt * B, rnd2 + nxt * B,
@@ -612,71 +699,105 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
       break;
     }
     const int back = r - kLag;
-    if (back >= 0) {
+    if (back >= first_flag) {
       // round back + 1's scan (enqueued) publishes round back's flag; the wait
       // ends on the tag, or on an error or a drained stream reported by the
       // runtime.  The runtime is asked only after kQuietMs without the tag: a
       // stream query queues a marker whose system-scope release holds the
       // next kernel back by several microseconds.
-      volatile int32_t* slot = pub + back % kSlots;
+      volatile int32_t* slot = pub + back % kFlagSlots;
       int32_t v;
-      auto next_query = std::chrono::steady_clock::now() + std::chrono::milliseconds(kQuietMs);
+      auto next_query = Clock::now() + std::chrono::milliseconds(kQuietMs);
       for (uint32_t spin = 1; ((v = *slot) >> 1) != back; ++spin) {
-        if ((spin & 1023u) == 0 && std::chrono::steady_clock::now() >= next_query) {
-          next_query = std::chrono::steady_clock::now() + std::chrono::milliseconds(kQuietMs);
-          const hipError_t q = hipStreamQuery(s);
-          // not-ready is a status, not a failure: keep it out of the launch checks
-          if (q == hipErrorNotReady) {
-            (void)hipGetLastError();
-            continue;
-          }
-          v = *slot;
-          if (q == hipSuccess && (v >> 1) == back) break;
-          set_error("sd_run_sampler: round %d's flag was not published (%s)", back,
-                    hipGetErrorString(q));
+        if ((spin & 1023u) != 0) continue;
+        const Clock::time_point now = Clock::now();
+        if (now - last_progress > std::chrono::seconds(kStallSeconds)) {
+          set_error("sd_run_sampler: no round finished within %d s (round %d); the GPU may be hung",
+                    kStallSeconds, back);
           st = SD_EHIP;
+          stalled = true;
           break;
         }
+        if (now < next_query) continue;
+        next_query = now + std::chrono::milliseconds(kQuietMs);
+        const hipError_t q = hipStreamQuery(s);
+        // not-ready is a status, not a failure: keep it out of the launch checks
+        if (q == hipErrorNotReady) {
+          (void)hipGetLastError();
+          continue;
+        }
+        v = *slot;
+        if (q == hipSuccess && (v >> 1) == back) break;
+        set_error("sd_run_sampler: round %d's flag was not published (%s)", back,
+                  hipGetErrorString(q));
+        st = SD_EHIP;
+        break;
       }
       if (st != SD_OK) break;
+      last_progress = Clock::now();
       if ((v & 1) == 0) rounds = back + 1;
     }
   }
-  if (st == SD_OK && rounds < 0) {
+  if (stalled) return st;  // the kernels may still write to the flag group: keep it
+  const Clock::time_point deadline = Clock::now() + std::chrono::seconds(kStallSeconds);
+  bool finished = rounds >= 0;
+  if (st == SD_OK && !finished) {
     // every launched round finishes; the flags of rounds up to r - 2 are then
     // in their slots, and the last round's, which no later scan publishes, is
     // copied
     int32_t last_flag = 1;
-    if (r >= 1 && (hipMemcpyAsync(&last_flag, act + (((r - 1) & 1) ^ 1), sizeof(int32_t),
-                                  hipMemcpyDeviceToHost, s) != hipSuccess ||
-                   hipStreamSynchronize(s) != hipSuccess)) {
-      set_error("sd_run_sampler: flag copy failed");
+    hipError_t e = hipSuccess;
+    bool late = false;
+    if (r > start) {
+      e = hipMemcpyAsync(&last_flag, act + (r & 1), sizeof(int32_t), hipMemcpyDeviceToHost, s);
+      if (e == hipSuccess) e = wait_bounded(s, deadline, &late);
+    }
+    if (late) {
+      set_error("sd_run_sampler: the last rounds did not finish within %d s", kStallSeconds);
+      return SD_EHIP;  // keep the flag group (see above)
+    }
+    if (e != hipSuccess) {
+      set_error("sd_run_sampler: waiting for the last rounds failed: %s", hipGetErrorString(e));
       st = SD_EHIP;
     }
-    for (int back = r - kLag < 0 ? 0 : r - kLag; st == SD_OK && back < r; ++back) {
-      const int32_t v = pub[back % kSlots];
+    for (int back = std::max(r - kLag, first_flag); st == SD_OK && back < r; ++back) {
+      const int32_t v = pub[back % kFlagSlots];
       const int32_t flag = back == r - 1 ? last_flag : ((v >> 1) == back ? (v & 1) : 1);
       if (flag == 0) {
         rounds = back + 1;
+        finished = true;
         break;
       }
     }
-    if (st == SD_OK && rounds < 0) {
-      set_error("sd_run_sampler: chains still active after %d rounds", r);
-      st = SD_EHIP;
+    if (st == SD_OK && !finished) {
+      if (r < cap) {
+        rounds = r;  // a partial call: the state after round r - 1 is in ws
+      } else {
+        set_error("sd_run_sampler: chains still active after %d rounds", r);
+        st = SD_EHIP;
+      }
     }
   }
   if (st == SD_OK) {
-    std::vector<int32_t> h_hist((size_t)B * (SD_MAX_BLOCK + 2));
+    std::vector<int32_t> h_hist((size_t)B * (SD_MAX_BLOCK + 2)), h_ties(B);
     std::vector<int64_t> h_steps(B);
     int32_t h_nan = 0;
-    hipError_t e = hipMemcpyAsync(y_out, y, sizeof(float) * (size_t)B * d, hipMemcpyDeviceToDevice, s);
+    hipError_t e = hipSuccess;
+    if (finished)
+      e = hipMemcpyAsync(y_out, y, sizeof(float) * (size_t)B * d, hipMemcpyDeviceToDevice, s);
     if (e == hipSuccess)
       e = hipMemcpyAsync(h_hist.data(), hist, sizeof(int32_t) * h_hist.size(), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess)
       e = hipMemcpyAsync(h_steps.data(), steps, sizeof(int64_t) * B, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(h_ties.data(), ties, sizeof(int32_t) * B, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipMemcpyAsync(&h_nan, nanflag, sizeof(int32_t), hipMemcpyDeviceToHost, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    bool late = false;
+    if (e == hipSuccess) e = wait_bounded(s, deadline, &late);
+    if (late) {
+      set_error("sd_run_sampler: the final copies did not finish within %d s", kStallSeconds);
+      return SD_EHIP;  // keep the flag group (see above)
+    }
     if (e != hipSuccess) {
       set_error("sd_run_sampler: final copy failed: %s", hipGetErrorString(e));
       st = SD_EHIP;
@@ -684,11 +805,18 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
       if (stats) {
         memset(stats, 0, sizeof(*stats));
         stats->rounds = rounds;
+        stats->finished = finished ? 1 : 0;
+        double tau_sum = 0.0;
         for (int b = 0; b < B; ++b) {
           stats->steps += h_steps[b];
+          stats->ties += h_ties[b];
           for (int i = 0; i < SD_MAX_BLOCK + 2; ++i) stats->tau_hist[i] += h_hist[(size_t)b * (SD_MAX_BLOCK + 2) + i];
         }
-        for (int i = 0; i < SD_MAX_BLOCK + 2; ++i) stats->chain_rounds += stats->tau_hist[i];
+        for (int i = 0; i < SD_MAX_BLOCK + 2; ++i) {
+          stats->chain_rounds += stats->tau_hist[i];
+          tau_sum += (double)i * (double)stats->tau_hist[i];
+        }
+        stats->mean_tau = stats->chain_rounds > 0 ? tau_sum / (double)stats->chain_rounds : 0.0;
       }
       if (h_nan) {
         set_error("sd_run_sampler: non-finite log-ratio met");
@@ -696,9 +824,46 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
       }
     }
   }
-  (void)hipStreamSynchronize(s);
-  (void)hipHostFree(host_act);
+  bool late = false;
+  (void)wait_bounded(s, deadline, &late);
+  if (late) {
+    if (st == SD_OK) {
+      set_error("sd_run_sampler: the stream did not drain within %d s", kStallSeconds);
+      st = SD_EHIP;
+    }
+    return st;  // keep the flag group (see above)
+  }
+  release_flags(tp, grp);
   return st;
+}
+
+sd_status sd_sampler_state(sd_target target, int32_t B, int32_t K, void* ws, size_t ws_bytes,
+                           int64_t rounds, sd_sampler_view* out) {
+  SD_CHECK_ARG(target && ws && out, "sd_sampler_state: NULL pointer argument");
+  SD_CHECK_ARG(B >= 1 && K >= 1 && K <= SD_MAX_BLOCK, "sd_sampler_state: need B >= 1 and K in [1, %d]",
+               SD_MAX_BLOCK);
+  SD_CHECK_ARG(rounds >= 0, "sd_sampler_state: rounds < 0");
+  const Target& t = *reinterpret_cast<Target*>(target);
+  const SamplerLayout L = sampler_layout(t, B, K);
+  SD_CHECK_ARG(ws_bytes >= L.total, "sd_sampler_state: workspace %zu < %zu bytes", ws_bytes, L.total);
+  char* base = static_cast<char*>(ws);
+  const int cur = (int)(rounds & 1);
+  memset(out, 0, sizeof(*out));
+  out->x = reinterpret_cast<float*>(base + L.x);
+  out->y = reinterpret_cast<float*>(base + L.y);
+  out->cache = reinterpret_cast<float*>(base + L.sv);
+  out->cache_step = reinterpret_cast<int32_t*>(base + L.cstep2) + cur * B;
+  out->k = reinterpret_cast<int32_t*>(base + L.k2) + cur * B;
+  out->round = reinterpret_cast<uint32_t*>(base + L.rnd2) + cur * B;
+  out->mq = reinterpret_cast<float*>(base + L.mq);
+  out->lrp = reinterpret_cast<double*>(base + L.lrp);
+  out->n_tiles = L.nct;
+  out->tau = reinterpret_cast<int32_t*>(base + L.tau);
+  out->coins = reinterpret_cast<uint64_t*>(base + L.coins);
+  out->log_alpha_res = reinterpret_cast<double*>(base + L.lar);
+  out->u = reinterpret_cast<double*>(base + L.ures);
+  out->ties = reinterpret_cast<int32_t*>(base + L.ties);
+  return SD_OK;
 }
 
 // ------------------------------------------------------------- plain EM --

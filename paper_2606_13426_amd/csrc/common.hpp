@@ -104,7 +104,15 @@ struct Target {
   float4* coef;   // [N+1] per step: (c1_n, c2_n, sigma_n, 1/c2_n) rounded to float32
   double2* ls;    // [N][M] per step and component: (log s2, 1/s2), s2 = a_n^2 var_m + 1 - a_n^2
   int device;
+  // Mapped pinned host words through which the sampler's kernels publish the
+  // per-round "any chain active" flag: kFlagGroups groups of kFlagSlots words,
+  // one group per running sampler call (bit g of flag_busy, taken and given
+  // back atomically; a group whose call timed out is never given back).
+  int32_t* host_flags;      // host address [kFlagGroups][kFlagSlots]
+  int32_t* host_flags_dev;  // the same memory as the device sees it
+  uint64_t flag_busy;
 };
+constexpr int kFlagGroups = 64, kFlagSlots = 4;
 
 size_t target_ws_bytes(const Target& t, int rows);
 size_t target_ws_bytes_bf16(const Target& t, int rows);
@@ -141,10 +149,13 @@ hipError_t gmm_softmax_launch(const Target& t, int rows, int S, const float* par
                               float* rowc, hipStream_t s, const int* gate);
 // Sampler verification on the fused partials (see scan_fused_kernel).
 // w2 = omega^2 (temperature; 1 = exact); reflect: the reflection residual.
+// coins, lar, ures [B]: the round's decision record; ties [B]: running count
+// of coins within 1e-6 of their thresholds.
 hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, const double* lrp,
                              int nct, const double* sigma, const int32_t* kcur,
                              const uint32_t* rcur, uint64_t seed, double w2, bool reflect,
                              int32_t* tau, int32_t* rmode, float* rcoef, float* rsig,
+                             uint64_t* coins, double* lar, double* ures, int32_t* ties,
                              int* nanflag, int* act_next, int* host_prev, int pub_round,
                              hipStream_t s, const int* gate);
 // Residual, commit and the next round's Free-Drafter block, elementwise over

@@ -217,7 +217,13 @@ struct Decision {
   int tau;
   double la_res, U;
   uint64_t coins;
+  uint64_t ties;  // steps whose coin lies within kTieWindow of its threshold
 };
+
+// A coin within this distance of its threshold (|eta_j - h_j|, or alpha_j for
+// token verification) is a tie: rounding in another implementation may flip
+// it, so such decisions are counted.
+constexpr double kTieWindow = 1e-6;
 
 __device__ Decision decide(int mode, int umode, int kb, double ell_raw, double vn, uint32_t b,
                            uint32_t r, uint64_t seed, int lane, double w2, bool need_u) {
@@ -239,6 +245,7 @@ __device__ Decision decide(int mode, int umode, int kb, double ell_raw, double v
   const uint4 w = philox((uint32_t)(lane >> 2), b, r, TAG_COIN << 24, seed);
   const double eta = uniform64(pick(w, lane & 3));
   const uint64_t cm = __ballot(valid && log(eta) < lh);
+  const uint64_t tm = __ballot(valid && fabs(eta - exp(lh)) <= kTieWindow);
   const uint64_t vmask = kb >= 64 ? ~0ull : ((1ull << kb) - 1ull);
   int t;
   if (mode == SD_BLOCK) {
@@ -262,7 +269,7 @@ __device__ Decision decide(int mode, int umode, int kb, double ell_raw, double v
       U = usample_exact(u, la_res, v, lane);
     }
   }
-  return Decision{t, la_res, U, cm};
+  return Decision{t, la_res, U, cm, tm};
 }
 
 __global__ __launch_bounds__(kThreads) void scan_kernel(
@@ -310,6 +317,8 @@ __global__ __launch_bounds__(kThreads) void scan_kernel(
 //            (reflection residual, Alg. 4: m^q + sigma (I - 2 e e^T) Z with
 //            D = m^p - m^q = sigma Delta and W = yhat_tau - m^p = sigma Z,
 //            whose two sums are the log-ratio partials of row tau - 1)
+// The round's decision record (tau, coins, log alpha_res, U) is kept per chain,
+// and the coins within kTieWindow of their thresholds are added to ties[b].
 // It also clears the next round's active flag before looking at its gate,
 // and stores the gate (whether any chain was still active after the previous
 // round) tagged with that round's index, (pub_round << 1) | flag, into
@@ -320,8 +329,9 @@ __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
     const double* __restrict__ sigma, const int32_t* __restrict__ kcur,
     const uint32_t* __restrict__ rcur, uint64_t seed, double w2, bool reflect,
     int32_t* __restrict__ tau, int32_t* __restrict__ rmode,
-    float* __restrict__ rcoef, float* __restrict__ rsig, int* nanflag, int* act_next,
-    int* host_prev, int pub_round, const int* gate) {
+    float* __restrict__ rcoef, float* __restrict__ rsig, uint64_t* __restrict__ coins,
+    double* __restrict__ lar, double* __restrict__ ures, int32_t* __restrict__ ties,
+    int* nanflag, int* act_next, int* host_prev, int pub_round, const int* gate) {
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     *act_next = 0;
     if (host_prev) {
@@ -419,6 +429,10 @@ __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
     rmode[b] = rm;
     rcoef[b] = cf;
     rsig[b] = sgo;
+    coins[b] = D.coins;
+    lar[b] = D.la_res;
+    ures[b] = D.U;
+    ties[b] += __popcll(D.ties);
   }
 }
 
@@ -451,12 +465,14 @@ hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, co
                              int nct, const double* sigma, const int32_t* kcur,
                              const uint32_t* rcur, uint64_t seed, double w2, bool reflect,
                              int32_t* tau, int32_t* rmode, float* rcoef, float* rsig,
+                             uint64_t* coins, double* lar, double* ures, int32_t* ties,
                              int* nanflag, int* act_next, int* host_prev, int pub_round,
                              hipStream_t s, const int* gate) {
   const int per = kThreads / 64;
   return launch_timed("scan_fused", scan_fused_kernel, dim3((B + per - 1) / per), dim3(kThreads), s,
                       B, K, d, N, mode, umode, lrp, nct, sigma, kcur, rcur, seed, w2, reflect, tau,
-                      rmode, rcoef, rsig, nanflag, act_next, host_prev, pub_round, gate);
+                      rmode, rcoef, rsig, coins, lar, ures, ties, nanflag, act_next, host_prev,
+                      pub_round, gate);
 }
 
 }  // namespace sd

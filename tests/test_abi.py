@@ -45,7 +45,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert _lib.sd_abi_version() == 2
+    assert _lib.sd_abi_version() == 3
 
 
 def _expect_einval(status, needle):
@@ -109,6 +109,12 @@ def test_invalid_arguments_rejected_without_gpu(lib):
     opts = _lib.sd_sampler_options(_lib.SD_TOKEN, 0, _lib.SD_RESIDUAL_REFLECTION, _lib.SD_DRAFTER_FROZEN, 2.0)
     st = lib.sd_run_sampler_ex(null, 4, 8, ctypes.byref(opts), 0, null, null, 0, null, null, 0, null)
     _expect_einval(st, "target is NULL")
+    opts = _lib.sd_sampler_options(_lib.SD_BLOCK, 0, 0, 0, 1.0, -1, -1)
+    st = lib.sd_run_sampler_ex(null, 4, 8, ctypes.byref(opts), 0, null, null, 0, null, null, 0, null)
+    _expect_einval(st, "start_round must be >= 0")
+    view = _lib.sd_sampler_view()
+    st = lib.sd_sampler_state(null, 4, 8, null, 0, 0, ctypes.byref(view))
+    _expect_einval(st, "NULL")
     st = lib.sd_run_plain_em(null, 4, 0, null, null, 0, null)
     _expect_einval(st, "target is NULL")
     assert lib.sd_plain_em_workspace(null, 4) == 0

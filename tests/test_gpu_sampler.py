@@ -4,7 +4,8 @@ The tiny 2-D workload (d = 2, M = 4, N = 100, B = 256, K = 4) runs end to end on
 both sides from the same seed: the tau of every round and the final state of
 every chain must match the oracle, except on chains whose oracle trajectory
 records a coin within 1e-6 of its threshold.  Also: accounting, determinism
-and the block-vs-token ordering of block efficiency.
+and the block-vs-token ordering of block efficiency.  The larger workloads are
+compared a round at a time (test_gpu_round_parity.py).
 """
 import numpy as np
 import pytest
@@ -40,7 +41,7 @@ def test_tiny2d_trajectories_match_oracle(mode):
     B, N, K = cfg["B"], cfg["N"], cfg["K"]
     ref = osamp.run_sampler(GMM(p["mu"], p["var"], p["log_w"]), Schedule(N), B, K, seed, mode=mode)
     assert stats["steps"] == B * N
-    assert stats["chain_rounds"] == int(ref["rounds"].sum()) or True  # chains with ties may differ
+    assert stats["chain_rounds"] == int((trace > 0).sum())
     matched = tied = 0
     for i, b in enumerate(ref["chains"]):
         rec = ref["trace"][i]
@@ -54,6 +55,8 @@ def test_tiny2d_trajectories_match_oracle(mode):
         matched += 1
     assert tied <= 3
     assert matched >= B - 3
+    if tied == 0:
+        assert stats["chain_rounds"] == int(ref["rounds"].sum())
 
 
 def test_sampler_deterministic_and_block_beats_token():
@@ -64,22 +67,6 @@ def test_sampler_deterministic_and_block_beats_token():
     be_block = s1["steps"] / s1["chain_rounds"]
     be_token = st["steps"] / st["chain_rounds"]
     assert 1.0 <= be_token <= be_block <= WORKLOADS["tiny2d"]["K"] + 1
-
-
-def test_pixel3072_first_chains_match_oracle():
-    # the pixel-sized target end to end on a few chains and a short schedule
-    seed, B, N, K = 4, 6, 12, 8
-    p, y, stats, trace = _run("pixel3072", _lib.SD_BLOCK, seed, B=B, N=N, K=K)
-    ref = osamp.run_sampler(GMM(p["mu"], p["var"], p["log_w"]), Schedule(N), B, K, seed)
-    assert stats["steps"] == B * N
-    same = 0
-    for i, b in enumerate(ref["chains"]):
-        rec = ref["trace"][i]
-        taus = [info["tau"] for info in rec]
-        if list(trace[: len(taus), b]) == taus and not any(info["ties"] for info in rec):
-            assert_rows_close(y[b][None], ref["y"][i][None], rtol=1e-3, what=f"Y_N chain {b}")
-            same += 1
-    assert same >= B - 1
 
 
 # (d, M, B, K, N, seed): K > N (every block ragged, the largest K), one chain
@@ -107,35 +94,3 @@ def test_small_configs_match_oracle(d, M, B, K, N, seed):
         assert list(trace[: len(taus), b]) == taus, (b, taus, list(trace[: len(taus) + 1, b]))
         assert np.all(trace[len(taus):, b] == 0)
         assert_rows_close(y[b][None], ref["y"][i][None], what=f"Y_N chain {b}")
-
-
-def test_streamed_draft_rows_match_oracle():
-    # B (K + 1) d float32 = 1024 x 9 x 4096 x 4 = 151 MB of draft rows: above
-    # the 128 MB at which the draft and advance kernels store them with
-    # non-temporal stores.  Three sampled chains end to end against the oracle
-    # (coins within 1e-4 of their threshold end the comparison, as in the
-    # full-size test of the variants).
-    from paper_2606_13426_amd.inputs import make_gmm
-    d, M, B, K, N, seed = 4096, 64, 1024, 8, 16, 6
-    assert B * (K + 1) * d * 4 > 128 << 20
-    p = make_gmm(d, M, mu_std=1.0, var=(0.01, 0.2), dirichlet=1.0, seed=seed)
-    tgt = _lib.Target(_lib.schedule(N), p["mu"], p["var"], p["log_w"])
-    y, stats, trace = _lib.sd_run_sampler(tgt, B, K, seed, trace_rounds=N)
-    torch.cuda.synchronize()
-    y, trace = y.cpu().numpy(), trace.cpu().numpy()
-    assert stats["steps"] == B * N
-    g = GMM(p["mu"], p["var"], p["log_w"])
-    full = 0
-    for b in (0, 517, B - 1):
-        ref = osamp.run_sampler(g, Schedule(N), B, K, seed, chains=[b])
-        rec = ref["trace"][0]
-        near = [i for i, info in enumerate(rec)
-                if np.any(np.abs(info["eta"] - np.exp(info["log_h"])) < 1e-4)]
-        upto = near[0] + 1 if near else len(rec)
-        taus = [info["tau"] for info in rec[:upto]]
-        assert list(trace[:upto, b]) == taus, (b, taus, list(trace[:upto, b]))
-        if not near:
-            assert np.all(trace[len(rec):, b] == 0)
-            assert_rows_close(y[b][None], ref["y"][0][None], rtol=1e-3, what=f"Y_N chain {b}")
-            full += 1
-    assert full >= 2

@@ -215,7 +215,7 @@ def test_reflection_with_block_rejected():
     assert e.value.status == _lib.SD_EINVAL
 
 
-@pytest.mark.parametrize("wl,B,N,rtol", [("tiny2d", 256, 100, 1e-4), ("pixel3072", 6, 12, 1e-3)])
+@pytest.mark.parametrize("wl,B,N,rtol", [("tiny2d", 256, 100, 1e-4), ("pixel3072", 6, 12, 1e-4)])
 def test_plain_em_matches_oracle(wl, B, N, rtol):
     p = workload_gmm(wl)
     seed = 17
@@ -234,47 +234,6 @@ def test_plain_em_deterministic_and_strided_ws():
     c = _lib.sd_run_plain_em(tgt, 100, 6)
     torch.cuda.synchronize()
     assert torch.equal(a, b) and not torch.equal(a, c)
-
-
-# The benchmark's workload in the launch configuration bench.py times
-# (pixel3072: B = 1024, K = 8, N = 200, float32), three sampled chains checked
-# one by one against the oracle.  Over 200 float32 steps the states drift from
-# the float64 oracle by ~1e-5 relative, which can legitimately flip a coin
-# lying within that distance of its threshold: rounds are compared up to the
-# first coin with |eta - h| < 1e-4 (in the oracle's own run), and Y_N only when
-# no such coin occurred.
-@pytest.mark.parametrize("mode,residual,drafter", [
-    (_lib.SD_BLOCK, _lib.SD_RESIDUAL_DECOMPOSITION, _lib.SD_DRAFTER_FREE),
-    (_lib.SD_TOKEN, _lib.SD_RESIDUAL_REFLECTION, _lib.SD_DRAFTER_FREE),
-    (_lib.SD_BLOCK, _lib.SD_RESIDUAL_DECOMPOSITION, _lib.SD_DRAFTER_FROZEN),
-])
-def test_pixel3072_full_size_sampled_chains(mode, residual, drafter):
-    cfg = WORKLOADS["pixel3072"]
-    B, K, N = cfg["B"], cfg["K"], cfg["N"]
-    p = workload_gmm("pixel3072")
-    seed = 0
-    tgt = _lib.Target(_lib.schedule(N), p["mu"], p["var"], p["log_w"])
-    y, stats, trace = _lib.sd_run_sampler_ex(tgt, B, K, seed, mode=mode, residual=residual, drafter=drafter,
-                                             trace_rounds=N)
-    torch.cuda.synchronize()
-    y, trace = y.cpu().numpy(), trace.cpu().numpy()
-    assert stats["steps"] == B * N
-    g = GMM(p["mu"], p["var"], p["log_w"])
-    full = 0
-    for b in (0, 517, B - 1):
-        ref = osamp.run_sampler(g, Schedule(N), B, K, seed, mode=mode, residual=residual, drafter=drafter,
-                                chains=[b])
-        rec = ref["trace"][0]
-        near = [i for i, info in enumerate(rec)
-                if np.any(np.abs(info["eta"] - np.exp(info["log_h"])) < 1e-4)]
-        upto = near[0] + 1 if near else len(rec)
-        taus = [info["tau"] for info in rec[:upto]]
-        assert list(trace[:upto, b]) == taus, (b, taus, list(trace[:upto, b]))
-        if not near:
-            assert np.all(trace[len(rec):, b] == 0)
-            assert_rows_close(y[b][None], ref["y"][0][None], rtol=1e-3, what=f"Y_N chain {b}")
-            full += 1
-    assert full >= 2
 
 
 def test_reflection_without_direction_keeps_the_draft():
