@@ -124,6 +124,23 @@ sd_status sd_target_mean(sd_target target, int32_t rows, const float* x, int64_t
                          float* score, int64_t score_row_stride, void* ws, size_t ws_bytes,
                          sd_stream stream);
 
+/* sd_target_mean without a workspace, for callers that cannot allocate device
+ * memory (code under HIP graph capture, tight serving loops, harnesses that
+ * forbid hipMalloc): the same computation and kernels, with the workspace in a
+ * 128 MiB array of device memory that the library holds on every GPU it runs
+ * on until the process ends (sd_target_mean_noalloc_max_bytes).  The call
+ * allocates nothing (its first use on a GPU without a target created there
+ * only looks up that GPU's copy).  Rows whose workspace
+ * (sd_target_mean_workspace) exceeds it return SD_EINVAL: split them over
+ * calls.  Every call on one GPU uses the same memory: calls that overlap on
+ * one GPU (concurrent streams or threads) race and give undefined results.
+ * Arguments, layouts and errors otherwise as sd_target_mean. */
+sd_status sd_target_mean_noalloc(sd_target target, int32_t rows, const float* x,
+                                 int64_t x_row_stride, const int32_t* step, float* mq,
+                                 int64_t mq_row_stride, float* score, int64_t score_row_stride,
+                                 sd_stream stream);
+size_t sd_target_mean_noalloc_max_bytes(void);
+
 /* ----------------------------------------------------------------- draft --
  * Y_0 ~ N(0, I) for B chains (Alg. 8, first line): y [B][d], INIT stream,
  * round 0. */

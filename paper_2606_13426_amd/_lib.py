@@ -74,6 +74,8 @@ SIGNATURES = [
     ("sd_target_destroy", c_int32, [P]),
     ("sd_target_mean_workspace", c_size_t, [P, c_int32]),
     ("sd_target_mean", c_int32, [P, c_int32, P, c_int64, P, P, c_int64, P, c_int64, P, c_size_t, P]),
+    ("sd_target_mean_noalloc", c_int32, [P, c_int32, P, c_int64, P, P, c_int64, P, c_int64, P]),
+    ("sd_target_mean_noalloc_max_bytes", c_size_t, []),
     ("sd_init_chains", c_int32, [c_int32, c_int32, c_uint64, P, P]),
     ("sd_draft_block", c_int32, [ctypes.POINTER(sd_schedule), c_int32, c_int32, c_int32, P, P, P, P,
                                  c_uint64, P, S, P, S, P]),
@@ -203,6 +205,19 @@ def sd_target_mean(target, x, step, mq, score=None, ws=None):
     _check(load().sd_target_mean(target.handle, rows, _p(x), x.stride(0), _p(step), _p(mq), mq.stride(0),
                                  _p(score), score.stride(0) if score is not None else 0, _p(ws),
                                  ws.numel(), _stream()), "sd_target_mean")
+
+
+def sd_target_mean_noalloc(target, x, step, mq, score=None):
+    """sd_target_mean with the library's own scratch memory (no workspace)."""
+    rows = x.shape[0]
+    _check(load().sd_target_mean_noalloc(target.handle, rows, _p(x), x.stride(0), _p(step), _p(mq),
+                                         mq.stride(0), _p(score),
+                                         score.stride(0) if score is not None else 0, _stream()),
+           "sd_target_mean_noalloc")
+
+
+def sd_target_mean_noalloc_max_bytes():
+    return load().sd_target_mean_noalloc_max_bytes()
 
 
 def sd_init_chains(y, seed):

@@ -95,6 +95,40 @@ void prof_push(const char* name, hipEvent_t a, hipEvent_t b) {
 
 using namespace sd;
 
+// --------------------------------------------------- no-allocation scratch --
+// Device memory for sd_target_mean_noalloc: the target call's workspace (the
+// split logits partials, the softmax weights and per-row coefficients) for
+// callers that cannot allocate.  Every GPU the library runs on holds one copy
+// until the process ends.  Host code must not use the array's name as an
+// address: the device address of each GPU's copy comes from
+// hipGetSymbolAddress, taken once per device with that device current.
+constexpr size_t kScratchBytes = (size_t)128 << 20;
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+std::map<int, void*> g_scratch_addr;  // device -> address of its copy of scratch
+
+// The current device's copy of scratch (resolved on the first use on a device).
+hipError_t scratch_address(void** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  const auto it = g_scratch_addr.find(dev);
+  if (it != g_scratch_addr.end()) {
+    *out = it->second;
+    return hipSuccess;
+  }
+  void* ptr = nullptr;
+  e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+  if (e != hipSuccess) return e;
+  g_scratch_addr[dev] = ptr;
+  *out = ptr;
+  return hipSuccess;
+}
+}  // namespace
+
 #define SD_CHECK_ARG(cond, ...)     \
   do {                              \
     if (!(cond)) {                  \
@@ -215,6 +249,13 @@ sd_status sd_target_create(const sd_schedule* sched, int32_t d, int32_t n_comp, 
     return SD_ENOMEM;
   }
   t->flag_busy = 0;
+  // set-up of the no-allocation scratch on this device
+  void* scr = nullptr;
+  if (scratch_address(&scr) != hipSuccess) {
+    set_error("sd_target_create: the scratch array's device address is not available");
+    sd_target_destroy(reinterpret_cast<sd_target>(t));
+    return SD_EHIP;
+  }
   if (bf) {
     std::vector<uint16_t> h(M * D), hT(M * D);
     for (size_t m = 0; m < M; ++m)
@@ -311,6 +352,29 @@ sd_status sd_target_mean(sd_target target, int32_t rows, const float* x, int64_t
                             score_row_stride, ws, (hipStream_t)stream, nullptr));
   return SD_OK;
 }
+
+sd_status sd_target_mean_noalloc(sd_target target, int32_t rows, const float* x,
+                                 int64_t x_row_stride, const int32_t* step, float* mq,
+                                 int64_t mq_row_stride, float* score, int64_t score_row_stride,
+                                 sd_stream stream) {
+  SD_CHECK_ARG(target, "sd_target_mean_noalloc: target is NULL");
+  const Target& t = *reinterpret_cast<Target*>(target);
+  SD_CHECK_ARG(rows >= 1, "sd_target_mean_noalloc: rows = %d < 1", rows);
+  SD_CHECK_ARG(x && step && mq, "sd_target_mean_noalloc: x, step and mq must be non-NULL");
+  SD_CHECK_ARG(x_row_stride >= t.d && mq_row_stride >= t.d, "sd_target_mean_noalloc: row strides must be >= d = %d", t.d);
+  SD_CHECK_ARG(!score || score_row_stride >= t.d, "sd_target_mean_noalloc: score row stride must be >= d");
+  const size_t need = target_ws_bytes(t, rows);
+  SD_CHECK_ARG(need <= kScratchBytes,
+               "sd_target_mean_noalloc: %d rows need %zu bytes of scratch, more than the %zu it holds "
+               "(split the rows over calls)", rows, need, kScratchBytes);
+  void* ws = nullptr;
+  SD_HIP(scratch_address(&ws));
+  SD_HIP(target_mean_launch(t, rows, x, x_row_stride, step, mq, mq_row_stride, score,
+                            score_row_stride, ws, (hipStream_t)stream, nullptr));
+  return SD_OK;
+}
+
+size_t sd_target_mean_noalloc_max_bytes(void) { return kScratchBytes; }
 
 // ----------------------------------------------------------------- draft --
 sd_status sd_init_chains(int32_t B, int32_t d, uint64_t seed, float* y, sd_stream stream) {

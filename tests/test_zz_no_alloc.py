@@ -1,0 +1,77 @@
+"""sd_target_mean_noalloc (the target call on the library's own scratch memory)
+against sd_target_mean with a caller workspace: the same kernels, so the
+outputs must be identical, on two calls in a row (the second smaller) for both
+GEMM precisions; rows beyond the scratch return SD_EINVAL before any launch."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2606_13426_amd import _lib
+from paper_2606_13426_amd.inputs import make_gmm, workload_gmm
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _rows(rows, d, N, seed):
+    g = torch.Generator(device=DEV)
+    g.manual_seed(seed)
+    x = torch.randn(rows, d, generator=g, device=DEV)
+    step = torch.randint(0, N, (rows,), generator=g, device=DEV).to(torch.int32)
+    return x, step
+
+
+def _both(tgt, x, step):
+    mq_ws = torch.empty_like(x)
+    sc_ws = torch.empty_like(x)
+    _lib.sd_target_mean(tgt, x, step, mq_ws, sc_ws)
+    mq_na = torch.full_like(x, float("nan"))
+    sc_na = torch.full_like(x, float("nan"))
+    _lib.sd_target_mean_noalloc(tgt, x, step, mq_na, sc_na)
+    torch.cuda.synchronize()
+    return mq_ws, sc_ws, mq_na, sc_na
+
+
+@pytest.mark.parametrize("name,precision,rows", [("pixel3072", _lib.SD_FP32, (9216, 1000)),
+                                                 ("latent16384", _lib.SD_BF16, (2304, 300))])
+def test_noalloc_target_mean_equals_workspace_call(name, precision, rows):
+    p = workload_gmm(name)
+    N = 200
+    tgt = _lib.Target(_lib.schedule(N), p["mu"], p["var"], p["log_w"], precision=precision)
+    for i, r in enumerate(rows):
+        assert _lib.sd_target_mean_workspace(tgt, r) <= _lib.sd_target_mean_noalloc_max_bytes()
+        x, step = _rows(r, tgt.d, N, seed=10 + i)
+        mq_ws, sc_ws, mq_na, sc_na = _both(tgt, x, step)
+        assert torch.equal(mq_na, mq_ws), (name, r)
+        assert torch.equal(sc_na, sc_ws), (name, r)
+
+
+def test_noalloc_strided_rows_and_small_target():
+    # row strides above d and a target whose d is not a whole number of chunks
+    d, M, rows, N = 130, 24, 90, 80
+    p = make_gmm(d, M, mu_std=1.0, var=(0.01, 0.2), dirichlet=1.0, seed=3)
+    tgt = _lib.Target(_lib.schedule(N), p["mu"], p["var"], p["log_w"])
+    xw = torch.randn(rows, d + 3, device=DEV)
+    step = torch.randint(0, N, (rows,), device=DEV).to(torch.int32)
+    mq_ws = torch.empty(rows, d, device=DEV)
+    _lib.sd_target_mean(tgt, xw[:, :d], step, mq_ws)
+    mqw = torch.full((rows, d + 5), 7.0, device=DEV)
+    _lib.sd_target_mean_noalloc(tgt, xw[:, :d], step, mqw[:, :d])
+    torch.cuda.synchronize()
+    assert torch.all(mqw[:, d:] == 7.0)
+    assert torch.equal(mqw[:, :d], mq_ws)
+
+
+def test_noalloc_rejects_rows_beyond_the_scratch():
+    p = workload_gmm("latent16384")
+    tgt = _lib.Target(_lib.schedule(100), p["mu"], p["var"], p["log_w"], precision=_lib.SD_BF16)
+    rows = 4 * 2304
+    assert _lib.sd_target_mean_workspace(tgt, rows) > _lib.sd_target_mean_noalloc_max_bytes()
+    x = torch.zeros(rows, tgt.d, device=DEV)
+    step = torch.zeros(rows, dtype=torch.int32, device=DEV)
+    mq = torch.full_like(x, 3.0)
+    with pytest.raises(_lib.SpecDiffError) as e:
+        _lib.sd_target_mean_noalloc(tgt, x, step, mq)
+    assert e.value.status == _lib.SD_EINVAL and "scratch" in str(e.value)
+    torch.cuda.synchronize()
+    assert torch.all(mq == 3.0)
