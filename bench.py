@@ -3,16 +3,18 @@
 Step = one full run of the sampler (all hot-path steps: Free-Drafter drafts,
 the Gaussian-mixture target on every draft state, log-ratio reductions, the
 block-verification scan with U-sampling, the residual draw and the commit)
-over one batch of B chains from Y_0 to Y_N, on the pixel-sized workload
-(d = 3*32*32, M = 64 components, B = 1024 chains, K = 8 drafts, N = 200 steps,
-float32).  value = verified chain-steps per second = B * N / seconds per run.
+over one batch of B chains from Y_0 to Y_N, on the latent-sized workload
+(d = 4*64*64, M = 1024 components, B = 256 chains, K = 8 drafts, N = 1000
+steps, bf16 GEMM operands with float32 accumulation).  value = verified
+chain-steps per second = B * N / seconds per run.
 
-Per-kernel durations are measured live with HIP events recorded around every
-launch on the launch's stream; the dominant kernel's roofline uses its
-algorithmic work (see the ALGO table below) over its measured time.  The
-verification-only workload (B = 4096, K = 32, d = 12288) and token
-verification are reported as extra fields; the CPU oracle is timed on a
-bounded sample of chains of the same workload.
+Per-kernel durations are measured live with HIP events on the launch's
+stream; the dominant kernel's roofline uses its algorithmic work (see
+algorithmic_work) over its measured time.  The pixel-sized float32 workload
+(with token verification), the 64x64x3 pixel workload, the
+verification-only workload (B = 4096, K = 32, d = 12288) and the paper's
+variants are extra fields; the CPU oracle is timed on a bounded sample of
+rounds of the headline workload.
 """
 import argparse
 import json
@@ -195,6 +197,7 @@ def run_sampler_bench(lib, name, mode, steps, warmup, profile):
     be = st["steps"] / st["chain_rounds"]
     act, rows_v, rows_t = _counts_from_trace(trace0, N, K)
     return dict(B=B, K=K, N=N, d=d, M=M, sec=sec, be=be, rounds=st["rounds"], prof=prof, seen=seen,
+                mean_tau=st["mean_tau"], ties=st["ties"],
                 breakdown=breakdown,
                 act=act, rows_verified=rows_v, rows_target=rows_t, tau_hist=st["tau_hist"][: K + 2],
                 steps=steps)
@@ -431,7 +434,12 @@ def verify_bench(lib, steps, warmup):
 
 
 def cpu_baseline(name, budget_s):
-    """The oracle (single-threaded NumPy float64) on a bounded sample of chains."""
+    """The oracle (NumPy float64) on a bounded sample of the workload: whole
+    chains one after another, round by round (Alg. 8), until the budget is
+    spent; value = steps advanced / seconds.  Its matrix products run on the
+    BLAS thread pool (cores = that pool's threads), the rest on one thread."""
+    from threadpoolctl import threadpool_info
+
     from oracle import sampler as osamp
     from oracle.gmm import GMM
     from oracle.schedule import Schedule
@@ -440,22 +448,41 @@ def cpu_baseline(name, budget_s):
     p = workload_gmm(name)
     g = GMM(p["mu"], p["var"], p["log_w"])
     sch = Schedule(cfg["N"])
+    N, K = cfg["N"], cfg["K"]
     t0 = time.perf_counter()
-    chains = 0
-    while chains < cfg["B"]:
-        osamp.run_sampler(g, sch, cfg["B"], cfg["K"], 0, chains=[chains])
+    chains = rounds = steps = 0
+    done = False
+    while chains < cfg["B"] and not done:
+        y, sc = osamp.init_state(g, sch, 0, chains)
+        k = r = 0
+        while k < N:
+            y, sc, k, info = osamp.run_round(g, sch, K, y, sc, k, r, 0, chains)
+            r += 1
+            rounds += 1
+            steps += info["steps"]
+            if time.perf_counter() - t0 > budget_s:
+                done = True
+                break
         chains += 1
-        if time.perf_counter() - t0 > budget_s:
-            break
     el = time.perf_counter() - t0
-    return dict(value=chains * cfg["N"] / el, unit="chain-steps/s", cores=1, kind="oracle",
-                sample=f"{chains} of {cfg['B']} chains of {name}, full {cfg['N']}-step runs, "
-                       f"{el:.1f} s, single-threaded NumPy float64")
+    blas = [i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"]
+    cores = max(blas) if blas else 1
+    return dict(value=steps / el, unit="chain-steps/s", cores=cores, kind="oracle",
+                sample=f"{name}: chains 0..{chains - 1} of {cfg['B']} from Y_0, {rounds} rounds, "
+                       f"{steps} chain-steps in {el:.1f} s (NumPy float64, {cores} BLAS threads)")
 
 
 def _dtype(name):
     from paper_2606_13426_amd.inputs import WORKLOADS
-    return "bf16 GEMM operands, f32 accumulate and states" if WORKLOADS[name].get("precision") == "bf16" else "f32"
+    return "bf16" if WORKLOADS[name].get("precision") == "bf16" else "f32"
+
+
+def _precision(name):
+    from paper_2606_13426_amd.inputs import WORKLOADS
+    if WORKLOADS[name].get("precision") == "bf16":
+        return ("bf16 operands of the two denoiser GEMMs with f32 accumulation; f32 states and "
+                "epilogue, f64 softmax, log-ratio sums and scans")
+    return "f32 (GEMMs as exact split-bf16 products, f32 accumulation); f64 softmax, log-ratio sums and scans"
 
 
 # the denoiser GEMM shapes of the workloads (m x k @ k x n) and two square
@@ -530,10 +557,12 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="pixel3072")
+    ap.add_argument("--workload", default="latent16384")
+    ap.add_argument("--variants-workload", default="pixel3072",
+                    help="workload of the variants field (the paper's R/D/B table, Frozen Drafter, plain EM)")
     ap.add_argument("--no-extra", action="store_true", help="skip the token and verification-only runs")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-budget", type=float, default=15.0)
+    ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--calibrate-mfma", action="store_true",
                     help="only time the library's register-only bf16 matrix-instruction loop (the sustained "
                          "matrix-core rate beside the published peak) and exit")
@@ -566,7 +595,8 @@ def main():
         lib.load()
         # torch initialises the device before the library's first HIP call
         assert torch.cuda.is_available(), "bench.py needs a GPU"
-        print(json.dumps(dict(workload=args.workload, variants=variants_bench(lib, args.workload, args.steps))))
+        print(json.dumps(dict(workload=args.variants_workload,
+                              variants=variants_bench(lib, args.variants_workload, args.steps))))
         return
     if args.calibrate_mfma:
         import torch
@@ -619,31 +649,39 @@ def main():
                 config=dict(workload=args.workload, d=res["d"], M=res["M"], B=res["B"], K=res["K"],
                             N=res["N"], verification="block", drafter="free", usample="exact",
                             parallelism="single-gpu"),
-                mean_accepted_steps_per_block=res["be"], rounds_per_run=res["rounds"],
-                roofline=roof, kernels=table)
+                precision=_precision(args.workload),
+                mean_accepted_steps_per_block=res["be"], mean_tau=res["mean_tau"], ties=res["ties"],
+                rounds_per_run=res["rounds"], roofline=roof, kernels=table)
     if not args.no_extra:
-        tok = run_sampler_bench(lib, args.workload, lib.SD_TOKEN, max(2, args.steps // 2), 1, profile=False)
-        line["token"] = dict(value=tok["B"] * tok["N"] / tok["sec"], ms_per_step=1e3 * tok["sec"],
-                             mean_accepted_steps_per_block=tok["be"], rounds_per_run=tok["rounds"])
-        line["verify_only"] = verify_bench(lib, args.steps, args.warmup)
-        # the bf16-denoiser workloads, each run end to end (not the headline value)
+        # the other sampler workloads, each run end to end (not the headline
+        # value); the pixel-sized one with block and token verification
         others = {}
-        for wl in ("latent16384", "pixel12288"):
+        for wl in ("pixel3072", "pixel12288", "latent16384"):
             if wl == args.workload:
                 continue
-            r2 = run_sampler_bench(lib, wl, lib.SD_BLOCK, 3, 1, profile=True)
-            roof2, table2 = roofline_of(r2, 3)
+            r2 = run_sampler_bench(lib, wl, lib.SD_BLOCK, max(3, args.steps // 2), 1, profile=True)
+            roof2, table2 = roofline_of(r2, max(3, args.steps // 2))
+            if roof2:
+                roof2["traffic"] = measured_traffic(wl, roof2["kernel"])
             others[wl] = dict(value=r2["B"] * r2["N"] / r2["sec"], unit="chain-steps/s",
                               ms_per_step=1e3 * r2["sec"], dtype=_dtype(wl),
                               mean_accepted_steps_per_block=r2["be"], rounds_per_run=r2["rounds"],
+                              ties=r2["ties"],
                               config=dict(d=r2["d"], M=r2["M"], B=r2["B"], K=r2["K"], N=r2["N"]),
                               roofline=roof2, denoiser_gemms=table2.get("denoiser_gemms"),
                               kernels={k: dict(avg_us=v["avg_us"], bound=v.get("bound"), frac=v.get("frac"))
                                        for k, v in table2.items() if "avg_us" in v})
+            if wl == "pixel3072":
+                tok = run_sampler_bench(lib, wl, lib.SD_TOKEN, max(2, args.steps // 2), 1, profile=False)
+                others[wl]["token"] = dict(value=tok["B"] * tok["N"] / tok["sec"], ms_per_step=1e3 * tok["sec"],
+                                           mean_accepted_steps_per_block=tok["be"],
+                                           rounds_per_run=tok["rounds"])
         line["other_workloads"] = others
-        line["library_gemms"] = library_gemms()
+        line["verify_only"] = verify_bench(lib, args.steps, args.warmup)
         line["mfma_calibration"] = mfma_calibration(lib)
-        line["variants"] = variants_bench(lib, args.workload, args.steps)
+        line["library_gemms"] = library_gemms()
+        line["variants"] = dict(workload=args.variants_workload,
+                                **variants_bench(lib, args.variants_workload, args.steps))
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(args.workload, args.cpu_budget)
     print(json.dumps(line))
