@@ -509,7 +509,7 @@ SamplerLayout sampler_layout(const Target& t, int B, int K) {
     off = a256(off + bytes);
     return o;
   };
-  L.nct = lr_tiles(t);
+  L.nct = lr_tiles(t, (int)K1);
   L.y = take(4 * Bs * d);
   L.x = take(4 * Bs * K1 * d);
   L.sv = take(4 * Bs * d);

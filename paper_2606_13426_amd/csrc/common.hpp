@@ -124,14 +124,14 @@ hipError_t target_mean_launch(const Target& t, int rows, const float* x, int64_t
 
 // The sampler's target call on its [B][K+1][d] block (x rows contiguous,
 // row stride d) that also leaves the verification's partial sums in
-// lrp[row][lr_tiles(t)][3] (see gmm_mean_lr_kernel); the draft means are
+// lrp[row][lr_tiles(t, K1)][3] (see gmm_mean_lr_kernel); the draft means are
 // recomputed from x, the cache rows sv [B][d] and the cache steps cstep [B];
 // rnd = chains' rounds.
 hipError_t target_mean_lr_launch(const Target& t, int rows, int K1, const float* x,
                                  const int32_t* step, float* mq, const float* sv,
                                  const int32_t* cstep, double* lrp, const uint32_t* rnd,
                                  uint64_t seed, void* ws, hipStream_t s, const int* gate);
-int lr_tiles(const Target& t);
+int lr_tiles(const Target& t, int K1);
 // bf16 versions of the three calls above (dispatched to by them).
 hipError_t target_mean_bf16_launch(const Target& t, int rows, const float* x, int64_t ldx,
                                    const int32_t* step, float* mq, int64_t ldq, float* score,
@@ -140,7 +140,7 @@ hipError_t target_mean_lr_bf16_launch(const Target& t, int rows, int K1, const f
                                       const int32_t* step, float* mq, const float* sv,
                                       const int32_t* cstep, double* lrp, const uint32_t* rnd,
                                       uint64_t seed, void* ws, hipStream_t s, const int* gate);
-int lr_tiles_bf16(const Target& t);
+int lr_tiles_bf16(const Target& t, int K1);
 // Softmax over the split logits partials part[S][rows][M] (+ xsq[S][rows]):
 // P[rows][M] = r a / s2 (float32, or bf16 when p_bf16) and rowc[rows][3] =
 // (c1, c2, rho) of each row's step.

@@ -1055,8 +1055,8 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
                       t.muT_split, x, rowc, sv, cstep, t.coef, mq, lrp, rnd, seed, gate);
 }
 
-int lr_tiles(const Target& t) {
-  return t.prec == SD_BF16 ? lr_tiles_bf16(t) : (t.d + TILE - 1) / TILE;
+int lr_tiles(const Target& t, int K1) {
+  return t.prec == SD_BF16 ? lr_tiles_bf16(t, K1) : (t.d + TILE - 1) / TILE;
 }
 
 }  // namespace sd

@@ -10,13 +10,16 @@
 //   softmax:         the float32 path's kernels, writing P in bf16;
 //   gmm_mean_bf16 / gmm_mean_lr_bf16: O = P mu (mu^T stored as bf16) and the
 //                    epilogue in float32, the latter with the verification
-//                    partial sums of the sampler (as the float32 path).
+//                    partial sums of the sampler (as the float32 path); the
+//                    sampler's call with at least 512 components runs on the
+//                    chain-aligned 288 x 256 tiles of gemm_bf16_big.hpp.
 // The mean GEMMs' 128 x 128 accumulator tile is handed to the epilogue
 // through LDS in two passes of 64 columns, each over the operand buffers'
 // storage.
 #include "bufio.hpp"
 #include "common.hpp"
 #include "gemm_bf16.hpp"
+#include "gemm_bf16_big.hpp"
 #include "gemm_bf16_wide.hpp"
 #include "philox.hpp"
 #include "rows.hpp"
@@ -474,6 +477,233 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
   }
 }
 
+// The sampler's mean GEMM on the 288-row tiles of gemm_bf16_big.hpp whose
+// rows are whole chains: tile rt holds the CT chains rt CT .. (CT K1 <= 288
+// rows), so no chain straddles two tiles.  Same outputs as
+// gmm_mean_lr_bf16_kernel (m^q, and the float64 partials of ||m^p - m^q||^2,
+// (yhat_{j+1} - m^p).(m^p - m^q) and G.(m^p - m^q) per draft row and column
+// tile).  The epilogue works on the accumulators where they are: each lane
+// holds four consecutive columns of one row per block, so x and m^q move as
+// 16-byte row segments, the next draft comes from the neighbouring lane, G
+// and the chains' cache rows are staged once in LDS, and the per-row sums are
+// combined over the four lanes of a row and the column wavefronts in a fixed
+// order.  Needs d % TC == 0, M % KC == 0, aligned rows and CT <= kChains.
+template <class T>
+struct BigMean {
+  static constexpr int QW = T::TC / 64;  // column wavefronts
+  // chains whose G and cache rows fit the operand buffers beside the partials
+  static constexpr int kFit = (int)((2 * sizeof(typename T::Lds) - QW * bf16b::TR * 3 * sizeof(double)) /
+                                    (2 * sizeof(float) * T::TC));
+  static constexpr int kChains = kFit < 56 ? kFit : 56;
+};
+
+// Within a 16-lane row of the accumulator layout lane l holds tile row
+// 16 rb + l % 16: the row below is lane l + 1 (DPP row_shl:1), and for lane 15
+// it is lane 0 of the next block (DPP row_shr:15 of that block's values).
+__device__ __forceinline__ float next_row1(float cur, float nxt) {
+  const int fix = __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, nxt), 0x11f, 0xf, 0xf, false);
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(fix, __builtin_bit_cast(int, cur), 0x101,
+                                                               0xf, 0xf, false));
+}
+__device__ __forceinline__ float4 next_row(float4 cur, float4 nxt) {
+  return make_float4(next_row1(cur.x, nxt.x), next_row1(cur.y, nxt.y), next_row1(cur.z, nxt.z),
+                     next_row1(cur.w, nxt.w));
+}
+
+// Lane l receives lane l ^ 8's value (DPP row_ror:8 inside each 16-lane row).
+__device__ __forceinline__ float xchg8_1(float v) {
+  return __builtin_bit_cast(float, __builtin_amdgcn_update_dpp(0, __builtin_bit_cast(int, v), 0x128, 0xf,
+                                                               0xf, false));
+}
+__device__ __forceinline__ float4 xchg8(float4 v) {
+  return make_float4(xchg8_1(v.x), xchg8_1(v.y), xchg8_1(v.z), xchg8_1(v.w));
+}
+
+__device__ __forceinline__ int big_tile_order(int nrt, int nct, int& rt) {
+  // each XCD takes a contiguous range of column tiles (its slice of mu^T stays
+  // in its L2) and walks the row tiles fastest inside it
+  const int lin = xcd_tile(nrt * nct);
+  rt = lin % nrt;
+  return lin / nrt;
+}
+
+template <class T>
+__global__ __launch_bounds__(T::kThreads, T::TC == 128 ? 2 : 1) void gmm_mean_lr_bf16_big_kernel(
+    int R, int M, int d, int K1, int CT, const uint16_t* __restrict__ P,
+    const uint16_t* __restrict__ muT, const float* __restrict__ X, const float* __restrict__ rowc,
+    const float* __restrict__ SV, const int32_t* __restrict__ cstep,
+    const float4* __restrict__ coef, float* __restrict__ mq, double* __restrict__ lrp,
+    const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
+  using bf16b::CB;
+  using bf16b::RB;
+  using bf16b::TR;
+  constexpr int TC = T::TC, QW = BigMean<T>::QW, NCH = BigMean<T>::kChains;
+  if (gate && *gate == 0) return;
+  __shared__ typename T::Lds sm[2];
+  __shared__ float rc[3 * TR];
+  __shared__ float cscale[NCH];
+  __shared__ uint32_t crnd[NCH];
+  const int B = R / K1;
+  const int nrt = (B + CT - 1) / CT, nct = d / TC;
+  int rt;
+  const int ct = big_tile_order(nrt, nct, rt);
+  const int b_first = rt * CT;
+  const int nchain = min(CT, B - b_first);
+  const int r0 = b_first * K1, rows = nchain * K1, c0 = ct * TC;
+  for (int e = threadIdx.x; e < 3 * TR; e += T::kThreads)
+    rc[e] = e < 3 * rows ? rowc[3 * (int64_t)r0 + e] : 0.f;
+  if ((int)threadIdx.x < nchain) {
+    crnd[threadIdx.x] = rnd[b_first + threadIdx.x];
+    cscale[threadIdx.x] = coef[cstep[b_first + threadIdx.x]].w;  // 1 / c2 at the cache step
+  }
+  bf16b::f32x4 acc[RB][CB];
+  bf16b::zero(acc);
+  T::run(sm, buf_view(muT + (int64_t)c0 * M, (int64_t)TC * M * 2), M,
+         buf_view(P + (int64_t)r0 * M, (int64_t)rows * M * 2), M, 0, M, acc);
+  const __amdgpu_buffer_rsrc_t vx = buf_view(X + (int64_t)r0 * d, (int64_t)min(R - r0, rows + 1) * d * 4);
+  const __amdgpu_buffer_rsrc_t vq = buf_view(mq + (int64_t)r0 * d, (int64_t)rows * d * 4);
+  const __amdgpu_buffer_rsrc_t vs = buf_view(SV + (int64_t)b_first * d, (int64_t)nchain * d * 4);
+  // HBM accesses of the epilogue cover whole 128-byte lines: lane l moves 16
+  // bytes of row 8 h + l % 8 of a row block at column 16 ((l / 8) % 2) + 4
+  // (l / 16) of a pair of column blocks, 8 rows x 128 bytes per instruction.
+  // Lanes l and l ^ 8 then swap one value per pair (xchg8) to reach the
+  // accumulator layout (row l % 16, four columns of each block), and back for
+  // the stores of m^q.
+  const int lane = threadIdx.x & 63, b3 = (lane >> 3) & 1;
+  const int row7 = T::out_row(0) - (lane & 15) + (lane & 7);
+  const int colp = c0 + T::out_col(0) - 4 * ((lane >> 4) & 3) + 16 * b3 + 4 * ((lane >> 4) & 3);
+  auto load_x = [&](int rb, float4 (&raw)[CB]) {
+#pragma unroll
+    for (int pr = 0; pr < CB / 2; ++pr) {
+      raw[2 * pr] = buf_ld4(vx, (uint32_t)(((row7 + 16 * rb) * d + colp + 32 * pr) * 4));
+      raw[2 * pr + 1] = buf_ld4(vx, (uint32_t)(((row7 + 16 * rb + 8) * d + colp + 32 * pr) * 4));
+    }
+  };
+  auto to_acc_layout = [&](const float4 (&raw)[CB], float4 (&xv)[CB]) {
+#pragma unroll
+    for (int pr = 0; pr < CB / 2; ++pr) {
+      const float4 lo = raw[2 * pr], hi = raw[2 * pr + 1];
+      const float4 recv = xchg8(b3 ? lo : hi);
+      xv[2 * pr] = b3 ? recv : lo;
+      xv[2 * pr + 1] = b3 ? hi : recv;
+    }
+  };
+  // x is prefetched two row blocks ahead (the first ones before G is drawn)
+  float4 xraw[RB][CB], xr[RB][CB];
+  load_x(0, xraw[0]);
+  load_x(1, xraw[1]);
+  // G of the tile's chains and columns (four normals per Philox block) and the
+  // chains' cache rows, into the (now free) operand buffers: gz, svs
+  // [chain][column]; then the per-row partial sums of each column wavefront
+  float* gz = reinterpret_cast<float*>(&sm[0]);
+  float* svs = gz + NCH * TC;
+  double* part = reinterpret_cast<double*>(svs + NCH * TC);
+  for (int e = threadIdx.x; e < nchain * (TC / 4); e += T::kThreads) {
+    const int cl = e / (TC / 4), g4 = e % (TC / 4);
+    const float4 z = normals4(philox((uint32_t)((c0 >> 2) + g4), (uint32_t)(b_first + cl), crnd[cl],
+                                     TAG_RESID << 24, seed));
+    *reinterpret_cast<float4*>(&gz[cl * TC + 4 * g4]) = z;
+    *reinterpret_cast<float4*>(&svs[cl * TC + 4 * g4]) = buf_ld4(vs, (uint32_t)((cl * d + c0 + 4 * g4) * 4));
+  }
+  __syncthreads();
+  const int wc = T::col_wave(), sub = (threadIdx.x >> 4) & 3;
+  to_acc_layout(xraw[0], xr[0]);
+#pragma unroll
+  for (int rb = 0; rb < RB; ++rb) {
+    if (rb + 2 < RB) load_x(rb + 2, xraw[rb + 2]);
+    if (rb + 1 < RB) to_acc_layout(xraw[rb + 1], xr[rb + 1]);
+    const float4 (&xa)[CB] = xr[rb];
+    const int lr = T::out_row(rb);  // tile row
+    // rows past the tile's chains read zeros and store nothing (buffer views)
+    const int b = min(lr / K1, NCH - 1), j = lr - (lr / K1) * K1;
+    const bool keep = lr < rows && j < K1 - 1;
+    const float c1 = rc[3 * min(lr, TR - 1)], c2 = rc[3 * min(lr, TR - 1) + 1],
+                rho = rc[3 * min(lr, TR - 1) + 2];
+    const float c2s = c2 * cscale[b];
+    double a2 = 0.0, az = 0.0, ag = 0.0;
+#pragma unroll
+    for (int pr = 0; pr < CB / 2; ++pr) {
+      float4 qs[2];
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const int cb = 2 * pr + h;
+        const int tcol = T::out_col(cb);
+        // the next draft of each row is the next row's x: lane l + 1 of the
+        // same 16-lane row (DPP row shift), and for lane 15 row 0 of the next
+        // block (lane 0 of its 16-lane row); past the wavefront's last block a
+        // load
+        const float4 y = rb + 1 < RB ? next_row(xa[cb], xr[rb + 1 < RB ? rb + 1 : rb][cb])
+                                     : buf_ld4(vx, (uint32_t)(((lr + 1) * d + c0 + tcol) * 4));
+        const bf16b::f32x4 o = acc[rb][cb];
+        const float4 x = xa[cb];
+        const float4 sv = *reinterpret_cast<const float4*>(&svs[b * TC + tcol]);
+        const float4 qv = make_float4(c1 * x.x + c2 * (o[0] - rho * x.x), c1 * x.y + c2 * (o[1] - rho * x.y),
+                                      c1 * x.z + c2 * (o[2] - rho * x.z), c1 * x.w + c2 * (o[3] - rho * x.w));
+        qs[h] = qv;
+        const float4 gv = *reinterpret_cast<const float4*>(&gz[b * TC + tcol]);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float pe = draft_mean(c1, comp(x, e), c2s, comp(sv, e));  // m^p
+          const double dd = (double)pe - (double)comp(qv, e);
+          const double zz = (double)comp(y, e) - (double)pe;
+          a2 = fma(dd, dd, a2);
+          az = fma(zz, dd, az);
+          ag = fma((double)comp(gv, e), dd, ag);
+        }
+      }
+      // m^q of the pair back to whole-line rows (the inverse swap), with
+      // non-temporal stores: the round reads back two of a chain's K + 1 rows
+      const float4 recv = xchg8(b3 ? qs[0] : qs[1]);
+      buf_st4_stream(vq, (uint32_t)(((row7 + 16 * rb) * d + colp + 32 * pr) * 4), b3 ? recv : qs[0]);
+      buf_st4_stream(vq, (uint32_t)(((row7 + 16 * rb + 8) * d + colp + 32 * pr) * 4), b3 ? qs[1] : recv);
+    }
+    // the four lanes of the row (sub = 0..3), in a fixed order
+    a2 += __shfl_xor(a2, 16);
+    az += __shfl_xor(az, 16);
+    ag += __shfl_xor(ag, 16);
+    a2 += __shfl_xor(a2, 32);
+    az += __shfl_xor(az, 32);
+    ag += __shfl_xor(ag, 32);
+    if (sub == 0) {
+      double* o = part + ((int64_t)wc * TR + lr) * 3;
+      o[0] = keep ? a2 : 0.0;
+      o[1] = keep ? az : 0.0;
+      o[2] = keep ? ag : 0.0;
+    }
+  }
+  __syncthreads();
+  // the column wavefronts of each row, in a fixed order
+  for (int lr = threadIdx.x; lr < rows; lr += T::kThreads) {
+    double t[3];
+#pragma unroll
+    for (int q = 0; q < 3; ++q) {
+      double v = part[lr * 3 + q];
+#pragma unroll
+      for (int w = 1; w < QW; ++w) v += part[(w * TR + lr) * 3 + q];
+      t[q] = v;
+    }
+    double* o = lrp + ((int64_t)(r0 + lr) * nct + ct) * 3;
+    o[0] = t[0];
+    o[1] = t[1];
+    o[2] = t[2];
+  }
+}
+
+// The tile of the sampler's bf16 mean GEMM: 288 x 256, one workgroup per
+// compute unit.
+using MeanTile = bf16b::Tile<256, 64>;
+
+// Chains per tile of the chain-aligned mean GEMM, and whether it applies.
+inline int big_chains(int K1) { return min(bf16b::TR / K1, BigMean<MeanTile>::kChains); }
+// (for fewer than 512 components a tile's contraction is too short to pay for
+// the one-workgroup-per-compute-unit epilogue: the 128 x 128 kernel, two per
+// compute unit, is faster there)
+inline bool big_mean_ok(const Target& t, int K1, bool vecd) {
+  return vecd && t.d % MeanTile::TC == 0 && t.M % MeanTile::KC == 0 && t.M >= 512 && K1 <= bf16b::TR &&
+         (int64_t)(bf16b::TR + 1) * t.d * 4 < ((int64_t)1 << 31) &&
+         (int64_t)bf16b::TR * t.M * 2 < ((int64_t)1 << 31);
+}
+
 struct Plan {
   int S, ksplit;
   bool wide;  // the logits GEMM may run on 256 x 256 tiles (d a whole number of chunks)
@@ -591,6 +821,18 @@ hipError_t target_mean_lr_bf16_launch(const Target& t, int R, int K1, const floa
   const bool vecd = (t.d % 4 == 0) && aligned16(x) && aligned16(mq) && aligned16(sv);
   hipError_t e = logits_and_softmax(t, p, w, R, x, t.d, vecd, step, s, gate);
   if (e != hipSuccess) return e;
+  // chain-aligned 288 x 256 tiles: whole column tiles of d, whole chunks of
+  // M, aligned rows, 32-bit offsets inside a tile's views
+  // the tile count of the partials (lr_tiles_bf16) assumes this kernel
+  // whenever the shapes allow it: the sampler's workspace rows are aligned
+  if (big_mean_ok(t, K1, t.d % 4 == 0)) {
+    if (!vecd) return hipErrorInvalidValue;
+    const int CT = big_chains(K1), B = R / K1;
+    return launch_timed("gmm_mean_lr_bf16", gmm_mean_lr_bf16_big_kernel<MeanTile>,
+                        dim3(((B + CT - 1) / CT) * (t.d / MeanTile::TC)), dim3(MeanTile::kThreads), s, R,
+                        t.M, t.d, K1, CT, w.P, t.muT16, x, w.rowc, sv, cstep, t.coef, mq, lrp, rnd,
+                        seed, gate);
+  }
   dim3 g2((t.d + TN - 1) / TN, (R + TM - 1) / TM);
   // the buffer path: whole chunks of M, whole tiles of d, aligned rows, at
   // least eight rows per chain, 32-bit offsets inside a tile's views
@@ -602,6 +844,8 @@ hipError_t target_mean_lr_bf16_launch(const Target& t, int R, int K1, const floa
                       mq, lrp, vecd, rnd, seed, gate);
 }
 
-int lr_tiles_bf16(const Target& t) { return (t.d + TN - 1) / TN; }
+int lr_tiles_bf16(const Target& t, int K1) {
+  return big_mean_ok(t, K1, t.d % 4 == 0) ? t.d / MeanTile::TC : (t.d + TN - 1) / TN;
+}
 
 }  // namespace sd

@@ -63,10 +63,14 @@ def test_noalloc_strided_rows_and_small_target():
 
 
 def test_noalloc_rejects_rows_beyond_the_scratch():
-    p = workload_gmm("latent16384")
+    # a small d and many components: the first row count (doubling) whose
+    # workspace exceeds the scratch
+    p = make_gmm(64, 1024, mu_std=1.0, var=(0.01, 0.1), dirichlet=0.5, seed=5)
     tgt = _lib.Target(_lib.schedule(100), p["mu"], p["var"], p["log_w"], precision=_lib.SD_BF16)
-    rows = 4 * 2304
-    assert _lib.sd_target_mean_workspace(tgt, rows) > _lib.sd_target_mean_noalloc_max_bytes()
+    rows = 1024
+    while _lib.sd_target_mean_workspace(tgt, rows) <= _lib.sd_target_mean_noalloc_max_bytes():
+        rows *= 2
+    assert rows <= 1 << 20
     x = torch.zeros(rows, tgt.d, device=DEV)
     step = torch.zeros(rows, dtype=torch.int32, device=DEV)
     mq = torch.full_like(x, 3.0)
