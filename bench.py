@@ -45,6 +45,8 @@ MEASURED_TRAFFIC = {
                                              sources="ea7ba0139a0bc5b69f3731957c94da1a81dfb8b2"),
     ("pixel3072", "gmm_mean_lr"): dict(bytes=(136.1 + 122.0) * 1e6, unit="gmm.hip",
                                        sources="f3e06c62cf09a8fbf8101f1fe1e515fc20c93769"),
+    ("latent16384", "gmm_mean_lr_bf16"): dict(bytes=(277.7 + 154.0) * 1e6, unit="gmm_bf16.hip",
+                                              sources="2d6a90c33c9ca8b85d501d6e9f496200d045a0c5"),
 }
 
 

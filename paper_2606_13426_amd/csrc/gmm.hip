@@ -393,14 +393,14 @@ __device__ __forceinline__ double group_reduce(double v, bool is_max, double* re
     v = is_max ? fmax(v, u) : v + u;
   }
   if constexpr (G > 64) {
-    constexpr int NW = G / 64;  // wavefronts per row (one row per workgroup)
-    const int w = threadIdx.x >> 6;
+    constexpr int NW = G / 64;  // wavefronts per row: the row's are w0 .. w0 + NW - 1
+    const int w = threadIdx.x >> 6, w0 = w - w % NW;
     __syncthreads();  // the previous use of red is complete
     if ((threadIdx.x & 63) == 0) red[w] = v;
     __syncthreads();
-    v = red[0];
+    v = red[w0];
 #pragma unroll
-    for (int i = 1; i < NW; ++i) v = is_max ? fmax(v, red[i]) : v + red[i];
+    for (int i = 1; i < NW; ++i) v = is_max ? fmax(v, red[w0 + i]) : v + red[w0 + i];
   }
   return v;
 }

@@ -55,7 +55,7 @@ def _rows_near_data(p, rows, N, seed):
 
 
 @pytest.mark.parametrize("d,M,rows,N", [(33, 5, 70, 60), (300, 70, 257, 100), (3072, 64, 200, 200),
-                                        (1024, 256, 130, 500)])
+                                        (1024, 256, 130, 500), (256, 320, 90, 80), (512, 512, 131, 100)])
 def test_bf16_target_mean_matches_oracle(d, M, rows, N):
     p = make_gmm(d, M, mu_std=1.0, var=(0.01, 0.2), dirichlet=1.0, seed=d + M)
     x, step = _rows_near_data(p, rows, N, seed=rows)

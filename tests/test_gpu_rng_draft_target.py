@@ -85,8 +85,10 @@ def _target_case(d, M, rows, seed, mu_std=1.0, var=(0.01, 0.2)):
     return p
 
 
+# the last two: 256 < M <= 512, two rows per softmax workgroup, each over two
+# wavefronts (M = 320 leaves lanes past M)
 @pytest.mark.parametrize("d,M,rows,N", [(2, 4, 300, 100), (33, 5, 70, 60), (130, 70, 129, 200),
-                                        (3072, 64, 200, 200)])
+                                        (3072, 64, 200, 200), (300, 320, 150, 100), (512, 512, 130, 100)])
 def test_target_mean_matches_oracle(d, M, rows, N):
     p = _target_case(d, M, rows, seed=d + M)
     rng = np.random.default_rng(rows)

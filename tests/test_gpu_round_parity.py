@@ -5,7 +5,10 @@ read through sd_sampler_state before and after each round; tests/round_parity.py
 holds the comparison rules.
 
 * bf16 fused rounds at the pixel12288 and latent16384 shapes (K + 1 = 17 and 9:
-  the aligned mean kernel with its two-chain cache rows): m^q per-row relative
+  the 128-row mean tiles whose rows straddle chains, and the chain-aligned
+  288 x 256 tiles, 32 chains of 9 rows), and at shapes that give the
+  chain-aligned tile other chain counts (K + 1 = 2, 5, 17, 32: 56, 56, 16
+  and 9 chains per tile, partial last tiles, M not a power of two): m^q per-row relative
   L2 <= 2e-2 against the float64 oracle, then, stage-wise, ||Delta||, ell, tau,
   coins, alpha_res, U, the new state and the next cache against the oracle fed
   the GPU's own drafts and m^q.  Reduced B (row tiles that straddle chains,
@@ -50,10 +53,13 @@ def _straddling(B, K1, tile=128):
 
 
 # (workload or (d, M, K, N), B, sampled chains): the two bf16 workloads' shapes
-# at reduced and full B, and a block of K + 1 = 5 rows (the mean kernel's
-# general epilogue)
+# at reduced and full B, a block of K + 1 = 5 rows with M = 64 (the 128-row
+# kernel's general epilogue), and M >= 512 with d a multiple of 256 (the
+# chain-aligned tile) at K + 1 = 5, 17, 2 and 32
 BF16_ROUNDS = [("latent16384", 16, None), ("pixel12288", 16, None), ("latent16384", 256, 20),
-               ("pixel12288", 512, 20), ((1024, 64, 4, 40), 48, None)]
+               ("pixel12288", 512, 20), ((1024, 64, 4, 40), 48, None), ((512, 512, 4, 40), 70, None),
+               ((512, 512, 16, 60), 40, None), ((768, 576, 1, 30), 130, None),
+               ((512, 1024, 31, 80), 20, None)]
 
 
 @pytest.mark.parametrize("name,B,nsel", BF16_ROUNDS)

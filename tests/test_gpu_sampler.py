@@ -71,10 +71,11 @@ def test_sampler_deterministic_and_block_beats_token():
 
 # (d, M, B, K, N, seed): K > N (every block ragged, the largest K), one chain
 # with K = 1, the aligned float32 path (M = 64, d a multiple of 64), ragged d
-# with M % 4 == 0, and M = 128 (two k-chunks in the mean GEMM, the
-# four-components-per-lane softmax)
+# with M % 4 == 0, M = 128 (two k-chunks in the mean GEMM, the
+# four-components-per-lane softmax), and M = 320 (two rows per softmax
+# workgroup, each over two wavefronts)
 SMALL = [(5, 3, 7, 64, 40, 1), (8, 4, 1, 1, 30, 2), (128, 64, 20, 4, 30, 3),
-         (130, 12, 9, 7, 25, 4), (256, 128, 8, 3, 20, 5)]
+         (130, 12, 9, 7, 25, 4), (256, 128, 8, 3, 20, 5), (64, 320, 9, 3, 20, 6)]
 
 
 @pytest.mark.parametrize("d,M,B,K,N,seed", SMALL)

@@ -7,7 +7,8 @@ whose oracle run records a coin within 1e-6 of its threshold; log-ratios to
 1e-10 relative (float64 reductions of the same float32 data); U to 1e-7;
 states within 1e-4 of max(|ref|, rms(row)) (float32 arithmetic against the
 float64 oracle).  The plain EM chain compounds float32 rounding over N target
-calls and is held to the same per-row bound on tiny2d, 1e-3 at d = 3072.
+calls and is held to the same per-row bound, on tiny2d and on pixel3072 over
+its whole schedule (N = 200).
 """
 import math
 
@@ -215,7 +216,7 @@ def test_reflection_with_block_rejected():
     assert e.value.status == _lib.SD_EINVAL
 
 
-@pytest.mark.parametrize("wl,B,N,rtol", [("tiny2d", 256, 100, 1e-4), ("pixel3072", 6, 12, 1e-4)])
+@pytest.mark.parametrize("wl,B,N,rtol", [("tiny2d", 256, 100, 1e-4), ("pixel3072", 6, 200, 1e-4)])
 def test_plain_em_matches_oracle(wl, B, N, rtol):
     p = workload_gmm(wl)
     seed = 17
