@@ -491,9 +491,12 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
 template <class T>
 struct BigMean {
   static constexpr int QW = T::TC / 64;  // column wavefronts
+  // LDS stride of a chain's G and cache rows in floats: four more than a row,
+  // so the two or three chains of a 16-lane row group fall on different banks
+  static constexpr int GS = T::TC + 4;
   // chains whose G and cache rows fit the operand buffers beside the partials
   static constexpr int kFit = (int)((2 * sizeof(typename T::Lds) - QW * bf16b::TR * 3 * sizeof(double)) /
-                                    (2 * sizeof(float) * T::TC));
+                                    (2 * sizeof(float) * GS));
   static constexpr int kChains = kFit < 56 ? kFit : 56;
 };
 
@@ -537,7 +540,7 @@ __global__ __launch_bounds__(T::kThreads, T::TC == 128 ? 2 : 1) void gmm_mean_lr
   using bf16b::CB;
   using bf16b::RB;
   using bf16b::TR;
-  constexpr int TC = T::TC, QW = BigMean<T>::QW, NCH = BigMean<T>::kChains;
+  constexpr int TC = T::TC, QW = BigMean<T>::QW, NCH = BigMean<T>::kChains, GS = BigMean<T>::GS;
   if (gate && *gate == 0) return;
   __shared__ typename T::Lds sm[2];
   __shared__ float rc[3 * TR];
@@ -594,16 +597,17 @@ __global__ __launch_bounds__(T::kThreads, T::TC == 128 ? 2 : 1) void gmm_mean_lr
   load_x(1, xraw[1]);
   // G of the tile's chains and columns (four normals per Philox block) and the
   // chains' cache rows, into the (now free) operand buffers: gz, svs
-  // [chain][column]; then the per-row partial sums of each column wavefront
+  // [chain][column], GS floats per chain; then the per-row partial sums of
+  // each column wavefront
   float* gz = reinterpret_cast<float*>(&sm[0]);
-  float* svs = gz + NCH * TC;
-  double* part = reinterpret_cast<double*>(svs + NCH * TC);
+  float* svs = gz + NCH * GS;
+  double* part = reinterpret_cast<double*>(svs + NCH * GS);
   for (int e = threadIdx.x; e < nchain * (TC / 4); e += T::kThreads) {
     const int cl = e / (TC / 4), g4 = e % (TC / 4);
     const float4 z = normals4(philox((uint32_t)((c0 >> 2) + g4), (uint32_t)(b_first + cl), crnd[cl],
                                      TAG_RESID << 24, seed));
-    *reinterpret_cast<float4*>(&gz[cl * TC + 4 * g4]) = z;
-    *reinterpret_cast<float4*>(&svs[cl * TC + 4 * g4]) = buf_ld4(vs, (uint32_t)((cl * d + c0 + 4 * g4) * 4));
+    *reinterpret_cast<float4*>(&gz[cl * GS + 4 * g4]) = z;
+    *reinterpret_cast<float4*>(&svs[cl * GS + 4 * g4]) = buf_ld4(vs, (uint32_t)((cl * d + c0 + 4 * g4) * 4));
   }
   __syncthreads();
   const int wc = T::col_wave(), sub = (threadIdx.x >> 4) & 3;
@@ -636,11 +640,11 @@ __global__ __launch_bounds__(T::kThreads, T::TC == 128 ? 2 : 1) void gmm_mean_lr
                                      : buf_ld4(vx, (uint32_t)(((lr + 1) * d + c0 + tcol) * 4));
         const bf16b::f32x4 o = acc[rb][cb];
         const float4 x = xa[cb];
-        const float4 sv = *reinterpret_cast<const float4*>(&svs[b * TC + tcol]);
+        const float4 sv = *reinterpret_cast<const float4*>(&svs[b * GS + tcol]);
         const float4 qv = make_float4(c1 * x.x + c2 * (o[0] - rho * x.x), c1 * x.y + c2 * (o[1] - rho * x.y),
                                       c1 * x.z + c2 * (o[2] - rho * x.z), c1 * x.w + c2 * (o[3] - rho * x.w));
         qs[h] = qv;
-        const float4 gv = *reinterpret_cast<const float4*>(&gz[b * TC + tcol]);
+        const float4 gv = *reinterpret_cast<const float4*>(&gz[b * GS + tcol]);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const float pe = draft_mean(c1, comp(x, e), c2s, comp(sv, e));  // m^p

@@ -13,6 +13,8 @@ holds the comparison rules.
   coins, alpha_res, U, the new state and the next cache against the oracle fed
   the GPU's own drafts and m^q.  Reduced B (row tiles that straddle chains,
   a ragged last tile) and one round at the full B.
+* a whole bf16 run on the chain-aligned tile (d = 1024, M = 512, K = 8) in
+  lockstep for the three modes: 24 chains stage-wise every round.
 * pixel3072 in float32 at the benchmark's size (B = 1024, N = 200) in
   lockstep for block/Free, token/reflection and block/Frozen: 32 chains every
   round stage-wise and, in turn, every fourth round of each against the
@@ -116,12 +118,16 @@ def test_bf16_fused_round_stagewise(name, B, nsel):
 
 
 def _lockstep(mode, residual, drafter, name="pixel3072", B=None, N=None, K=None, M=None, d=None,
-              nchains=32, seed=0, every=4):
+              nchains=32, seed=0, every=4, precision=None):
+    """Run the sampler a round per call and check `nchains` chains every round
+    stage-wise; with every > 0 also, in turn, every `every`-th round of each
+    against the oracle's own round (float32 targets only)."""
     cfg = WORKLOADS[name]
     B, N, K = B or cfg["B"], N or cfg["N"], K or cfg["K"]
     p = workload_gmm(name) if d is None else make_gmm(d, M, mu_std=1.0, var=(0.01, 0.2), dirichlet=1.0,
                                                       seed=d)
-    tgt = _lib.Target(_lib.schedule(N), p["mu"], p["var"], p["log_w"])
+    kw_t = {} if precision is None else dict(precision=precision)
+    tgt = _lib.Target(_lib.schedule(N), p["mu"], p["var"], p["log_w"], **kw_t)
     ws = torch.empty(_lib.sd_sampler_workspace(tgt, B, K), dtype=torch.uint8, device=DEV)
     trace = torch.zeros(N, B, dtype=torch.int32, device=DEV)
     chains = np.unique(np.linspace(0, B - 1, nchains).astype(int))
@@ -143,7 +149,7 @@ def _lockstep(mode, residual, drafter, name="pixel3072", B=None, N=None, K=None,
         active = 0
         for i, b in enumerate(chains):
             active += check_round(g, sch, K, seed, i, int(b), before, after, stats, *om,
-                                  independent=(r + i) % every == 0)
+                                  independent=every > 0 and (r + i) % every == 0)
         before = after
         r += 1
         if st["finished"]:
@@ -167,6 +173,19 @@ def test_pixel3072_full_size_lockstep(mode, residual, drafter):
     assert stats.ties <= max(3, stats.compared // 200), stats.ties
     print(f"lockstep: {stats.compared} chain-rounds, {stats.independent} independent, "
           f"ties {stats.ties}, float32 flips {stats.f32_flips}, worst {stats.worst}")
+
+
+@pytest.mark.parametrize("mode,residual,drafter", list(_MODES))
+def test_bf16_chain_aligned_tile_lockstep(mode, residual, drafter):
+    # a whole bf16 run on the chain-aligned mean tile (M = 512, d a multiple of
+    # 256, K + 1 = 9: 32 chains per tile; 72 chains leave a last tile of 8),
+    # 24 chains checked stage-wise every round: the oracle's verification and
+    # residual fed the GPU's drafts, m^q and draft means
+    stats, st = _lockstep(mode, residual, drafter, B=72, N=60, K=8, M=512, d=1024, nchains=24, seed=3,
+                          every=0, precision=_lib.SD_BF16)
+    assert stats.compared >= 24 * (60 // 9) and stats.independent == 0
+    assert stats.ties <= max(3, stats.compared // 200), stats.ties
+    print(f"bf16 lockstep: {stats.compared} chain-rounds, ties {stats.ties}, worst {stats.worst}")
 
 
 def test_streamed_draft_rows_lockstep():
