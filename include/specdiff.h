@@ -19,6 +19,9 @@
  *    sd_target_create also allocates 1 KB of mapped pinned host memory: the
  *    words through which a running sampler call learns, round by round,
  *    whether any chain is still active (up to 64 calls at once per target).
+ *    A sampler call that runs two chain groups (sd_sampler_options.groups)
+ *    creates one HIP stream the first time it uses a given slot of those
+ *    words; the target keeps it until sd_target_destroy.
  *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL is the
  *    null stream).  Only sd_run_sampler reads results back: a per-round "any
  *    chain active" flag that its kernels store into the mapped host memory,
@@ -45,7 +48,7 @@
 extern "C" {
 #endif
 
-#define SD_ABI_VERSION 3
+#define SD_ABI_VERSION 4
 #define SD_MAX_BLOCK 64
 
 typedef enum {
@@ -302,7 +305,21 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
  *                       chain has reached step N; n >= 0 = at most n (0 with
  *                       start_round 0 only initialises).  The state stays in
  *                       ws (see sd_sampler_state); a call that ends before the
- *                       run is finished does not write y_out. */
+ *                       run is finished does not write y_out;
+ *  groups               1: every round runs as one sequence of kernels on
+ *                       `stream`; 2: the chains are split into two halves
+ *                       (the first B/2 and the rest) whose rounds run on
+ *                       `stream` and on a second stream of the library at
+ *                       the same time, so that one half's latency-bound
+ *                       kernels overlap the other's matrix work (joined back
+ *                       into `stream` before the call returns); 0: the
+ *                       library chooses (two when each half has at least
+ *                       2048 target rows, B/2 (K+1)).  The results do not
+ *                       depend on it:
+ *                       every row is computed in the same order either way,
+ *                       so y_out, tau_trace, the statistics and the state are
+ *                       bit-identical.  A run split over calls may change it
+ *                       between calls.  With B = 1 it is 1. */
 typedef struct {
   sd_verify_mode mode;
   sd_usample_mode usample_mode;
@@ -311,12 +328,13 @@ typedef struct {
   double omega;
   int32_t start_round;
   int32_t max_rounds;
+  int32_t groups;
 } sd_sampler_options;
 
 /* sd_run_sampler with options (sd_run_sampler is this call with DECOMPOSITION,
- * FREE, omega = 1, start_round = 0 and max_rounds = -1).  Same workspace
- * (sd_sampler_workspace), outputs and errors; SD_EINVAL also for a negative
- * start_round. */
+ * FREE, omega = 1, start_round = 0, max_rounds = -1 and groups = 0).  Same
+ * workspace (sd_sampler_workspace, sized for either grouping), outputs and
+ * errors; SD_EINVAL also for a negative start_round or groups outside 0..2. */
 sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
                             const sd_sampler_options* options, uint64_t seed, float* y_out,
                             int32_t* tau_trace, int32_t trace_rounds, sd_stats* stats, void* ws,

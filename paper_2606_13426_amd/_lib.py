@@ -42,7 +42,7 @@ class sd_stats(ctypes.Structure):
 class sd_sampler_options(ctypes.Structure):
     _fields_ = [("mode", c_int32), ("usample_mode", c_int32), ("residual", c_int32),
                 ("drafter", c_int32), ("omega", c_double), ("start_round", c_int32),
-                ("max_rounds", c_int32)]
+                ("max_rounds", c_int32), ("groups", c_int32)]
 
 
 class sd_sampler_view(ctypes.Structure):
@@ -321,11 +321,12 @@ def sd_run_sampler(target, B, K, seed, mode=SD_BLOCK, usample_mode=SD_USAMPLE_EX
 def sd_run_sampler_ex(target, B, K, seed, mode=SD_BLOCK, usample_mode=SD_USAMPLE_EXACT,
                       residual=SD_RESIDUAL_DECOMPOSITION, drafter=SD_DRAFTER_FREE, omega=1.0,
                       y_out=None, trace_rounds=0, ws=None, device="cuda", start_round=0,
-                      max_rounds=-1, trace=None):
-    """Alg. 8 with the sampler options (residual, drafter, temperature, and the
+                      max_rounds=-1, trace=None, groups=0):
+    """Alg. 8 with the sampler options (residual, drafter, temperature, the
     rounds of a run this call does: max_rounds < 0 until done, 0 initialise
-    only); returns as sd_run_sampler.  A partial run continues with the same
-    ws (and trace) and start_round = stats["rounds"]."""
+    only, and the chain groups run concurrently: 0 the library's choice, 1, 2);
+    returns as sd_run_sampler.  A partial run continues with the same ws (and
+    trace) and start_round = stats["rounds"]."""
     import torch
     if y_out is None:
         y_out = torch.empty(B, target.d, dtype=torch.float32, device=device)
@@ -337,7 +338,7 @@ def sd_run_sampler_ex(target, B, K, seed, mode=SD_BLOCK, usample_mode=SD_USAMPLE
         trace_rounds = trace.shape[0]
     st = sd_stats()
     opts = sd_sampler_options(mode, usample_mode, residual, drafter, float(omega), int(start_round),
-                              int(max_rounds))
+                              int(max_rounds), int(groups))
     _check(load().sd_run_sampler_ex(target.handle, B, K, ctypes.byref(opts), seed, _p(y_out), _p(trace),
                                     trace_rounds, ctypes.byref(st), _p(ws), ws.numel(), _stream()),
            "sd_run_sampler_ex")

@@ -41,10 +41,11 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
     const float* __restrict__ MQ, float* __restrict__ y, int32_t* __restrict__ step,
     double* __restrict__ sigma, int32_t* __restrict__ hist, int64_t* __restrict__ steps,
     int* act_next, int32_t* __restrict__ trace, int r_round, int trace_rounds, bool vec_ok,
-    bool frozen, bool stream, const int* gate) {
+    bool frozen, bool stream, const int* gate, int chain0, int trace_ld) {
   if (gate && *gate == 0) return;
   const int N = sc.N, K1 = K + 1;
   const int b = blockIdx.y;
+  const uint32_t chain = (uint32_t)(chain0 + b);  // the generator's chain index
   const int t = tauv[b];
   const int k = kcur[b];
   const uint32_t r = rcur[b];
@@ -68,7 +69,7 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
       crow_next[b] = crow_cur[b];
       cstep_next[b] = cstep_cur[b];
     }
-    if (trace && r_round < trace_rounds) trace[(int64_t)r_round * B + b] = active ? t : 0;
+    if (trace && r_round < trace_rounds) trace[(int64_t)r_round * trace_ld + b] = active ? t : 0;
   }
   if (!active) return;
   // the next round's step index and sigma of every target row
@@ -96,7 +97,7 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
     const float4 cn = step_coef(sc, coef, k + t - 1);
     const float c2s = cn.y * step_coef(sc, coef, cstep_cur[b]).w;
     const float sg = rsig[b], cf = rcoef[b];
-    const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, TAG_RESID << 24, seed));
+    const float4 z = normals4(philox((uint32_t)g, chain, r, TAG_RESID << 24, seed));
 #pragma unroll
     for (int c = 0; c < 4; ++c) {
       const float pv = draft_mean(cn.x, xv[c], c2s, sv[c]);
@@ -121,7 +122,7 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
     float qv[4];
     load4(qb + (int64_t)kb * d, cnt, vec, qv);
     const float sg = rsig[b];
-    const float4 z = normals4(philox((uint32_t)g, (uint32_t)b, r, TAG_TARGET << 24, seed));
+    const float4 z = normals4(philox((uint32_t)g, chain, r, TAG_TARGET << 24, seed));
 #pragma unroll
     for (int c = 0; c < 4; ++c) yv[c] = qv[c] + sg * get4(z, c);
   } else {
@@ -144,7 +145,7 @@ __global__ __launch_bounds__(kThreads) void advance_kernel(
   for (int c = 0; c < 4; ++c) sv[c] = qcv[c] - cc.x * xcv[c];  // c2_c S_c
   store4(sb, cnt, vec, sv);
   store4(xb, cnt, vec, yv, stream);
-  draft_rows(sc, coef, K, knew, min(K, N - knew), (uint32_t)b, r + 1u, seed, g, yv, sv, cc.w, xb,
+  draft_rows(sc, coef, K, knew, min(K, N - knew), chain, r + 1u, seed, g, yv, sv, cc.w, xb,
              d, nullptr, d, cnt, vec, stream);
 }
 
@@ -158,15 +159,16 @@ hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int
                           const float* rsig, float* x, float* sv, const float* mq, float* y,
                           int32_t* step, double* sigma, int32_t* hist, int64_t* steps,
                           int* act_next, int32_t* trace, int r, int trace_rounds, bool frozen,
-                          hipStream_t s, const int* gate) {
+                          hipStream_t s, const int* gate, int chain0, int trace_ld,
+                          int64_t stream_bytes) {
   const int ng = (d + 3) / 4;
   dim3 grid((ng + kThreads - 1) / kThreads, B);
   const bool vec = (d % 4 == 0) && aligned16(x) && aligned16(sv) && aligned16(mq) && aligned16(y);
-  const bool stream = stream_rows((int64_t)B * (K + 1) * d * 4);
+  const bool stream = stream_rows(stream_bytes > 0 ? stream_bytes : (int64_t)B * (K + 1) * d * 4);
   return launch_timed("advance", advance_kernel, grid, dim3(kThreads), s, sc, coef, B, K, d, seed,
                       kcur, rcur, crow_cur, cstep_cur, knext, rnext, crow_next, cstep_next, tau, rmode,
                       rcoef, rsig, x, sv, mq, y, step, sigma, hist, steps, act_next, trace, r,
-                      trace_rounds, vec, frozen, stream, gate);
+                      trace_rounds, vec, frozen, stream, gate, chain0, trace_ld > 0 ? trace_ld : B);
 }
 
 }  // namespace sd

@@ -325,9 +325,11 @@ sd_status sd_target_destroy(sd_target target) {
   if (t->musq) (void)hipFree(t->musq);
   if (t->coef) (void)hipFree(t->coef);
   // a flag group still held by a call that timed out may be written by its
-  // kernels later: that memory is then left allocated
-  if (t->host_flags && __atomic_load_n(&t->flag_busy, __ATOMIC_ACQUIRE) == 0)
-    (void)hipHostFree(t->host_flags);
+  // kernels later: that memory and those side streams are then left alone
+  const bool idle = __atomic_load_n(&t->flag_busy, __ATOMIC_ACQUIRE) == 0;
+  if (t->host_flags && idle) (void)hipHostFree(t->host_flags);
+  for (int g = 0; g < kFlagGroups && idle; ++g)
+    if (t->side[g]) (void)hipStreamDestroy(t->side[g]);
   delete t;
   return SD_OK;
 }
@@ -493,10 +495,27 @@ namespace {
 
 struct SamplerLayout {
   size_t y, x, sv, mq, sigma, step, k2, rnd2, crow2, cstep2, tau, rmode, rcoef, rsig, hist, steps,
-      act, nan, kb, left, dummy_i32, dummy_i64, coins, lar, ures, ties, lrp, tws, total;
-  size_t tws_bytes;
+      act, nan, kb, left, dummy_i32, dummy_i64, coins, lar, ures, ties, lrp, tws, tws1, total;
+  size_t tws_bytes, tws1_bytes;
   int nct;
 };
+
+// With two chain groups, group 0 holds chains [0, B / 2) and group 1 the rest.
+inline int group_chain0(int B, int groups, int g) { return groups == 2 && g == 1 ? B / 2 : 0; }
+inline int group_chains(int B, int groups, int g) {
+  return groups == 2 ? (g == 0 ? B / 2 : B - B / 2) : B;
+}
+
+// The library's choice of chain groups (sd_sampler_options.groups = 0): two
+// when each half still has 2048 target rows or more.  Measured (one group /
+// two, ms per run): pixel3072 30.6 / 29.0, pixel12288 232 / 222, latent16384
+// 249 / 255 -- its 2304 rows make a logits grid of 252 one-per-CU workgroups,
+// and two halves need 280, a second wave.
+inline int choose_groups(int B, int K, int requested) {
+  if (B < 2) return 1;
+  if (requested == 1 || requested == 2) return requested;
+  return (int64_t)(B / 2) * (K + 1) >= 2048 ? 2 : 1;
+}
 
 inline size_t a256(size_t x) { return (x + 255) & ~(size_t)255; }
 
@@ -526,7 +545,7 @@ SamplerLayout sampler_layout(const Target& t, int B, int K) {
   L.rsig = take(4 * Bs);
   L.hist = take(4 * Bs * (SD_MAX_BLOCK + 2));
   L.steps = take(8 * Bs);
-  L.act = take(4 * 2);
+  L.act = take(4 * 2 * 2);  // [group][round parity]
   L.nan = take(4);
   L.kb = take(4 * Bs);
   L.left = take(4 * Bs);
@@ -538,10 +557,19 @@ SamplerLayout sampler_layout(const Target& t, int B, int K) {
   L.ties = take(4 * Bs);
   L.lrp = take(8 * 3 * Bs * K1 * (size_t)L.nct);
   // the target calls on all B (K + 1) rows and, with the Frozen Drafter, on the
-  // B states alone (fewer rows may take more splits of the logits GEMM)
-  const size_t rows = Bs * K1;
-  L.tws_bytes = std::max(target_ws_bytes(t, (int)rows), target_ws_bytes(t, B));
+  // B states alone (fewer rows may take more splits of the logits GEMM); with
+  // two chain groups each group's calls on its own rows, split as for all
+  // rows (so that every row is summed in the same order)
+  const int rows = (int)(Bs * K1);
+  L.tws_bytes = std::max(target_ws_bytes(t, rows), target_ws_bytes(t, B));
+  L.tws1_bytes = 0;
+  if (B >= 2) {
+    const int b0 = B / 2, b1 = B - B / 2;
+    L.tws_bytes = std::max({L.tws_bytes, target_ws_bytes(t, b0 * (int)K1, rows), target_ws_bytes(t, b0, B)});
+    L.tws1_bytes = std::max(target_ws_bytes(t, b1 * (int)K1, rows), target_ws_bytes(t, b1, B));
+  }
   L.tws = take(L.tws_bytes);
+  L.tws1 = take(L.tws1_bytes);
   L.total = off;
   return L;
 }
@@ -559,7 +587,7 @@ sd_status sd_run_sampler(sd_target target, int32_t B, int32_t K, sd_verify_mode 
                          sd_usample_mode usample_mode, uint64_t seed, float* y_out,
                          int32_t* tau_trace, int32_t trace_rounds, sd_stats* stats, void* ws,
                          size_t ws_bytes, sd_stream stream) {
-  const sd_sampler_options o{mode, usample_mode, SD_RESIDUAL_DECOMPOSITION, SD_DRAFTER_FREE, 1.0, 0, -1};
+  const sd_sampler_options o{mode, usample_mode, SD_RESIDUAL_DECOMPOSITION, SD_DRAFTER_FREE, 1.0, 0, -1, 0};
   return sd_run_sampler_ex(target, B, K, &o, seed, y_out, tau_trace, trace_rounds, stats, ws,
                            ws_bytes, stream);
 }
@@ -628,6 +656,8 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
                    isfinite(opts->omega * opts->omega),
                "sd_run_sampler: omega must be positive and finite, with omega^2 too");
   SD_CHECK_ARG(opts->start_round >= 0, "sd_run_sampler: start_round must be >= 0");
+  SD_CHECK_ARG(opts->groups >= 0 && opts->groups <= 2, "sd_run_sampler: groups = %d not in 0..2",
+               opts->groups);
   SD_CHECK_ARG(target, "sd_run_sampler: target is NULL");
   Target* tp = reinterpret_cast<Target*>(target);
   const Target& t = *tp;
@@ -674,6 +704,9 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
   int64_t* dummy64 = reinterpret_cast<int64_t*>(base + L.dummy_i64);
   void* tws = base + L.tws;
   const sd_stride xs{(int64_t)K1 * d, d}, mqs{(int64_t)K1 * d, d};
+  const int G = choose_groups(B, K, opts->groups);
+  // the draft rows are streamed past the caches, or not, as for the whole block
+  const int64_t block_bytes = (int64_t)B * K1 * d * 4;
 
   if (start == 0) {
     // Y_0 (also row 0 of x); the one explicit target call at Y_0, whose mean
@@ -687,8 +720,7 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
     SD_HIP(fill_i32_launch(hist, (int64_t)B * (SD_MAX_BLOCK + 2), 0, s));
     SD_HIP(fill_i64_launch(steps, B, 0, s));
     SD_HIP(fill_i32_launch(ties, B, 0, s));
-    SD_HIP(fill_i32_launch(act, 1, 1, s));
-    SD_HIP(fill_i32_launch(act + 1, 1, 0, s));
+    SD_HIP(fill_i32_launch(act, 4, 0, s));
     SD_HIP(fill_i32_launch(nanflag, 1, 0, s));
     SD_HIP(fill_i32_launch(step, B, 0, s));
     SD_HIP(fill_i32_launch(tau, B, 0, s));
@@ -703,25 +735,76 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
       SD_HIP(draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2, cstep2, mq, mqs, k2, rnd2, seed,
                                  x, xs, sv, s, nullptr));
   }
+  // each group's gate of round `start` (whether any of its chains is still
+  // active), from the chains' steps: a resumed run may group its chains
+  // differently from the call that left the state
+  const int par0 = start & 1;
+  SD_HIP(chains_active_launch(B, G == 2 ? B / 2 : B, N, k2 + par0 * B, act + par0, act + 2 + par0, s));
 
   // Round r's scan publishes round r - 1's active flag, tagged with r - 1, into
-  // slot (r - 1) % kFlagSlots of this call's group of mapped host words.  After
-  // enqueueing round r the host polls round r - kLag's slot until the tag is
-  // there (the queue stays kLag rounds ahead) and stops enqueueing at the
-  // first cleared flag.  No event or copy is queued per round: a marker
+  // slot (r - 1) % kFlagSlots of its group's block of mapped host words.  After
+  // enqueueing round r the host polls round r - kLag's slots until the tags are
+  // there (the queue stays kLag rounds ahead) and stops enqueueing once every
+  // group's flag is cleared.  No event or copy is queued per round: a marker
   // between rounds would hold the next round's first kernel back by several
   // microseconds.  The first flag this call reads is that of round start - 1
   // (published by round start's scan), so a finished run is seen at once.
-  const int grp = acquire_flags(tp);
-  if (grp < 0) {
-    set_error("sd_run_sampler: more than %d sampler calls at once on one target", kFlagGroups);
-    return SD_EUNSUPPORTED;
+  // With two chain groups the second group's rounds run on a second stream,
+  // forked from `stream` after the first group's first target call (so that
+  // the two run half a round apart: one group's latency-bound scan and
+  // residual overlap the other's GEMMs) and joined back into it at the end.
+  struct GroupRun {
+    int c0, nb, grp;
+    void* tws;
+    hipStream_t st;
+    int32_t* host_dev;
+    volatile int32_t* pub;
+  };
+  GroupRun gr[2]{};
+  auto release_all = [&]() {
+    for (int g = 0; g < G; ++g)
+      if (gr[g].grp >= 0) release_flags(tp, gr[g].grp);
+  };
+  for (int g = 0; g < G; ++g) gr[g].grp = -1;
+  for (int g = 0; g < G; ++g) {
+    GroupRun& q = gr[g];
+    q.c0 = group_chain0(B, G, g);
+    q.nb = group_chains(B, G, g);
+    q.tws = g == 0 ? tws : base + L.tws1;
+    q.grp = acquire_flags(tp);
+    if (q.grp < 0) {
+      release_all();
+      set_error("sd_run_sampler: more than %d sampler calls (or chain groups) at once on one target",
+                kFlagGroups);
+      return SD_EUNSUPPORTED;
+    }
+    int32_t* const host_act = t.host_flags + q.grp * kFlagSlots;
+    q.host_dev = t.host_flags_dev + q.grp * kFlagSlots;
+    for (int i = 0; i < kFlagSlots; ++i) host_act[i] = -1;  // tag -1: nothing published
+    q.pub = host_act;
+    q.st = s;
+    if (g == 1) {
+      hipStream_t& side = tp->side[q.grp];
+      if (!side && hipStreamCreateWithFlags(&side, hipStreamNonBlocking) != hipSuccess) {
+        side = nullptr;
+        release_all();
+        set_error("sd_run_sampler: the second chain group's stream could not be created");
+        return SD_EHIP;
+      }
+      q.st = side;
+    }
   }
-  int32_t* const host_act = t.host_flags + grp * kFlagSlots;
-  int32_t* const host_act_dev = t.host_flags_dev + grp * kFlagSlots;
-  for (int i = 0; i < kFlagSlots; ++i) host_act[i] = -1;  // tag -1: nothing published
   std::atomic_thread_fence(std::memory_order_seq_cst);
-  volatile int32_t* const pub = host_act;
+  hipEvent_t fork = nullptr, join = nullptr;
+  if (G == 2) {
+    if (hipEventCreateWithFlags(&fork, hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&join, hipEventDisableTiming) != hipSuccess) {
+      release_all();
+      set_error("sd_run_sampler: could not create the events of the second chain group");
+      return SD_EHIP;
+    }
+  }
+  bool forked = false;
   constexpr int kQuietMs = 20;
   const int first_flag = start > 0 ? start - 1 : 0;
   sd_status st = SD_OK;
@@ -729,34 +812,55 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
   int64_t rounds = -1;
   Clock::time_point last_progress = Clock::now();
   int r = start;
-  for (; r < end && rounds < 0; ++r) {
-    const int cur = r & 1, nxt = cur ^ 1;
-    const int* gate = act + cur;
+  auto enqueue = [&](const GroupRun& q, int cur, int nxt) -> hipError_t {
+    const int b0 = q.c0, nb = q.nb;
+    const int64_t rows0 = (int64_t)b0 * K1;
+    float *xg = x + rows0 * d, *mqg = mq + rows0 * d, *svg = sv + (int64_t)b0 * d,
+          *yg = y + (int64_t)b0 * d;
+    int32_t* stepg = step + rows0;
+    double *sigmag = sigma + rows0, *lrpg = lrp + rows0 * L.nct * 3;
+    const int32_t *kc = k2 + cur * B + b0, *crc = crow2 + cur * B + b0, *csc = cstep2 + cur * B + b0;
+    const uint32_t* rc = rnd2 + cur * B + b0;
+    const int* gate = act + 2 * (&q - gr) + cur;
+    int* next = act + 2 * (&q - gr) + nxt;
     hipError_t e = hipSuccess;
     if (frozen) {
       // the Frozen Drafter's target call at (Y_k, k) into row 0 of m^q (the
       // cache steps hold min(k, N - 1)), then the block drafted with that score
-      e = target_mean_launch(t, B, x, (int64_t)K1 * d, cstep2 + cur * B, mq, (int64_t)K1 * d,
-                             nullptr, 0, tws, s, gate);
+      e = target_mean_launch(t, nb, xg, (int64_t)K1 * d, csc, mqg, (int64_t)K1 * d, nullptr, 0, q.tws,
+                             q.st, gate, B);
       if (e == hipSuccess)
-        e = draft_cached_launch(t.sc, t.coef, B, K, d, y, crow2 + cur * B, cstep2 + cur * B, mq,
-                                mqs, k2 + cur * B, rnd2 + cur * B, seed, x, xs, sv, s, gate);
+        e = draft_cached_launch(t.sc, t.coef, nb, K, d, yg, crc, csc, mqg, mqs, kc, rc, seed, xg, xs, svg,
+                                q.st, gate, b0, block_bytes);
     }
     if (e == hipSuccess)
-      e = target_mean_lr_launch(t, B * K1, K1, x, step, mq, sv, cstep2 + cur * B, lrp,
-                                rnd2 + cur * B, seed, tws, s, gate);
-    int32_t* publish = r >= 1 ? host_act_dev + (r - 1) % kFlagSlots : nullptr;
+      e = target_mean_lr_launch(t, nb * K1, K1, xg, stepg, mqg, svg, csc, lrpg, rc, seed, q.tws, q.st,
+                                gate, B * K1, b0);
+    if (G == 2 && !forked && e == hipSuccess) {
+      // (the first group's first round: everything before this is on `stream`)
+      e = hipEventRecord(fork, s);
+      if (e == hipSuccess) e = hipStreamWaitEvent(gr[1].st, fork, 0);
+      forked = e == hipSuccess;
+    }
+    int32_t* publish = r >= 1 ? q.host_dev + (r - 1) % kFlagSlots : nullptr;
     if (e == hipSuccess)
-      e = scan_fused_launch(B, K, d, N, (int)mode, (int)usample_mode, lrp, L.nct, sigma,
-                            k2 + cur * B, rnd2 + cur * B, seed, w2, reflect, tau, rmode, rcoef,
-                            rsig, coins, lar, ures, ties, nanflag, act + nxt, publish, r - 1, s,
-                            gate);
+      e = scan_fused_launch(nb, K, d, N, (int)mode, (int)usample_mode, lrpg, L.nct, sigmag, kc, rc, seed,
+                            w2, reflect, tau + b0, rmode + b0, rcoef + b0, rsig + b0, coins + b0,
+                            lar + b0, ures + b0, ties + b0, nanflag, next, publish, r - 1, q.st, gate,
+                            b0);
     if (e == hipSuccess)
-      e = advance_launch(t.sc, t.coef, B, K, d, seed, k2 + cur * B, rnd2 + cur * B,
-                         crow2 + cur * B, cstep2 + cur * B, k2 + nxt * B, rnd2 + nxt * B,
-                         crow2 + nxt * B, cstep2 + nxt * B, tau, rmode, rcoef, rsig, x, sv, mq, y,
-                         step, sigma, hist, steps, act + nxt, tau_trace, r,
-                         tau_trace ? trace_rounds : 0, frozen, s, gate);
+      e = advance_launch(t.sc, t.coef, nb, K, d, seed, kc, rc, crc, csc, k2 + nxt * B + b0,
+                         rnd2 + nxt * B + b0, crow2 + nxt * B + b0, cstep2 + nxt * B + b0, tau + b0,
+                         rmode + b0, rcoef + b0, rsig + b0, xg, svg, mqg, yg, stepg, sigmag,
+                         hist + (int64_t)b0 * (SD_MAX_BLOCK + 2), steps + b0, next,
+                         tau_trace ? tau_trace + b0 : nullptr, r, tau_trace ? trace_rounds : 0,
+                         frozen, q.st, gate, b0, B, block_bytes);
+    return e;
+  };
+  for (; r < end && rounds < 0; ++r) {
+    const int cur = r & 1, nxt = cur ^ 1;
+    hipError_t e = hipSuccess;
+    for (int g = 0; g < G && e == hipSuccess; ++g) e = enqueue(gr[g], cur, nxt);
     if (e != hipSuccess) {
       set_error("sd_run_sampler: launch failed in round %d: %s", r, hipGetErrorString(e));
       st = SD_EHIP;
@@ -764,70 +868,89 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
     }
     const int back = r - kLag;
     if (back >= first_flag) {
-      // round back + 1's scan (enqueued) publishes round back's flag; the wait
-      // ends on the tag, or on an error or a drained stream reported by the
-      // runtime.  The runtime is asked only after kQuietMs without the tag: a
-      // stream query queues a marker whose system-scope release holds the
-      // next kernel back by several microseconds.
-      volatile int32_t* slot = pub + back % kFlagSlots;
-      int32_t v;
-      auto next_query = Clock::now() + std::chrono::milliseconds(kQuietMs);
-      for (uint32_t spin = 1; ((v = *slot) >> 1) != back; ++spin) {
-        if ((spin & 1023u) != 0) continue;
-        const Clock::time_point now = Clock::now();
-        if (now - last_progress > std::chrono::seconds(kStallSeconds)) {
-          set_error("sd_run_sampler: no round finished within %d s (round %d); the GPU may be hung",
-                    kStallSeconds, back);
+      // round back + 1's scans (enqueued) publish round back's flags; each
+      // wait ends on the tag, or on an error or a drained stream reported by
+      // the runtime.  The runtime is asked only after kQuietMs without the
+      // tag: a stream query queues a marker whose system-scope release holds
+      // the next kernel back by several microseconds.
+      bool any = false;
+      for (int g = 0; g < G && st == SD_OK; ++g) {
+        volatile int32_t* slot = gr[g].pub + back % kFlagSlots;
+        int32_t v;
+        auto next_query = Clock::now() + std::chrono::milliseconds(kQuietMs);
+        for (uint32_t spin = 1; ((v = *slot) >> 1) != back; ++spin) {
+          if ((spin & 1023u) != 0) continue;
+          const Clock::time_point now = Clock::now();
+          if (now - last_progress > std::chrono::seconds(kStallSeconds)) {
+            set_error("sd_run_sampler: no round finished within %d s (round %d); the GPU may be hung",
+                      kStallSeconds, back);
+            st = SD_EHIP;
+            stalled = true;
+            break;
+          }
+          if (now < next_query) continue;
+          next_query = now + std::chrono::milliseconds(kQuietMs);
+          const hipError_t q = hipStreamQuery(gr[g].st);
+          // not-ready is a status, not a failure: keep it out of the launch checks
+          if (q == hipErrorNotReady) {
+            (void)hipGetLastError();
+            continue;
+          }
+          v = *slot;
+          if (q == hipSuccess && (v >> 1) == back) break;
+          set_error("sd_run_sampler: round %d's flag was not published (%s)", back,
+                    hipGetErrorString(q));
           st = SD_EHIP;
-          stalled = true;
           break;
         }
-        if (now < next_query) continue;
-        next_query = now + std::chrono::milliseconds(kQuietMs);
-        const hipError_t q = hipStreamQuery(s);
-        // not-ready is a status, not a failure: keep it out of the launch checks
-        if (q == hipErrorNotReady) {
-          (void)hipGetLastError();
-          continue;
-        }
-        v = *slot;
-        if (q == hipSuccess && (v >> 1) == back) break;
-        set_error("sd_run_sampler: round %d's flag was not published (%s)", back,
-                  hipGetErrorString(q));
-        st = SD_EHIP;
-        break;
+        if (st == SD_OK && (v & 1) != 0) any = true;
       }
       if (st != SD_OK) break;
       last_progress = Clock::now();
-      if ((v & 1) == 0) rounds = back + 1;
+      if (!any) rounds = back + 1;
     }
   }
-  if (stalled) return st;  // the kernels may still write to the flag group: keep it
+  if (stalled) return st;  // the kernels may still write to the flag groups: keep them
+  if (G == 2) {
+    // the second group's work, done or failed, is ordered before what follows on `stream`
+    hipError_t e = hipEventRecord(join, gr[1].st);
+    if (e == hipSuccess) e = hipStreamWaitEvent(s, join, 0);
+    if (e != hipSuccess) {
+      set_error("sd_run_sampler: could not join the second chain group's stream: %s",
+                hipGetErrorString(e));
+      return SD_EHIP;  // keep the flag groups: the second stream may still run
+    }
+  }
   const Clock::time_point deadline = Clock::now() + std::chrono::seconds(kStallSeconds);
   bool finished = rounds >= 0;
   if (st == SD_OK && !finished) {
     // every launched round finishes; the flags of rounds up to r - 2 are then
     // in their slots, and the last round's, which no later scan publishes, is
     // copied
-    int32_t last_flag = 1;
+    int32_t last_flag[2] = {1, 1};
     hipError_t e = hipSuccess;
     bool late = false;
     if (r > start) {
-      e = hipMemcpyAsync(&last_flag, act + (r & 1), sizeof(int32_t), hipMemcpyDeviceToHost, s);
+      for (int g = 0; g < G && e == hipSuccess; ++g)
+        e = hipMemcpyAsync(&last_flag[g], act + 2 * g + (r & 1), sizeof(int32_t), hipMemcpyDeviceToHost, s);
       if (e == hipSuccess) e = wait_bounded(s, deadline, &late);
     }
     if (late) {
       set_error("sd_run_sampler: the last rounds did not finish within %d s", kStallSeconds);
-      return SD_EHIP;  // keep the flag group (see above)
+      return SD_EHIP;  // keep the flag groups (see above)
     }
     if (e != hipSuccess) {
       set_error("sd_run_sampler: waiting for the last rounds failed: %s", hipGetErrorString(e));
       st = SD_EHIP;
     }
     for (int back = std::max(r - kLag, first_flag); st == SD_OK && back < r; ++back) {
-      const int32_t v = pub[back % kFlagSlots];
-      const int32_t flag = back == r - 1 ? last_flag : ((v >> 1) == back ? (v & 1) : 1);
-      if (flag == 0) {
+      bool any = false;
+      for (int g = 0; g < G; ++g) {
+        const int32_t v = gr[g].pub[back % kFlagSlots];
+        const int32_t flag = back == r - 1 ? last_flag[g] : ((v >> 1) == back ? (v & 1) : 1);
+        if (flag != 0) any = true;
+      }
+      if (!any) {
         rounds = back + 1;
         finished = true;
         break;
@@ -860,7 +983,7 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
     if (e == hipSuccess) e = wait_bounded(s, deadline, &late);
     if (late) {
       set_error("sd_run_sampler: the final copies did not finish within %d s", kStallSeconds);
-      return SD_EHIP;  // keep the flag group (see above)
+      return SD_EHIP;  // keep the flag groups (see above)
     }
     if (e != hipSuccess) {
       set_error("sd_run_sampler: final copy failed: %s", hipGetErrorString(e));
@@ -895,9 +1018,11 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
       set_error("sd_run_sampler: the stream did not drain within %d s", kStallSeconds);
       st = SD_EHIP;
     }
-    return st;  // keep the flag group (see above)
+    return st;  // keep the flag groups (see above)
   }
-  release_flags(tp, grp);
+  release_all();
+  if (fork) (void)hipEventDestroy(fork);
+  if (join) (void)hipEventDestroy(join);
   return st;
 }
 

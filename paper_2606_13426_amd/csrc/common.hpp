@@ -111,35 +111,49 @@ struct Target {
   int32_t* host_flags;      // host address [kFlagGroups][kFlagSlots]
   int32_t* host_flags_dev;  // the same memory as the device sees it
   uint64_t flag_busy;
+  // the second stream of a sampler call that runs two chain groups, one per
+  // flag group (created at its first use, used only by the call that holds
+  // that flag group)
+  hipStream_t side[64];
 };
 constexpr int kFlagGroups = 64, kFlagSlots = 4;
+static_assert(sizeof(Target::side) / sizeof(hipStream_t) == kFlagGroups, "one side stream per flag group");
 
-size_t target_ws_bytes(const Target& t, int rows);
-size_t target_ws_bytes_bf16(const Target& t, int rows);
+// Workspace of a target call on `rows` rows whose logits GEMM is split over d
+// as for plan_rows rows (0: rows).  The split fixes the order in which the
+// partial logits are summed, so calls on parts of a batch that take the
+// whole batch's row count here give every row the same result as one call.
+size_t target_ws_bytes(const Target& t, int rows, int plan_rows = 0);
+size_t target_ws_bytes_bf16(const Target& t, int rows, int plan_rows = 0);
 // Rows' EM means (and scores if score != nullptr).  gate: nullable device flag;
 // when it reads 0 every kernel exits at once (finished sampler rounds).
 hipError_t target_mean_launch(const Target& t, int rows, const float* x, int64_t ldx,
                               const int32_t* step, float* mq, int64_t ldq, float* score,
-                              int64_t lds, void* ws, hipStream_t s, const int* gate);
+                              int64_t lds, void* ws, hipStream_t s, const int* gate,
+                              int plan_rows = 0);
 
 // The sampler's target call on its [B][K+1][d] block (x rows contiguous,
 // row stride d) that also leaves the verification's partial sums in
 // lrp[row][lr_tiles(t, K1)][3] (see gmm_mean_lr_kernel); the draft means are
 // recomputed from x, the cache rows sv [B][d] and the cache steps cstep [B];
-// rnd = chains' rounds.
+// rnd = chains' rounds; chain0 = the generator's chain index of the first
+// chain (a part of a batch); plan_rows as for target_ws_bytes.
 hipError_t target_mean_lr_launch(const Target& t, int rows, int K1, const float* x,
                                  const int32_t* step, float* mq, const float* sv,
                                  const int32_t* cstep, double* lrp, const uint32_t* rnd,
-                                 uint64_t seed, void* ws, hipStream_t s, const int* gate);
+                                 uint64_t seed, void* ws, hipStream_t s, const int* gate,
+                                 int plan_rows = 0, int chain0 = 0);
 int lr_tiles(const Target& t, int K1);
 // bf16 versions of the three calls above (dispatched to by them).
 hipError_t target_mean_bf16_launch(const Target& t, int rows, const float* x, int64_t ldx,
                                    const int32_t* step, float* mq, int64_t ldq, float* score,
-                                   int64_t lds, void* ws, hipStream_t s, const int* gate);
+                                   int64_t lds, void* ws, hipStream_t s, const int* gate,
+                                   int plan_rows = 0);
 hipError_t target_mean_lr_bf16_launch(const Target& t, int rows, int K1, const float* x,
                                       const int32_t* step, float* mq, const float* sv,
                                       const int32_t* cstep, double* lrp, const uint32_t* rnd,
-                                      uint64_t seed, void* ws, hipStream_t s, const int* gate);
+                                      uint64_t seed, void* ws, hipStream_t s, const int* gate,
+                                      int plan_rows = 0, int chain0 = 0);
 int lr_tiles_bf16(const Target& t, int K1);
 // Softmax over the split logits partials part[S][rows][M] (+ xsq[S][rows]):
 // P[rows][M] = r a / s2 (float32, or bf16 when p_bf16) and rowc[rows][3] =
@@ -150,19 +164,23 @@ hipError_t gmm_softmax_launch(const Target& t, int rows, int S, const float* par
 // Sampler verification on the fused partials (see scan_fused_kernel).
 // w2 = omega^2 (temperature; 1 = exact); reflect: the reflection residual.
 // coins, lar, ures [B]: the round's decision record; ties [B]: running count
-// of coins within 1e-6 of their thresholds.
+// of coins within 1e-6 of their thresholds; chain0: the generator's chain
+// index of chain 0.
 hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, const double* lrp,
                              int nct, const double* sigma, const int32_t* kcur,
                              const uint32_t* rcur, uint64_t seed, double w2, bool reflect,
                              int32_t* tau, int32_t* rmode, float* rcoef, float* rsig,
                              uint64_t* coins, double* lar, double* ures, int32_t* ties,
                              int* nanflag, int* act_next, int* host_prev, int pub_round,
-                             hipStream_t s, const int* gate);
+                             hipStream_t s, const int* gate, int chain0 = 0);
 // Residual, commit and the next round's Free-Drafter block, elementwise over
 // (chain, four coordinates); per-chain state is read from the *cur arrays and
 // written to the *next arrays (round parity), so no workgroup races another.
 // frozen: the Frozen Drafter drafts after its own target call, so the round
 // ends with the new state in x row 0 and the next cache at (row 0, step k).
+// chain0: the generator's chain index of chain 0; trace rows are trace_ld
+// chains apart (0: B).  stream_bytes: the draft block whose size decides
+// whether its rows are streamed past the caches (0: this call's block).
 hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int d,
                           uint64_t seed, const int32_t* kcur, const uint32_t* rcur,
                           const int32_t* crow_cur, const int32_t* cstep_cur, int32_t* knext,
@@ -171,7 +189,8 @@ hipError_t advance_launch(const Sched& sc, const float4* coef, int B, int K, int
                           const float* rsig, float* x, float* sv, const float* mq, float* y,
                           int32_t* step, double* sigma, int32_t* hist, int64_t* steps,
                           int* act_next, int32_t* trace, int r, int trace_rounds, bool frozen,
-                          hipStream_t s, const int* gate);
+                          hipStream_t s, const int* gate, int chain0 = 0, int trace_ld = 0,
+                          int64_t stream_bytes = 0);
 
 // ---------------------------------------------------------------- kernels --
 hipError_t init_chains_launch(int B, int d, uint64_t seed, float* y, float* x0, int64_t x0c,
@@ -187,7 +206,8 @@ hipError_t draft_cached_launch(const Sched& sc, const float4* coef, int B, int K
                                const int32_t* crow, const int32_t* cstep, const float* mqprev,
                                sd_stride mqs, const int32_t* k, const uint32_t* rnd,
                                uint64_t seed, float* x, sd_stride xs, float* sv,
-                               hipStream_t s, const int* gate);
+                               hipStream_t s, const int* gate, int chain0 = 0,
+                               int64_t stream_bytes = 0);
 hipError_t verify_launch(int B, int K, int d, int mode, const float* yd, sd_stride ys,
                          const float* mp, sd_stride mps, const float* mq, sd_stride mqs,
                          const double* sigma, const int32_t* kb, const uint32_t* rnd,
@@ -218,6 +238,10 @@ hipError_t residual_commit_launch(int B, int K, int d, int N, const float* yd, s
                                   int32_t* crow, int32_t* cstep, int32_t* adv, int32_t* trace,
                                   int r, int trace_rounds, hipStream_t s, const int* gate);
 hipError_t fill_i32_launch(int32_t* p, int64_t n, int32_t v, hipStream_t s);
+// *f0 = 1 if a chain of [0, split) has k < N, else 0; *f1 the same for
+// [split, B) (one workgroup).
+hipError_t chains_active_launch(int B, int split, int N, const int32_t* k, int* f0, int* f1,
+                                hipStream_t s);
 hipError_t fill_i64_launch(int64_t* p, int64_t n, int64_t v, hipStream_t s);
 hipError_t prepare_launch(const Sched& sc, int B, int K, const int32_t* k, int32_t* kb,
                           int32_t* left, int32_t* step, double* sigma, int32_t* tau,

@@ -44,7 +44,7 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(
     const float* __restrict__ mqprev, int64_t qc, int64_t qr, const int32_t* __restrict__ kk,
     const uint32_t* __restrict__ rnd, uint64_t seed, float* __restrict__ x, int64_t xc,
     int64_t xr, float* __restrict__ mp, int64_t mc, int64_t mr, float* __restrict__ svout,
-    bool vec_ok, bool stream, const int* gate) {
+    bool vec_ok, bool stream, const int* gate, int chain0) {
   if (gate && *gate == 0) return;
   const int b = blockIdx.y;
   const int g = blockIdx.x * kThreads + threadIdx.x;
@@ -75,8 +75,8 @@ __global__ __launch_bounds__(kThreads) void draft_kernel(
     load4(cs + (int64_t)b * d + e0, cnt, vec, sv);
   }
   store4(xb, cnt, vec, yv, stream);
-  draft_rows(sc, coef, K, k, kb, (uint32_t)b, r, seed, g, yv, sv, scale, xb, xr, mb, mr, cnt, vec,
-             stream);
+  draft_rows(sc, coef, K, k, kb, (uint32_t)(chain0 + b), r, seed, g, yv, sv, scale, xb, xr, mb, mr,
+             cnt, vec, stream);
 }
 
 // One thread per chain, at the start of a round:
@@ -132,6 +132,29 @@ __global__ void fill_i32_kernel(int32_t* p, int64_t n, int32_t v) {
   if (i < n) p[i] = v;
 }
 
+__global__ __launch_bounds__(kThreads) void chains_active_kernel(int B, int split, int N,
+                                                                const int32_t* __restrict__ k,
+                                                                int* f0, int* f1) {
+  __shared__ int any[2];
+  if (threadIdx.x < 2) any[threadIdx.x] = 0;
+  __syncthreads();
+  int a0 = 0, a1 = 0;
+  for (int b = threadIdx.x; b < B; b += kThreads) {
+    const int on = k[b] < N ? 1 : 0;
+    if (b < split)
+      a0 |= on;
+    else
+      a1 |= on;
+  }
+  if (a0) atomicOr(&any[0], 1);
+  if (a1) atomicOr(&any[1], 1);
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    *f0 = any[0];
+    *f1 = any[1];
+  }
+}
+
 __global__ void fill_i64_kernel(int64_t* p, int64_t n, int64_t v) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) p[i] = v;
@@ -182,7 +205,7 @@ hipError_t draft_launch(const Sched& sc, int B, int K, int d, const float* y, co
   return timed("draft_block", s, [&] {
     draft_kernel<false><<<grid, kThreads, 0, s>>>(sc, nullptr, K, d, y, cs, nullptr, nullptr, nullptr, 0, 0,
                                                   k, rnd, seed, x, xs.chain, xs.row, mp, mps.chain,
-                                                  mps.row, nullptr, vec, stream, gate);
+                                                  mps.row, nullptr, vec, stream, gate, 0);
   });
 }
 
@@ -191,16 +214,17 @@ hipError_t draft_cached_launch(const Sched& sc, const float4* coef, int B, int K
                                const int32_t* crow, const int32_t* cstep, const float* mqprev,
                                sd_stride mqs, const int32_t* k, const uint32_t* rnd,
                                uint64_t seed, float* x, sd_stride xs, float* sv,
-                               hipStream_t s, const int* gate) {
+                               hipStream_t s, const int* gate, int chain0, int64_t stream_bytes) {
   const int ng = (d + 3) / 4;
   dim3 grid((ng + kThreads - 1) / kThreads, B);
   const bool vec = draft_vec(d, xs, sd_stride{d, d}, y, x, sv) && aligned16(mqprev) &&
                    mqs.chain % 4 == 0 && mqs.row % 4 == 0;
-  const bool stream = stream_rows((int64_t)B * (K + 1) * d * 4);
+  const bool stream = stream_rows(stream_bytes > 0 ? stream_bytes : (int64_t)B * (K + 1) * d * 4);
   return timed("draft_block", s, [&] {
     draft_kernel<true><<<grid, kThreads, 0, s>>>(sc, coef, K, d, y, nullptr, crow, cstep, mqprev,
                                                  mqs.chain, mqs.row, k, rnd, seed, x, xs.chain,
-                                                 xs.row, nullptr, 0, 0, sv, vec, stream, gate);
+                                                 xs.row, nullptr, 0, 0, sv, vec, stream, gate,
+                                                 chain0);
   });
 }
 
@@ -219,6 +243,12 @@ hipError_t fill_i32_launch(int32_t* p, int64_t n, int32_t v, hipStream_t s) {
   if (n <= 0) return hipSuccess;
   const int64_t nb = (n + 255) / 256;
   fill_i32_kernel<<<(unsigned)nb, 256, 0, s>>>(p, n, v);
+  return hipGetLastError();
+}
+
+hipError_t chains_active_launch(int B, int split, int N, const int32_t* k, int* f0, int* f1,
+                                hipStream_t s) {
+  chains_active_kernel<<<1, kThreads, 0, s>>>(B, split, N, k, f0, f1);
   return hipGetLastError();
 }
 

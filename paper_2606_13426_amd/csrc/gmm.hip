@@ -620,7 +620,8 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     const uint16_t* __restrict__ muTs, const float* __restrict__ X,
     const float* __restrict__ rowc, const float* __restrict__ SV,
     const int32_t* __restrict__ cstep, const float4* __restrict__ coef, float* __restrict__ mq,
-    double* __restrict__ lrp, const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
+    double* __restrict__ lrp, const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate,
+    int chain0) {
   if (gate && *gate == 0) return;
   __shared__ TileLds sm;
   __shared__ float rc[3 * TILE];
@@ -736,7 +737,7 @@ __global__ __launch_bounds__(kThreads) void gmm_mean_lr_kernel(
     const int e = threadIdx.x + kThreads * u;
     if (e < nchain * 16)
       *reinterpret_cast<float4*>(&sm.b[(e >> 4) * LDW + 4 * (e & 15)]) =
-          normals4(philox((uint32_t)((c0 >> 2) + (e & 15)), (uint32_t)(b_first + (e >> 4)), rn[u],
+          normals4(philox((uint32_t)((c0 >> 2) + (e & 15)), (uint32_t)(chain0 + b_first + (e >> 4)), rn[u],
                           TAG_RESID << 24, seed));
   }
   __syncthreads();
@@ -906,11 +907,13 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // number of splits minimise (rounds of workgroups over 512 slots, two per
 // compute unit) x (chunks per workgroup), i.e. the critical path, preferring
 // fewer splits on ties.
-Plan make_plan(const Target& t, int R) {
+// Buffers for R rows; the split is chosen for plan_rows rows (0: R).
+Plan make_plan(const Target& t, int R, int plan_rows = 0) {
   Plan p{};
   // the aligned path's tiles (kSplitRows rows, two workgroups per compute
   // unit); the unaligned kernel takes the same splits
-  const int tiles = ((R + kSplitRows - 1) / kSplitRows) * ((t.M + TILE - 1) / TILE);
+  const int Rp = plan_rows > 0 ? plan_rows : R;
+  const int tiles = ((Rp + kSplitRows - 1) / kSplitRows) * ((t.M + TILE - 1) / TILE);
   const int nchunks = (t.d + KC - 1) / KC;
   constexpr int kSlots = 512, kMaxSplits = 32;
   int best_cost = 1 << 30, best_per = nchunks;
@@ -956,8 +959,9 @@ hipError_t logits_launch(const Target& t, const Plan& p, int R, const float* x, 
 
 }  // namespace
 
-size_t target_ws_bytes(const Target& t, int rows) {
-  return t.prec == SD_BF16 ? target_ws_bytes_bf16(t, rows) : make_plan(t, rows).total;
+size_t target_ws_bytes(const Target& t, int rows, int plan_rows) {
+  return t.prec == SD_BF16 ? target_ws_bytes_bf16(t, rows, plan_rows)
+                           : make_plan(t, rows, plan_rows).total;
 }
 
 hipError_t gmm_softmax_launch(const Target& t, int R, int S, const float* part, const double* xsq,
@@ -1005,10 +1009,12 @@ hipError_t gmm_softmax_launch(const Target& t, int R, int S, const float* part, 
 
 hipError_t target_mean_launch(const Target& t, int R, const float* x, int64_t ldx,
                               const int32_t* step, float* mq, int64_t ldq, float* score,
-                              int64_t lds, void* ws, hipStream_t s, const int* gate) {
+                              int64_t lds, void* ws, hipStream_t s, const int* gate,
+                              int plan_rows) {
   if (t.prec == SD_BF16)
-    return target_mean_bf16_launch(t, R, x, ldx, step, mq, ldq, score, lds, ws, s, gate);
-  const Plan p = make_plan(t, R);
+    return target_mean_bf16_launch(t, R, x, ldx, step, mq, ldq, score, lds, ws, s, gate,
+                                   plan_rows);
+  const Plan p = make_plan(t, R, plan_rows);
   char* base = static_cast<char*>(ws);
   float* part = reinterpret_cast<float*>(base + p.off_part);
   double* xsq = reinterpret_cast<double*>(base + p.off_xsq);
@@ -1030,11 +1036,12 @@ hipError_t target_mean_launch(const Target& t, int R, const float* x, int64_t ld
 hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
                                  const int32_t* step, float* mq, const float* sv,
                                  const int32_t* cstep, double* lrp, const uint32_t* rnd,
-                                 uint64_t seed, void* ws, hipStream_t s, const int* gate) {
+                                 uint64_t seed, void* ws, hipStream_t s, const int* gate,
+                                 int plan_rows, int chain0) {
   if (t.prec == SD_BF16)
     return target_mean_lr_bf16_launch(t, R, K1, x, step, mq, sv, cstep, lrp, rnd, seed, ws, s,
-                                      gate);
-  const Plan p = make_plan(t, R);
+                                      gate, plan_rows, chain0);
+  const Plan p = make_plan(t, R, plan_rows);
   char* base = static_cast<char*>(ws);
   float* part = reinterpret_cast<float*>(base + p.off_part);
   double* xsq = reinterpret_cast<double*>(base + p.off_xsq);
@@ -1052,7 +1059,7 @@ hipError_t target_mean_lr_launch(const Target& t, int R, int K1, const float* x,
                    (int64_t)(TILE + 2) * t.d * 4 < ((int64_t)1 << 31) && t.M < 1 << 22;
   return launch_timed("gmm_mean_lr", vec ? gmm_mean_lr_kernel<true> : gmm_mean_lr_kernel<false>, g2,
                       dim3(kThreads), s, R, t.M, t.d, K1, P, t.muT,
-                      t.muT_split, x, rowc, sv, cstep, t.coef, mq, lrp, rnd, seed, gate);
+                      t.muT_split, x, rowc, sv, cstep, t.coef, mq, lrp, rnd, seed, gate, chain0);
 }
 
 int lr_tiles(const Target& t, int K1) {

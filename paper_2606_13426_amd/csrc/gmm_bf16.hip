@@ -271,7 +271,7 @@ __device__ __forceinline__ void mean_lr_epilogue_vec(
     float* stg, float* gz, const float* cscale, const float* rc, const f32x16 (&acc)[2][2], int R,
     int d, int K1, int r0, int c0, int ct, int nct, int b_first, int nchain,
     const float* __restrict__ X, const float* __restrict__ SV, float* __restrict__ mq,
-    double* __restrict__ lrp, const uint32_t* __restrict__ rnd, uint64_t seed) {
+    double* __restrict__ lrp, const uint32_t* __restrict__ rnd, uint64_t seed, int chain0) {
   const int cg = threadIdx.x & 15, lr0 = 8 * (threadIdx.x >> 4);
   const int B = R / K1;
   const __amdgpu_buffer_rsrc_t vx = buf_view(X + (int64_t)r0 * d, (int64_t)min(R - r0, TM + 1) * d * 4);
@@ -305,7 +305,7 @@ __device__ __forceinline__ void mean_lr_epilogue_vec(
       if (e < nchain * 16) {
         const int tcol = c0 + epi_col(e & 15, p);
         *reinterpret_cast<float4*>(&gz[(e >> 4) * LDO + 4 * (e & 15)]) =
-            normals4(philox((uint32_t)(tcol >> 2), (uint32_t)(b_first + (e >> 4)), rn[u],
+            normals4(philox((uint32_t)(tcol >> 2), (uint32_t)(chain0 + b_first + (e >> 4)), rn[u],
                             TAG_RESID << 24, seed));
       }
     }
@@ -371,7 +371,7 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
     const uint16_t* __restrict__ muT, const float* __restrict__ X, const float* __restrict__ rowc,
     const float* __restrict__ SV, const int32_t* __restrict__ cstep,
     const float4* __restrict__ coef, float* __restrict__ mq, double* __restrict__ lrp, bool vecd,
-    const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
+    const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate, int chain0) {
   if (gate && *gate == 0) return;
   __shared__ OperandLds sm[2];
   __shared__ float rc[3 * TM];
@@ -398,7 +398,7 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
   if ((int)threadIdx.x < nchain) cscale[threadIdx.x] = coef[csi].w;
   if constexpr (VEC) {
     mean_lr_epilogue_vec(stg, gz, cscale, rc, acc, R, d, K1, r0, c0, ct, nct, b_first, nchain, X,
-                         SV, mq, lrp, rnd, seed);
+                         SV, mq, lrp, rnd, seed, chain0);
     return;
   }
   double t2 = 0.0, tz = 0.0, tg = 0.0;  // this lane's row (see reduce_rows16), both passes
@@ -412,7 +412,7 @@ __global__ __launch_bounds__(kThreads, 2) void gmm_mean_lr_bf16_kernel(
       const int cl = e >> 4, gq = e & 15;
       const int bb = b_first + cl;
       const int tcol = c0 + epi_col(gq, p);
-      const float4 z = normals4(philox((uint32_t)(tcol >> 2), (uint32_t)bb, rnd[bb],
+      const float4 z = normals4(philox((uint32_t)(tcol >> 2), (uint32_t)(chain0 + bb), rnd[bb],
                                        TAG_RESID << 24, seed));
       *reinterpret_cast<float4*>(&gz[cl * LDO + 4 * gq]) = z;
     }
@@ -536,7 +536,7 @@ __global__ __launch_bounds__(T::kThreads, T::TC == 128 ? 2 : 1) void gmm_mean_lr
     const uint16_t* __restrict__ muT, const float* __restrict__ X, const float* __restrict__ rowc,
     const float* __restrict__ SV, const int32_t* __restrict__ cstep,
     const float4* __restrict__ coef, float* __restrict__ mq, double* __restrict__ lrp,
-    const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate) {
+    const uint32_t* __restrict__ rnd, uint64_t seed, const int* gate, int chain0) {
   using bf16b::CB;
   using bf16b::RB;
   using bf16b::TR;
@@ -604,7 +604,7 @@ __global__ __launch_bounds__(T::kThreads, T::TC == 128 ? 2 : 1) void gmm_mean_lr
   double* part = reinterpret_cast<double*>(svs + NCH * GS);
   for (int e = threadIdx.x; e < nchain * (TC / 4); e += T::kThreads) {
     const int cl = e / (TC / 4), g4 = e % (TC / 4);
-    const float4 z = normals4(philox((uint32_t)((c0 >> 2) + g4), (uint32_t)(b_first + cl), crnd[cl],
+    const float4 z = normals4(philox((uint32_t)((c0 >> 2) + g4), (uint32_t)(chain0 + b_first + cl), crnd[cl],
                                      TAG_RESID << 24, seed));
     *reinterpret_cast<float4*>(&gz[cl * GS + 4 * g4]) = z;
     *reinterpret_cast<float4*>(&svs[cl * GS + 4 * g4]) = buf_ld4(vs, (uint32_t)((cl * d + c0 + 4 * g4) * 4));
@@ -721,12 +721,14 @@ inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 // x (chunks per workgroup), over 256 slots of one 256 x 256 workgroup per
 // compute unit when d is a whole number of chunks, else over 512 slots of two
 // 128 x 128 workgroups per compute unit.
-Plan make_plan(const Target& t, int R) {
+// Buffers for R rows; the split over d is chosen for plan_rows rows (0: R).
+Plan make_plan(const Target& t, int R, int plan_rows = 0) {
   Plan p{};
   p.wide = t.d % KC == 0;
   const int tm = p.wide ? bf16w::WT : TM, tn = p.wide ? bf16w::WT : TN;
   const int slots = p.wide ? 256 : 512;
-  const int tiles = ((R + tm - 1) / tm) * ((t.M + tn - 1) / tn);
+  const int Rp = plan_rows > 0 ? plan_rows : R;
+  const int tiles = ((Rp + tm - 1) / tm) * ((t.M + tn - 1) / tn);
   const int nchunks = (t.d + KC - 1) / KC;
   int best_cost = 1 << 30, best_per = nchunks;
   for (int S = 1; S <= 8 && S <= nchunks; ++S) {
@@ -791,12 +793,15 @@ hipError_t logits_and_softmax(const Target& t, const Plan& p, const Bufs& w, int
 
 }  // namespace
 
-size_t target_ws_bytes_bf16(const Target& t, int rows) { return make_plan(t, rows).total; }
+size_t target_ws_bytes_bf16(const Target& t, int rows, int plan_rows) {
+  return make_plan(t, rows, plan_rows).total;
+}
 
 hipError_t target_mean_bf16_launch(const Target& t, int R, const float* x, int64_t ldx,
                                    const int32_t* step, float* mq, int64_t ldq, float* score,
-                                   int64_t lds, void* ws, hipStream_t s, const int* gate) {
-  const Plan p = make_plan(t, R);
+                                   int64_t lds, void* ws, hipStream_t s, const int* gate,
+                                   int plan_rows) {
+  const Plan p = make_plan(t, R, plan_rows);
   const Bufs w = carve(p, ws);
   const bool vecx = (ldx % 4 == 0) && aligned16(x);
   hipError_t e = logits_and_softmax(t, p, w, R, x, ldx, vecx, step, s, gate);
@@ -819,8 +824,9 @@ hipError_t target_mean_bf16_launch(const Target& t, int R, const float* x, int64
 hipError_t target_mean_lr_bf16_launch(const Target& t, int R, int K1, const float* x,
                                       const int32_t* step, float* mq, const float* sv,
                                       const int32_t* cstep, double* lrp, const uint32_t* rnd,
-                                      uint64_t seed, void* ws, hipStream_t s, const int* gate) {
-  const Plan p = make_plan(t, R);
+                                      uint64_t seed, void* ws, hipStream_t s, const int* gate,
+                                      int plan_rows, int chain0) {
+  const Plan p = make_plan(t, R, plan_rows);
   const Bufs w = carve(p, ws);
   const bool vecd = (t.d % 4 == 0) && aligned16(x) && aligned16(mq) && aligned16(sv);
   hipError_t e = logits_and_softmax(t, p, w, R, x, t.d, vecd, step, s, gate);
@@ -835,7 +841,7 @@ hipError_t target_mean_lr_bf16_launch(const Target& t, int R, int K1, const floa
     return launch_timed("gmm_mean_lr_bf16", gmm_mean_lr_bf16_big_kernel<MeanTile>,
                         dim3(((B + CT - 1) / CT) * (t.d / MeanTile::TC)), dim3(MeanTile::kThreads), s, R,
                         t.M, t.d, K1, CT, w.P, t.muT16, x, w.rowc, sv, cstep, t.coef, mq, lrp, rnd,
-                        seed, gate);
+                        seed, gate, chain0);
   }
   dim3 g2((t.d + TN - 1) / TN, (R + TM - 1) / TM);
   // the buffer path: whole chunks of M, whole tiles of d, aligned rows, at
@@ -845,7 +851,7 @@ hipError_t target_mean_lr_bf16_launch(const Target& t, int R, int K1, const floa
   return launch_timed("gmm_mean_lr_bf16",
                       vec ? gmm_mean_lr_bf16_kernel<true> : gmm_mean_lr_bf16_kernel<false>, g2,
                       dim3(kThreads), s, R, t.M, t.d, K1, w.P, t.muT16, x, w.rowc, sv, cstep, t.coef,
-                      mq, lrp, vecd, rnd, seed, gate);
+                      mq, lrp, vecd, rnd, seed, gate, chain0);
 }
 
 int lr_tiles_bf16(const Target& t, int K1) {

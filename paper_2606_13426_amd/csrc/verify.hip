@@ -331,7 +331,7 @@ __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
     int32_t* __restrict__ tau, int32_t* __restrict__ rmode,
     float* __restrict__ rcoef, float* __restrict__ rsig, uint64_t* __restrict__ coins,
     double* __restrict__ lar, double* __restrict__ ures, int32_t* __restrict__ ties,
-    int* nanflag, int* act_next, int* host_prev, int pub_round, const int* gate) {
+    int* nanflag, int* act_next, int* host_prev, int pub_round, const int* gate, int chain0) {
   if (blockIdx.x == 0 && threadIdx.x == 0) {
     *act_next = 0;
     if (host_prev) {
@@ -402,7 +402,8 @@ __global__ __launch_bounds__(kThreads) void scan_fused_kernel(
   const double ell = valid ? -sz * inv - 0.5 * s2 * inv : 0.0;
   if (__ballot(valid && !(isfinite(ell) && isfinite(vn))) != 0ull && lane == 0) atomicOr(nanflag, 1);
   const uint32_t r = rcur[b];
-  const Decision D = decide(mode, umode, kb, ell, vn, (uint32_t)b, r, seed, lane, w2, !reflect);
+  const Decision D = decide(mode, umode, kb, ell, vn, (uint32_t)(chain0 + b), r, seed, lane, w2,
+                            !reflect);
   const int t = D.tau;
   int rm;
   float cf = 0.f, sgo = 0.f;
@@ -467,12 +468,12 @@ hipError_t scan_fused_launch(int B, int K, int d, int N, int mode, int umode, co
                              int32_t* tau, int32_t* rmode, float* rcoef, float* rsig,
                              uint64_t* coins, double* lar, double* ures, int32_t* ties,
                              int* nanflag, int* act_next, int* host_prev, int pub_round,
-                             hipStream_t s, const int* gate) {
+                             hipStream_t s, const int* gate, int chain0) {
   const int per = kThreads / 64;
   return launch_timed("scan_fused", scan_fused_kernel, dim3((B + per - 1) / per), dim3(kThreads), s,
                       B, K, d, N, mode, umode, lrp, nct, sigma, kcur, rcur, seed, w2, reflect, tau,
                       rmode, rcoef, rsig, coins, lar, ures, ties, nanflag, act_next, host_prev,
-                      pub_round, gate);
+                      pub_round, gate, chain0);
 }
 
 }  // namespace sd

@@ -45,7 +45,7 @@ def test_exports_every_declared_symbol(lib):
 
 
 def test_abi_version(lib):
-    assert _lib.sd_abi_version() == 3
+    assert _lib.sd_abi_version() == 4
 
 
 def _expect_einval(status, needle):
