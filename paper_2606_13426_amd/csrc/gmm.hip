@@ -382,7 +382,8 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_kernel(
 // power of two, 16 .. 256) with four consecutive components per lane, so
 // every per-component input is one 16-byte load per lane (one per split for
 // the logit partials) and a workgroup holds 256 / G rows.  Arithmetic as in
-// gmm_softmax_kernel; the max, the sum and rho are reduced over the G lanes
+// gmm_softmax_kernel; the max, then the normaliser sum_m e_m together with
+// sum_m e_m / s2_m (rho is their ratio), are reduced over the G lanes
 // (shuffles within a wavefront, then LDS across the wavefronts of a row).
 template <int G>
 __device__ __forceinline__ double group_reduce(double v, bool is_max, double* red) {
@@ -405,6 +406,34 @@ __device__ __forceinline__ double group_reduce(double v, bool is_max, double* re
   return v;
 }
 
+// Both sums of v over the G lanes of a row, as group_reduce.
+template <int G>
+__device__ __forceinline__ double2 group_sum2(double2 v, double* red) {
+  constexpr int W = G < 64 ? G : 64;
+#pragma unroll
+  for (int o = W / 2; o > 0; o >>= 1) {
+    v.x += __shfl_xor(v.x, o);
+    v.y += __shfl_xor(v.y, o);
+  }
+  if constexpr (G > 64) {
+    constexpr int NW = G / 64;
+    const int w = threadIdx.x >> 6, w0 = w - w % NW;
+    __syncthreads();  // the previous use of red is complete
+    if ((threadIdx.x & 63) == 0) {
+      red[2 * w] = v.x;
+      red[2 * w + 1] = v.y;
+    }
+    __syncthreads();
+    v = make_double2(red[2 * w0], red[2 * w0 + 1]);
+#pragma unroll
+    for (int i = 1; i < NW; ++i) {
+      v.x += red[2 * (w0 + i)];
+      v.y += red[2 * (w0 + i) + 1];
+    }
+  }
+  return v;
+}
+
 template <int G, class TP>
 __global__ __launch_bounds__(kThreads) void gmm_softmax_quad_kernel(
     int R, int M, int d, int S, const float* __restrict__ part, const double* __restrict__ xsq,
@@ -413,7 +442,7 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_quad_kernel(
     TP* __restrict__ P, float* __restrict__ rowc, const int* gate) {
   static_assert(G >= 16 && G <= kThreads && (G & (G - 1)) == 0, "G: a power of two in 16..256");
   if (gate && *gate == 0) return;
-  __shared__ double red[kThreads / 64];
+  __shared__ double red[2 * (kThreads / 64)];
   constexpr int RPW = kThreads / G;
   const int gl = threadIdx.x % G;
   const int row = blockIdx.x * RPW + (int)threadIdx.x / G;
@@ -456,20 +485,19 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_quad_kernel(
   mx = group_reduce<G>(mx, true, red);
   float e[4];
   float sum = 0.0f;
+  double sum_is2 = 0.0;
 #pragma unroll
   for (int c = 0; c < 4; ++c) {
     e[c] = has ? __expf((float)(lg[c] - mx)) : 0.0f;
     sum += e[c];
+    sum_is2 += (double)e[c] * t[c].y;
   }
-  const double inv = 1.0 / group_reduce<G>((double)sum, false, red);
-  double rho = 0.0;
+  const double2 tot = group_sum2<G>(make_double2((double)sum, sum_is2), red);
+  const double inv = 1.0 / tot.x;
+  const double rho = tot.y * inv;
   float pm[4];
 #pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const double rm = (double)e[c] * inv;
-    pm[c] = (float)(rm * a * t[c].y);
-    rho += rm * t[c].y;
-  }
+  for (int c = 0; c < 4; ++c) pm[c] = (float)((double)e[c] * inv * a * t[c].y);
   if (on && has) {
     if constexpr (sizeof(TP) == 2) {
       uint2 pk;
@@ -482,7 +510,6 @@ __global__ __launch_bounds__(kThreads) void gmm_softmax_quad_kernel(
       *reinterpret_cast<float4*>(P + (int64_t)row * M + m0) = make_float4(pm[0], pm[1], pm[2], pm[3]);
     }
   }
-  rho = group_reduce<G>(rho, false, red);
   if (on && gl == 0) {
     const float4 cf = coef[n];
     rowc[3 * (int64_t)row + 0] = cf.x;
