@@ -10,7 +10,10 @@ chain-steps per second = B * N / seconds per run.
 
 Per-kernel durations are measured live with HIP events on the launch's
 stream; the dominant kernel's roofline uses its algorithmic work (see
-algorithmic_work) over its measured time.  The pixel-sized float32 workload
+algorithmic_work) over its measured time.  Runs use the library's choice of
+chain groups (config.chain_groups); where it runs two concurrent groups, the
+per-kernel times and the roofline come from extra one-group runs of the same
+workload (roofline.chain_groups), since concurrent kernels share the GPU.  The pixel-sized float32 workload
 (with token verification), the 64x64x3 pixel workload, the
 verification-only workload (B = 4096, K = 32, d = 12288) and the paper's
 variants are extra fields; the CPU oracle is timed on a bounded sample of
@@ -35,18 +38,18 @@ METRIC = "verified chain-steps/sec + mean accepted steps per block; % MFMA / HBM
 
 # HBM bytes per launch of a workload's dominant kernel from two rocprofv3 passes
 # (FETCH_SIZE x 2.000 and WRITE_SIZE x 1.000, the factors a 1 GiB device copy
-# gives; profiles/sampler_pixel3072_hbm_traffic.md), valid while the kernel's
+# gives; profiles/sampler_latent16384_hbm_traffic.md), valid while the kernel's
 # sources (its translation unit, every library header and the C header) have
 # the digest (source_digest(unit)) recorded with them.
 PROFILE_EVERY = 4  # the timed runs' event sample of the dominant kernel's launches
 
 MEASURED_TRAFFIC = {
     ("verify12288", "logratio_reduce"): dict(bytes=(19344.1 + 8.5) * 1e6, unit="verify.hip",
-                                             sources="ea7ba0139a0bc5b69f3731957c94da1a81dfb8b2"),
+                                             sources="994e60dc80823bc02a857b7324bb96cc2088c940"),
     ("pixel3072", "gmm_mean_lr"): dict(bytes=(136.1 + 122.0) * 1e6, unit="gmm.hip",
-                                       sources="f3e06c62cf09a8fbf8101f1fe1e515fc20c93769"),
+                                       sources="7c311dd038d208c89e208709599b6df483f832b8"),
     ("latent16384", "gmm_mean_lr_bf16"): dict(bytes=(277.7 + 154.0) * 1e6, unit="gmm_bf16.hip",
-                                              sources="2d6a90c33c9ca8b85d501d6e9f496200d045a0c5"),
+                                              sources="e28ede5c02304c49847bdeaacecac95027894518"),
 }
 
 
@@ -145,7 +148,14 @@ def roof_entry(flops, nbytes, ms, eb):
                 frac=t_hbm / sec, algorithmic_flops=flops, algorithmic_bytes=nbytes)
 
 
-def run_sampler_bench(lib, name, mode, steps, warmup, profile):
+def run_sampler_bench(lib, name, mode, steps, warmup, profile, groups_req=0):
+    """Whole sampler runs on the workload (Y_0 to Y_N) with the library's
+    choice of chain groups: the seconds per run.  With profile, also the
+    per-kernel breakdown of one profiled run and live HIP-event times of a
+    systematic sample of the dominant kernel's launches over `steps` timed
+    runs -- in the same timed runs when the sampler runs one chain group, else
+    in `steps` extra runs with one group (the kernels of two concurrent groups
+    share the GPU, so their event durations would not be the kernels' own)."""
     import torch
     from paper_2606_13426_amd.inputs import WORKLOADS, workload_gmm
     cfg = WORKLOADS[name]
@@ -156,50 +166,69 @@ def run_sampler_bench(lib, name, mode, steps, warmup, profile):
     ws = torch.empty(lib.sd_sampler_workspace(tgt, B, K), dtype=torch.uint8, device="cuda")
     y = torch.empty(B, d, dtype=torch.float32, device="cuda")
     seed = 0
-    breakdown, only = {}, None
-    nw = max(warmup, 2 if profile else 0)
-    for w in range(nw):
-        last = w == nw - 1
-        if profile and last:
-            # the last (profiled) warm-up run gives the per-kernel breakdown and
-            # names the dominant kernel; the timed runs then bracket only it
-            lib.sd_profile_only(None)
-            lib.sd_profile_enable(True)
-        lib.sd_run_sampler(tgt, B, K, seed, mode=mode, y_out=y, ws=ws)
-        if profile and last:
-            breakdown = lib.sd_profile_read()
-            lib.sd_profile_enable(False)
-            only = max(breakdown, key=lambda n: breakdown[n][1])
+
+    def run(groups, trace_rounds=0):
+        return lib.sd_run_sampler_ex(tgt, B, K, seed, mode=mode, y_out=y, ws=ws, groups=groups,
+                                     trace_rounds=trace_rounds)
+
+    for _ in range(max(warmup, 1)):
+        _, st_w, _ = run(groups_req)
     torch.cuda.synchronize()
-    if profile:
-        # the timed runs bracket every PROFILE_EVERY-th launch of the dominant
-        # kernel: a systematic sample over the timed region whose events cost
-        # the stream a quarter of what timing every launch does
-        lib.sd_profile_only(only)
+    groups = st_w["groups"]
+    prof_groups = 1  # the grouping of the profiled runs
+
+    def profile_begin():
+        # one profiled run gives the per-kernel breakdown and names the
+        # dominant kernel; the timed runs then bracket every PROFILE_EVERY-th
+        # launch of it: a systematic sample whose events cost the stream a
+        # quarter of what timing every launch does
+        lib.sd_profile_only(None)
+        lib.sd_profile_enable(True)
+        run(prof_groups)
+        bd = lib.sd_profile_read()
+        lib.sd_profile_enable(False)
+        dom = max(bd, key=lambda n: bd[n][1])
+        torch.cuda.synchronize()
+        lib.sd_profile_only(dom)
         lib.sd_profile_every(PROFILE_EVERY)
         lib.sd_profile_enable(True)
+        return bd, dom
+
+    def profile_end(dom):
+        p, n = lib.sd_profile_read(), lib.sd_profile_seen(dom)
+        lib.sd_profile_enable(False)
+        lib.sd_profile_only(None)
+        lib.sd_profile_every(1)
+        return p, n
+
+    breakdown, only, prof, seen = {}, None, {}, 0
+    live = profile and groups == prof_groups
+    if live:
+        breakdown, only = profile_begin()
     stats = []
     t0 = time.perf_counter()
     for s in range(steps):
-        _, st, trace = lib.sd_run_sampler(tgt, B, K, seed, mode=mode, y_out=y, ws=ws,
-                                          trace_rounds=N if s == 0 else 0)
+        _, st, trace = run(groups_req, trace_rounds=N if s == 0 else 0)
         stats.append(st)
         if s == 0:
             trace0 = trace.cpu().numpy()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    prof = lib.sd_profile_read() if profile else {}
-    seen = lib.sd_profile_seen(only) if profile else 0
-    if profile:
-        lib.sd_profile_enable(False)
-        lib.sd_profile_only(None)
-        lib.sd_profile_every(1)
+    if live:
+        prof, seen = profile_end(only)
+    elif profile:
+        breakdown, only = profile_begin()
+        for _ in range(steps):
+            run(prof_groups)
+        torch.cuda.synchronize()
+        prof, seen = profile_end(only)
     sec = (t1 - t0) / steps
     st = stats[0]
     be = st["steps"] / st["chain_rounds"]
     act, rows_v, rows_t = _counts_from_trace(trace0, N, K)
     return dict(B=B, K=K, N=N, d=d, M=M, sec=sec, be=be, rounds=st["rounds"], prof=prof, seen=seen,
-                mean_tau=st["mean_tau"], ties=st["ties"],
+                mean_tau=st["mean_tau"], ties=st["ties"], groups=groups,
+                profile_groups=prof_groups if profile else None,
                 breakdown=breakdown,
                 act=act, rows_verified=rows_v, rows_target=rows_t, tau_hist=st["tau_hist"][: K + 2],
                 steps=steps)
@@ -305,9 +334,10 @@ def variants_bench(lib, name, steps):
         lib.sd_profile_enable(False)
         return prof
 
-    def sampler(mode, residual, drafter, omega, trace_rounds=0):
+    def sampler(mode, residual, drafter, omega, trace_rounds=0, groups=0):
         return lambda: lib.sd_run_sampler_ex(tgt, B, K, seed, mode=mode, residual=residual, drafter=drafter,
-                                             omega=omega, y_out=y, ws=ws, trace_rounds=trace_rounds)
+                                             omega=omega, y_out=y, ws=ws, trace_rounds=trace_rounds,
+                                             groups=groups)
 
     reps = max(2, steps // 3)
     kinds = {"R": (lib.SD_TOKEN, lib.SD_RESIDUAL_REFLECTION), "D": (lib.SD_TOKEN, lib.SD_RESIDUAL_DECOMPOSITION),
@@ -331,8 +361,10 @@ def variants_bench(lib, name, steps):
     em_prof = profiled(lambda: lib.sd_run_plain_em(tgt, B, seed, y_out=y, ws=em_ws))
     # speedup terms, per round of the block sampler (Free and Frozen) and per EM step
     tq1 = 1e3 * sum(v[1] for k, v in em_prof.items() if k.startswith("gmm_")) / N   # us per target call on B rows
-    free_prof = profiled(sampler(lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FREE, 1.0))
-    frz_prof = profiled(sampler(lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FROZEN, 1.0))
+    # (one chain group: a round's kernels then run one after another, so
+    # their event times add up to the round)
+    free_prof = profiled(sampler(lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FREE, 1.0, groups=1))
+    frz_prof = profiled(sampler(lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FROZEN, 1.0, groups=1))
     _, (_, _, trace) = timed_runs(sampler(lib.SD_BLOCK, lib.SD_RESIDUAL_DECOMPOSITION, lib.SD_DRAFTER_FREE,
                                           1.0, trace_rounds=N), 1)
     be_curve = _be_by_step(trace.cpu().numpy(), N)
@@ -563,6 +595,8 @@ def main():
     ap.add_argument("--variants-workload", default="pixel3072",
                     help="workload of the variants field (the paper's R/D/B table, Frozen Drafter, plain EM)")
     ap.add_argument("--no-extra", action="store_true", help="skip the token and verification-only runs")
+    ap.add_argument("--groups", dest="groups_req", type=int, default=0, choices=(0, 1, 2),
+                    help="chain groups of the workload's sampler runs (0: the library's choice)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-budget", type=float, default=20.0)
     ap.add_argument("--calibrate-mfma", action="store_true",
@@ -641,16 +675,18 @@ def main():
     from paper_2606_13426_amd import _lib as lib
     lib.load()
     assert torch.cuda.is_available(), "bench.py needs a GPU"
-    res = run_sampler_bench(lib, args.workload, lib.SD_BLOCK, args.steps, args.warmup, profile=True)
+    res = run_sampler_bench(lib, args.workload, lib.SD_BLOCK, args.steps, args.warmup, profile=True,
+                            groups_req=args.groups_req)
     roof, table = roofline_of(res, args.steps)
     if roof:
         roof["traffic"] = measured_traffic(args.workload, roof["kernel"])
+        roof["chain_groups"] = res["profile_groups"]
     line = dict(metric=METRIC, value=res["B"] * res["N"] / res["sec"], unit="chain-steps/s", n_gpus=1,
                 steps=args.steps, warmup=args.warmup, ms_per_step=1e3 * res["sec"], higher_is_better=True,
                 scaling="weak", vs_baseline=None, dtype=_dtype(args.workload), data="synthetic",
                 config=dict(workload=args.workload, d=res["d"], M=res["M"], B=res["B"], K=res["K"],
                             N=res["N"], verification="block", drafter="free", usample="exact",
-                            parallelism="single-gpu"),
+                            chain_groups=res["groups"], parallelism="single-gpu"),
                 precision=_precision(args.workload),
                 mean_accepted_steps_per_block=res["be"], mean_tau=res["mean_tau"], ties=res["ties"],
                 rounds_per_run=res["rounds"], roofline=roof, kernels=table)
@@ -665,11 +701,13 @@ def main():
             roof2, table2 = roofline_of(r2, max(3, args.steps // 2))
             if roof2:
                 roof2["traffic"] = measured_traffic(wl, roof2["kernel"])
+                roof2["chain_groups"] = r2["profile_groups"]
             others[wl] = dict(value=r2["B"] * r2["N"] / r2["sec"], unit="chain-steps/s",
                               ms_per_step=1e3 * r2["sec"], dtype=_dtype(wl),
                               mean_accepted_steps_per_block=r2["be"], rounds_per_run=r2["rounds"],
                               ties=r2["ties"],
-                              config=dict(d=r2["d"], M=r2["M"], B=r2["B"], K=r2["K"], N=r2["N"]),
+                              config=dict(d=r2["d"], M=r2["M"], B=r2["B"], K=r2["K"], N=r2["N"],
+                                          chain_groups=r2["groups"]),
                               roofline=roof2, denoiser_gemms=table2.get("denoiser_gemms"),
                               kernels={k: dict(avg_us=v["avg_us"], bound=v.get("bound"), frac=v.get("frac"))
                                        for k, v in table2.items() if "avg_us" in v})

@@ -272,6 +272,7 @@ typedef struct {
                            decisions another rounding may flip               */
   double mean_tau;      /* sum of tau over chain-rounds / chain_rounds        */
   int32_t finished;     /* 1 when every chain has reached step N              */
+  int32_t groups;       /* chain groups this call ran (sd_sampler_options)    */
   int64_t tau_hist[SD_MAX_BLOCK + 2]; /* tau_hist[t] = number of chain-rounds with tau = t */
 } sd_stats;
 

@@ -36,7 +36,7 @@ class sd_stride(ctypes.Structure):
 class sd_stats(ctypes.Structure):
     _fields_ = [("rounds", c_int64), ("chain_rounds", c_int64), ("steps", c_int64),
                 ("ties", c_int64), ("mean_tau", c_double), ("finished", c_int32),
-                ("tau_hist", c_int64 * (SD_MAX_BLOCK + 2))]
+                ("groups", c_int32), ("tau_hist", c_int64 * (SD_MAX_BLOCK + 2))]
 
 
 class sd_sampler_options(ctypes.Structure):
@@ -298,7 +298,7 @@ def sd_sampler_workspace(target, B, K):
 
 def _stats_dict(st):
     return dict(rounds=st.rounds, chain_rounds=st.chain_rounds, steps=st.steps, ties=st.ties,
-                mean_tau=st.mean_tau, finished=bool(st.finished),
+                mean_tau=st.mean_tau, finished=bool(st.finished), groups=st.groups,
                 tau_hist=[st.tau_hist[i] for i in range(SD_MAX_BLOCK + 2)])
 
 

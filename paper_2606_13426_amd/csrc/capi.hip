@@ -993,6 +993,7 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
         memset(stats, 0, sizeof(*stats));
         stats->rounds = rounds;
         stats->finished = finished ? 1 : 0;
+        stats->groups = G;
         double tau_sum = 0.0;
         for (int b = 0; b < B; ++b) {
           stats->steps += h_steps[b];
