@@ -18,7 +18,8 @@
  *    caller buffers, including a caller workspace sized by the *_workspace query.
  *    sd_target_create also allocates 1 KB of mapped pinned host memory: the
  *    words through which a running sampler call learns, round by round,
- *    whether any chain is still active (up to 64 calls at once per target).
+ *    whether any chain is still active: 64 slots per target, one per running
+ *    call and chain group (SD_EUNSUPPORTED beyond that).
  *    A sampler call that runs two chain groups (sd_sampler_options.groups)
  *    creates one HIP stream the first time it uses a given slot of those
  *    words; the target keeps it until sd_target_destroy.

@@ -812,7 +812,8 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
   int64_t rounds = -1;
   Clock::time_point last_progress = Clock::now();
   int r = start;
-  auto enqueue = [&](const GroupRun& q, int cur, int nxt) -> hipError_t {
+  auto enqueue = [&](int g, int cur, int nxt) -> hipError_t {
+    const GroupRun& q = gr[g];
     const int b0 = q.c0, nb = q.nb;
     const int64_t rows0 = (int64_t)b0 * K1;
     float *xg = x + rows0 * d, *mqg = mq + rows0 * d, *svg = sv + (int64_t)b0 * d,
@@ -821,8 +822,8 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
     double *sigmag = sigma + rows0, *lrpg = lrp + rows0 * L.nct * 3;
     const int32_t *kc = k2 + cur * B + b0, *crc = crow2 + cur * B + b0, *csc = cstep2 + cur * B + b0;
     const uint32_t* rc = rnd2 + cur * B + b0;
-    const int* gate = act + 2 * (&q - gr) + cur;
-    int* next = act + 2 * (&q - gr) + nxt;
+    const int* gate = act + 2 * g + cur;
+    int* next = act + 2 * g + nxt;
     hipError_t e = hipSuccess;
     if (frozen) {
       // the Frozen Drafter's target call at (Y_k, k) into row 0 of m^q (the
@@ -860,7 +861,7 @@ sd_status sd_run_sampler_ex(sd_target target, int32_t B, int32_t K,
   for (; r < end && rounds < 0; ++r) {
     const int cur = r & 1, nxt = cur ^ 1;
     hipError_t e = hipSuccess;
-    for (int g = 0; g < G && e == hipSuccess; ++g) e = enqueue(gr[g], cur, nxt);
+    for (int g = 0; g < G && e == hipSuccess; ++g) e = enqueue(g, cur, nxt);
     if (e != hipSuccess) {
       set_error("sd_run_sampler: launch failed in round %d: %s", r, hipGetErrorString(e));
       st = SD_EHIP;
