@@ -50,6 +50,8 @@ MEASURED_TRAFFIC = {
                                        sources="1d9832fb95c336178846c2f8d069c8aad7d8558d"),
     ("latent16384", "gmm_mean_lr_bf16"): dict(bytes=(277.7 + 154.0) * 1e6, unit="gmm_bf16.hip",
                                               sources="bc618f4030c65b9b569657e8f3ca128e666ddf1e"),
+    ("pixel12288", "gmm_mean_lr_bf16"): dict(bytes=(511.7 + 445.9) * 1e6, unit="gmm_bf16.hip",
+                                             sources="bc618f4030c65b9b569657e8f3ca128e666ddf1e"),
 }
 
 
