@@ -63,6 +63,7 @@ def test_two_groups_equal_one(case):
     two = _lib.sd_run_sampler_ex(tgt, B, K, 11, trace_rounds=N, groups=2, **kw)
     torch.cuda.synchronize()
     assert one[1]["finished"] and one[1]["steps"] == B * N
+    assert one[1]["groups"] == 1 and two[1]["groups"] == 2
     _same(one, two)
 
 
@@ -82,6 +83,29 @@ def test_split_run_changing_groups_equals_one_call():
                                           groups=2)
     torch.cuda.synchronize()
     _same(one, (y, st, trace))
+
+
+def test_init_only_then_resume_with_two_groups():
+    # max_rounds = 0 initialises the state only; the run resumed from it with
+    # two groups equals one call with one group
+    tgt, B, K, N, kw = _target(((128, 64), 20, 4, 30, None, {}))
+    one = _lib.sd_run_sampler_ex(tgt, B, K, 7, trace_rounds=N, groups=1)
+    ws = torch.empty(_lib.sd_sampler_workspace(tgt, B, K), dtype=torch.uint8, device="cuda")
+    trace = torch.zeros(N, B, dtype=torch.int32, device="cuda")
+    _, st, _ = _lib.sd_run_sampler_ex(tgt, B, K, 7, ws=ws, trace=trace, max_rounds=0, groups=2)
+    assert st["rounds"] == 0 and not st["finished"]
+    two = _lib.sd_run_sampler_ex(tgt, B, K, 7, ws=ws, trace=trace, start_round=st["rounds"], groups=2)
+    torch.cuda.synchronize()
+    _same(one, two)
+
+
+def test_library_choice_of_groups():
+    # two groups from 2048 target rows per half (B/2 (K + 1)), else one
+    p = make_gmm(64, 8, mu_std=1.0, var=(0.01, 0.2), dirichlet=1.0, seed=1)
+    tgt = _lib.Target(_lib.schedule(6), p["mu"], p["var"], p["log_w"])
+    for B, K, want in ((455, 8, 1), (456, 8, 2), (1, 8, 1)):
+        _, st, _ = _lib.sd_run_sampler_ex(tgt, B, K, 0)
+        assert st["groups"] == want, (B, K, st["groups"])
 
 
 def test_groups_out_of_range_rejected():
