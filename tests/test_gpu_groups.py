@@ -7,9 +7,12 @@ generator is keyed by the chain's index in the whole batch).
 
 Cases: float32 and bf16 targets, the three sampler modes, K > N, an odd number
 of chains, the chain-aligned bf16 mean tile (M >= 512) and the 128-row one,
-both bf16 workloads at full size, and a run split over calls that changes the
-grouping between calls.
+both bf16 workloads at full size, a run split over calls that changes the
+grouping between calls, and concurrent calls from several host threads on one
+target.
 """
+import threading
+
 import pytest
 import torch
 
@@ -106,6 +109,36 @@ def test_library_choice_of_groups():
     for B, K, want in ((455, 8, 1), (456, 8, 2), (1, 8, 1)):
         _, st, _ = _lib.sd_run_sampler_ex(tgt, B, K, 0)
         assert st["groups"] == want, (B, K, st["groups"])
+
+
+def test_concurrent_calls_on_one_target():
+    # three host threads, each on its own stream, share one target (its flag
+    # slots and second-group streams): each run equals the same run alone
+    tgt, B, K, N, _ = _target(((512, 64), 40, 4, 40, None, {}))
+    jobs = ((1, 2), (2, 1), (3, 2))
+    ref = [_lib.sd_run_sampler_ex(tgt, B, K, seed, trace_rounds=N, groups=g) for seed, g in jobs]
+    torch.cuda.synchronize()
+    out, errors = [None] * len(jobs), []
+
+    def work(i, seed, g):
+        try:
+            stream = torch.cuda.Stream()
+            with torch.cuda.stream(stream):
+                out[i] = _lib.sd_run_sampler_ex(tgt, B, K, seed, trace_rounds=N, groups=g)
+            stream.synchronize()
+        except Exception as e:  # re-raised in the main thread
+            errors.append(e)
+
+    threads = [threading.Thread(target=work, args=(i, seed, g)) for i, (seed, g) in enumerate(jobs)]
+    for th in threads:
+        th.start()
+    for th in threads:
+        th.join(timeout=120)
+    assert not any(th.is_alive() for th in threads)
+    if errors:
+        raise errors[0]
+    for a, b in zip(ref, out):
+        _same(a, b)
 
 
 def test_groups_out_of_range_rejected():
