@@ -674,7 +674,7 @@ def main():
         return
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}): chains are independent and "
-              "would shard across GPUs without communication, but multi-GPU runs are not part of this build",
+              "would shard across GPUs without communication, but multi-GPU runs are not implemented",
               file=sys.stderr)
         sys.exit(2)
     import torch

@@ -56,7 +56,7 @@ typedef enum {
   SD_OK = 0,
   SD_EINVAL = -1,       /* invalid argument (checked before any HIP call)    */
   SD_EHIP = -2,         /* a HIP runtime call failed                          */
-  SD_EUNSUPPORTED = -3, /* valid but not supported by this build              */
+  SD_EUNSUPPORTED = -3, /* valid but not supported by the library            */
   SD_ENOMEM = -4,       /* device allocation failed (sd_target_create only)   */
   SD_ENUMERIC = -5      /* a non-finite value was met (sd_run_sampler)        */
 } sd_status;
