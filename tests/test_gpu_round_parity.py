@@ -19,6 +19,8 @@ holds the comparison rules.
   lockstep for block/Free, token/reflection and block/Frozen: 32 chains every
   round stage-wise and, in turn, every fourth round of each against the
   oracle's own round from the GPU's state.
+* Temperature: pixel3072 at full size at omega = 2 (block/Free) and a whole
+  bf16 run on the chain-aligned tile at omega = 0.5 (token/reflection).
 * A run split over calls equals one call; the device's tie counts equal the
   oracle's.
 """
@@ -118,7 +120,7 @@ def test_bf16_fused_round_stagewise(name, B, nsel):
 
 
 def _lockstep(mode, residual, drafter, name="pixel3072", B=None, N=None, K=None, M=None, d=None,
-              nchains=32, seed=0, every=4, precision=None):
+              nchains=32, seed=0, every=4, precision=None, omega=1.0):
     """Run the sampler a round per call and check `nchains` chains every round
     stage-wise; with every > 0 also, in turn, every `every`-th round of each
     against the oracle's own round (float32 targets only)."""
@@ -134,7 +136,7 @@ def _lockstep(mode, residual, drafter, name="pixel3072", B=None, N=None, K=None,
     g = GMM(p["mu"], p["var"], p["log_w"])
     sch = Schedule(N)
     om = _MODES[(mode, residual, drafter)]
-    kw = dict(mode=mode, residual=residual, drafter=drafter, ws=ws, trace=trace)
+    kw = dict(mode=mode, residual=residual, drafter=drafter, ws=ws, trace=trace, omega=omega)
     _, st, _ = _lib.sd_run_sampler_ex(tgt, B, K, seed, max_rounds=0, **kw)
     assert st["rounds"] == 0
     stats = RoundStats()
@@ -149,7 +151,7 @@ def _lockstep(mode, residual, drafter, name="pixel3072", B=None, N=None, K=None,
         active = 0
         for i, b in enumerate(chains):
             active += check_round(g, sch, K, seed, i, int(b), before, after, stats, *om,
-                                  independent=every > 0 and (r + i) % every == 0)
+                                  independent=every > 0 and (r + i) % every == 0, omega=omega)
         before = after
         r += 1
         if st["finished"]:
@@ -186,6 +188,22 @@ def test_bf16_chain_aligned_tile_lockstep(mode, residual, drafter):
     assert stats.compared >= 24 * (60 // 9) and stats.independent == 0
     assert stats.ties <= max(3, stats.compared // 200), stats.ties
     print(f"bf16 lockstep: {stats.compared} chain-rounds, ties {stats.ties}, worst {stats.worst}")
+
+
+def test_tempered_lockstep():
+    # temperature (App. "Temperature"): pixel3072 at full size, block/Free at
+    # omega = 2, in lockstep as above; and a whole bf16 run on the
+    # chain-aligned tile, token/reflection at omega = 0.5, stage-wise
+    stats, _ = _lockstep(_lib.SD_BLOCK, _lib.SD_RESIDUAL_DECOMPOSITION, _lib.SD_DRAFTER_FREE, omega=2.0,
+                         nchains=32, seed=2)
+    assert stats.compared >= 32 * (200 // 9)
+    assert stats.f32_flips <= max(2, stats.independent // 500), stats.f32_flips
+    assert stats.ties <= max(3, stats.compared // 200), stats.ties
+    b16, _ = _lockstep(_lib.SD_TOKEN, _lib.SD_RESIDUAL_REFLECTION, _lib.SD_DRAFTER_FREE, B=72, N=60, K=8,
+                       M=512, d=1024, nchains=24, seed=3, every=0, precision=_lib.SD_BF16, omega=0.5)
+    assert b16.compared >= 24 * (60 // 9) and b16.ties <= max(3, b16.compared // 200), b16.ties
+    print(f"tempered lockstep: {stats.compared} / {b16.compared} chain-rounds, ties {stats.ties} / {b16.ties}, "
+          f"worst {stats.worst}")
 
 
 def test_streamed_draft_rows_lockstep():
