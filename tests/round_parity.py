@@ -103,7 +103,8 @@ def _close_scalar(got, want, rtol, what):
 
 
 def check_round(gmm, sched, K, seed, i, b, before, after, stats, mode=osamp.BLOCK,
-                residual=osamp.DECOMPOSITION, drafter=osamp.FREE, independent=False, omega=1.0):
+                residual=osamp.DECOMPOSITION, drafter=osamp.FREE, independent=False, omega=1.0,
+                usample=USAMPLE_EXACT):
     """Compare chain b (index i of the snapshots) over the round between `before`
     and `after` (see the module docstring).  Returns False for an inactive chain."""
     N = sched.n_steps
@@ -126,7 +127,7 @@ def check_round(gmm, sched, K, seed, i, b, before, after, stats, mode=osamp.BLOC
     mq = after["mq"][i]
     sig = sched.sigma(k + np.arange(kb + 1))
     # ---- stage-wise: the oracle fed the GPU's float32 inputs
-    v = osamp.verify_chain(drafts[1:], mp, mq, sig, kb, seed, b, rnd, mode, USAMPLE_EXACT, omega)
+    v = osamp.verify_chain(drafts[1:], mp, mq, sig, kb, seed, b, rnd, mode, usample, omega)
     lrp = after["lrp"][i][:kb]
     s2 = lrp[:, :, 0].sum(axis=1)
     sz = lrp[:, :, 1].sum(axis=1)
@@ -170,7 +171,7 @@ def check_round(gmm, sched, K, seed, i, b, before, after, stats, mode=osamp.BLOC
     c2c = float(sched.c2(int(before["cache_step"][i])))
     score_c = before["cache"][i].astype(F64) / c2c
     y_new, score_new, k_new, info = osamp.run_round(gmm, sched, K, y0, score_c, k, rnd, seed, b, mode,
-                                                    USAMPLE_EXACT, residual, drafter, omega)
+                                                    usample, residual, drafter, omega)
     stats.note("drafts", assert_rows_close(drafts[1:], info["yh"][1:], what=f"drafts chain {b} round {rnd}"))
     nrows = info["mq"].shape[0]
     stats.note("m^q", assert_rows_close(mq[:nrows], info["mq"], what=f"m^q chain {b} round {rnd}"))

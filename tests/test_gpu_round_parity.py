@@ -21,6 +21,8 @@ holds the comparison rules.
   oracle's own round from the GPU's state.
 * Temperature: pixel3072 at full size at omega = 2 (block/Free) and a whole
   bf16 run on the chain-aligned tile at omega = 0.5 (token/reflection).
+* The U draw with the paper's caps (Alg. 7 as run in its experiments) on a
+  pixel3072-shaped run.
 * A run split over calls equals one call; the device's tie counts equal the
   oracle's.
 """
@@ -120,7 +122,7 @@ def test_bf16_fused_round_stagewise(name, B, nsel):
 
 
 def _lockstep(mode, residual, drafter, name="pixel3072", B=None, N=None, K=None, M=None, d=None,
-              nchains=32, seed=0, every=4, precision=None, omega=1.0):
+              nchains=32, seed=0, every=4, precision=None, omega=1.0, usample=_lib.SD_USAMPLE_EXACT):
     """Run the sampler a round per call and check `nchains` chains every round
     stage-wise; with every > 0 also, in turn, every `every`-th round of each
     against the oracle's own round (float32 targets only)."""
@@ -136,7 +138,8 @@ def _lockstep(mode, residual, drafter, name="pixel3072", B=None, N=None, K=None,
     g = GMM(p["mu"], p["var"], p["log_w"])
     sch = Schedule(N)
     om = _MODES[(mode, residual, drafter)]
-    kw = dict(mode=mode, residual=residual, drafter=drafter, ws=ws, trace=trace, omega=omega)
+    kw = dict(mode=mode, residual=residual, drafter=drafter, ws=ws, trace=trace, omega=omega,
+              usample_mode=usample)
     _, st, _ = _lib.sd_run_sampler_ex(tgt, B, K, seed, max_rounds=0, **kw)
     assert st["rounds"] == 0
     stats = RoundStats()
@@ -151,7 +154,8 @@ def _lockstep(mode, residual, drafter, name="pixel3072", B=None, N=None, K=None,
         active = 0
         for i, b in enumerate(chains):
             active += check_round(g, sch, K, seed, i, int(b), before, after, stats, *om,
-                                  independent=every > 0 and (r + i) % every == 0, omega=omega)
+                                  independent=every > 0 and (r + i) % every == 0, omega=omega,
+                                  usample=usample)
         before = after
         r += 1
         if st["finished"]:
@@ -204,6 +208,17 @@ def test_tempered_lockstep():
     assert b16.compared >= 24 * (60 // 9) and b16.ties <= max(3, b16.compared // 200), b16.ties
     print(f"tempered lockstep: {stats.compared} / {b16.compared} chain-rounds, ties {stats.ties} / {b16.ties}, "
           f"worst {stats.worst}")
+
+
+def test_paper_usample_lockstep():
+    # the U draw with the paper's caps (Alg. 7: three doublings, four
+    # bisections, tolerance 1e-6) inside the sampler: 24 chains of a
+    # pixel3072-shaped run every round, every second one also against the
+    # oracle's own round
+    stats, _ = _lockstep(_lib.SD_BLOCK, _lib.SD_RESIDUAL_DECOMPOSITION, _lib.SD_DRAFTER_FREE, B=256, N=60,
+                         nchains=24, seed=5, every=2, usample=_lib.SD_USAMPLE_PAPER)
+    assert stats.compared >= 24 * (60 // 9) and stats.f32_flips <= 2
+    assert stats.ties <= max(3, stats.compared // 200), stats.ties
 
 
 def test_streamed_draft_rows_lockstep():
